@@ -1,0 +1,522 @@
+/*
+ * Plain CPU oracle of the batched class/depth view rasterizer.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the
+ * CPU-baseline leg of the benchmark load this library.  It shares no code,
+ * header, table or constant generator with the HIP library: it is written
+ * from the rasterization rules below, never from the kernels.
+ *
+ * What it computes (paper Sec. 3.2, Eq. obs_pv): for every agent i and camera
+ * k of its rig, a deterministic image Phi(A_i, W_i, K_ik) of the surrounding
+ * agents' boxes and the static map geometry seen through a pinhole camera
+ * with the configured intrinsics and extrinsics; the ego's own body is not
+ * drawn ("only the surroundings are rendered").  The paper draws flat-shaded
+ * RGB; this path draws, per pixel, the semantic class of the visible surface
+ * and its view-space depth.  The paper gives no rasterization internals, so
+ * the rules are fixed here (and identically, in separate code, on the GPU):
+ *
+ *  R1 camera   C = agent + Rot(heading) * mount.xy, Cz = z0 + mount.z;
+ *              camera heading (cc, sc) = heading (+) mount yaw, as
+ *              cc = c*cm - s*sm, sc = s*cm + c*sm (fp32, no contraction).
+ *              forward f = (cc, sc, 0), right r = (sc, -cc, 0), up (0, 0, 1)
+ *              (ego frame x forward, y left, z up; App. A.2 Tab. camera_rig).
+ *  R2 view     d = P - C;  xv = d.x*sc - d.y*cc;  yv = d.z;  zv = d.x*cc + d.y*sc.
+ *  R3 depth    plane of the unsnapped triangle: N = (V1-V0) x (V2-V0) in world
+ *              space, n_view = (N.x*sc - N.y*cc, N.z, N.x*cc + N.y*sc),
+ *              delta = N . (V0 - C); delta == 0 drops the triangle.  With
+ *              rd = 1/delta:  pa = (nx*rd)*(1/fx), pb = -(ny*rd)*(1/fy),
+ *              pc = nz*rd, and at pixel (i, j):
+ *              iz = fma(pa, i+0.5-cx, fma(pb, j+0.5-cy, pc))   (= 1/zv).
+ *  R4 near     Sutherland-Hodgman against zv >= near, edges v0v1, v1v2, v2v0;
+ *              each crossing point is computed from the inside vertex I
+ *              towards the outside vertex O: t = (near - I.z)/(O.z - I.z),
+ *              x = fma(t, O.x - I.x, I.x), y likewise, z = near; the 3- or
+ *              4-gon is fanned from its first vertex.
+ *  R5 snap     rz = 1/zv;  X = rint(256cx + 256fx*(xv*rz)),
+ *              Y = rint(256cy - 256fy*(yv*rz))   (8-bit subpixel, ties to
+ *              even); a coordinate with |value| > 2^29 (or NaN) drops the
+ *              triangle.
+ *  R6 fill     integer edge functions E_ab(p) = (b.x-a.x)(p.y-a.y) -
+ *              (b.y-a.y)(p.x-a.x) at pixel centres p = (256i+128, 256j+128);
+ *              area2 = E_01(v2): 0 drops, < 0 swaps v1 and v2 (two-sided).
+ *              Edge a->b is top-left iff dy < 0 or (dy == 0 and dx > 0)
+ *              (y grows downwards).  Covered iff every edge has E > 0, or
+ *              E == 0 and the edge is top-left.
+ *  R7 key      iz < 1/far (or NaN) rejects the pixel; iz = min(iz, IZCAP)
+ *              with IZCAP the smallest power of two >= 1/near;
+ *              q = (bits(IZCAP) >> 3) - (bits(iz) >> 3)  (24-bit reverse
+ *              depth, monotone in z, relative step 2^-20);
+ *              key = (q << 8) | class; the pixel keeps the minimum key, so
+ *              the nearest surface wins and an exact depth tie goes to the
+ *              lower class ID, whatever the triangle order.
+ *  R8 resolve  class = key & 255; depth = +inf when q == 0xFFFFFF (the clear
+ *              key carries the sky class 4), else
+ *              1 / float_from_bits(((bits(IZCAP) >> 3) - q) << 3 | 4).
+ *  R9 boxes    corners (x + (a*c - b*s), y + (a*s + b*c), z0 or z0 + H) with
+ *              a = +-L/2, b = +-W/2; 12 triangles (two per face).
+ *
+ * Arithmetic is IEEE fp32 with round-to-nearest and no contraction (this
+ * file must be compiled with -ffp-contract=off and without -ffast-math);
+ * fmaf() appears only where the rules name fma.  Integer edge functions are
+ * exact in int64.
+ *
+ * Per pixel the oracle also reports parity flags:
+ *   bit 0 EDGE  the pixel centre lies within 1e-4 px of an edge of a triangle
+ *               whose key there is <= the winning key (a coverage decision
+ *               that a one-quantum snap difference could flip);
+ *   bit 1 TIE   the best surface of a different class is within 1e-4
+ *               relative depth of the winner.
+ * and, optionally, how many raster triangles cover the pixel (watertightness).
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+#ifdef _OPENMP
+#include <omp.h>
+#endif
+
+#define SKY_CLASS 4u
+#define CLEAR_KEY ((0xFFFFFFu << 8) | SKY_CLASS)
+
+static uint32_t f2u(float f) { uint32_t u; memcpy(&u, &f, 4); return u; }
+static float u2f(uint32_t u) { float f; memcpy(&f, &u, 4); return f; }
+
+/* smallest power of two >= x (x > 0, normal) */
+static float pow2_ceil(float x)
+{
+    uint32_t u = f2u(x);
+    if ((u & 0x7FFFFFu) == 0) return x;
+    return u2f((u & 0x7F800000u) + 0x00800000u);
+}
+
+typedef struct {
+    float cx_, cy_, cz_;   /* camera position */
+    float cc, sc;          /* camera heading */
+} Cam;
+
+typedef struct {
+    int W, H;
+    float fx, fy, cx, cy, nearp, farp;
+    float fx256, fy256, cx256, cy256, rfx, rfy;
+    float izfar, izcap;
+    uint32_t qbase;
+} Params;
+
+typedef struct { float x, y, z; } V3;
+
+static V3 to_view(const Cam* c, float px, float py, float pz)
+{
+    float dx = px - c->cx_, dy = py - c->cy_, dz = pz - c->cz_;
+    V3 v;
+    float a = dx * c->sc, b = dy * c->cc;
+    v.x = a - b;
+    v.y = dz;
+    float e = dx * c->cc, f = dy * c->sc;
+    v.z = e + f;
+    return v;
+}
+
+/* R3: depth plane from the world-space triangle.  Returns 0 if dropped. */
+static int depth_plane(const Cam* c, const Params* P, const float* t /*9*/,
+                       float* pa, float* pb, float* pc)
+{
+    float e1x = t[3] - t[0], e1y = t[4] - t[1], e1z = t[5] - t[2];
+    float e2x = t[6] - t[0], e2y = t[7] - t[1], e2z = t[8] - t[2];
+    float Nx = e1y * e2z - e1z * e2y;
+    float Ny = e1z * e2x - e1x * e2z;
+    float Nz = e1x * e2y - e1y * e2x;
+    float d0x = t[0] - c->cx_, d0y = t[1] - c->cy_, d0z = t[2] - c->cz_;
+    float nx = Nx * c->sc - Ny * c->cc;
+    float ny = Nz;
+    float nz = Nx * c->cc + Ny * c->sc;
+    float delta = (Nx * d0x + Ny * d0y) + Nz * d0z;
+    if (delta == 0.0f || !isfinite(delta)) return 0;
+    float rd = 1.0f / delta;
+    *pa = (nx * rd) * P->rfx;
+    *pb = -((ny * rd) * P->rfy);
+    *pc = nz * rd;
+    return 1;
+}
+
+typedef struct {
+    uint32_t* key;      /* [H*W] min key */
+    uint32_t* edge_key; /* [H*W] min key of fragile coverage decisions */
+    uint32_t* k1;       /* best key */
+    uint32_t* k2;       /* best key of a class different from k1's */
+    uint16_t* cover;    /* optional coverage count */
+} Frame;
+
+static void frame_update_tie(Frame* F, int p, uint32_t k)
+{
+    uint32_t c = k & 255u;
+    uint32_t k1 = F->k1[p], k2 = F->k2[p];
+    if (c == (k1 & 255u)) {
+        if (k < k1) F->k1[p] = k;
+    } else if (k < k1) {
+        F->k2[p] = k1;
+        F->k1[p] = k;
+    } else if (c == (k2 & 255u)) {
+        if (k < k2) F->k2[p] = k;
+    } else if (k < k2) {
+        F->k2[p] = k;
+    }
+}
+
+static int snap(const Params* P, V3 v, int32_t* X, int32_t* Y)
+{
+    float rz = 1.0f / v.z;
+    float qx = v.x * rz, qy = v.y * rz;
+    float mx = P->fx256 * qx, my = P->fy256 * qy;
+    float sx = P->cx256 + mx, sy = P->cy256 - my;
+    float rx = rintf(sx), ry = rintf(sy);
+    if (!(fabsf(rx) <= 536870912.0f) || !(fabsf(ry) <= 536870912.0f)) return 0;
+    *X = (int32_t)rx;
+    *Y = (int32_t)ry;
+    return 1;
+}
+
+static int64_t floor_div256(int64_t a) { return a >= 0 ? a / 256 : -((-a + 255) / 256); }
+
+/* Rasterize one snapped triangle (R6, R7) into the frame. */
+static void raster_tri(const Params* P, Frame* F, int32_t X0, int32_t Y0, int32_t X1, int32_t Y1,
+                       int32_t X2, int32_t Y2, float pa, float pb, float pc, uint32_t cls)
+{
+    int64_t area2 = (int64_t)(X1 - X0) * (int64_t)(Y2 - Y0) - (int64_t)(Y1 - Y0) * (int64_t)(X2 - X0);
+    if (area2 == 0) return;
+    if (area2 < 0) {
+        int32_t tx = X1, ty = Y1;
+        X1 = X2; Y1 = Y2; X2 = tx; Y2 = ty;
+    }
+    int32_t ax[3] = {X1, X2, X0}, ay[3] = {Y1, Y2, Y0};
+    int32_t bx[3] = {X2, X0, X1}, by[3] = {Y2, Y0, Y1};
+    int tl[3];
+    double band[3];
+    for (int e = 0; e < 3; ++e) {
+        int64_t dx = (int64_t)bx[e] - ax[e], dy = (int64_t)by[e] - ay[e];
+        tl[e] = (dy < 0) || (dy == 0 && dx > 0);
+        band[e] = 0.0256 * sqrt((double)dx * (double)dx + (double)dy * (double)dy);
+    }
+    int32_t minX = X0 < X1 ? (X0 < X2 ? X0 : X2) : (X1 < X2 ? X1 : X2);
+    int32_t maxX = X0 > X1 ? (X0 > X2 ? X0 : X2) : (X1 > X2 ? X1 : X2);
+    int32_t minY = Y0 < Y1 ? (Y0 < Y2 ? Y0 : Y2) : (Y1 < Y2 ? Y1 : Y2);
+    int32_t maxY = Y0 > Y1 ? (Y0 > Y2 ? Y0 : Y2) : (Y1 > Y2 ? Y1 : Y2);
+    int64_t i0 = floor_div256((int64_t)minX - 128 + 255), i1 = floor_div256((int64_t)maxX - 128);
+    int64_t j0 = floor_div256((int64_t)minY - 128 + 255), j1 = floor_div256((int64_t)maxY - 128);
+    if (i0 < 0) i0 = 0;
+    if (j0 < 0) j0 = 0;
+    if (i1 > P->W - 1) i1 = P->W - 1;
+    if (j1 > P->H - 1) j1 = P->H - 1;
+    for (int64_t j = j0; j <= j1; ++j) {
+        int64_t py = 256 * j + 128;
+        float pyf = ((float)j + 0.5f) - P->cy;
+        for (int64_t i = i0; i <= i1; ++i) {
+            int64_t px = 256 * i + 128;
+            int covered = 1, near_edge = 0, in_band = 1;
+            for (int e = 0; e < 3; ++e) {
+                int64_t E = ((int64_t)bx[e] - ax[e]) * (py - ay[e]) - ((int64_t)by[e] - ay[e]) * (px - ax[e]);
+                if (!(E > 0 || (E == 0 && tl[e]))) covered = 0;
+                double Ed = (double)E;
+                if (fabs(Ed) <= band[e]) near_edge = 1;
+                if (Ed < -band[e]) in_band = 0;
+            }
+            if (!covered && !(near_edge && in_band)) continue;
+            float pxf = ((float)i + 0.5f) - P->cx;
+            float iz = fmaf(pa, pxf, fmaf(pb, pyf, pc));
+            if (!(iz >= P->izfar)) continue;
+            if (iz > P->izcap) iz = P->izcap;
+            uint32_t q = P->qbase - (f2u(iz) >> 3);
+            uint32_t key = (q << 8) | cls;
+            int p = (int)(j * P->W + i);
+            if (near_edge && in_band && key < F->edge_key[p] + 0u) {
+                if (key < F->edge_key[p]) F->edge_key[p] = key;
+            }
+            if (covered) {
+                if (key < F->key[p]) F->key[p] = key;
+                frame_update_tie(F, p, key);
+                if (F->cover) F->cover[p]++;
+            }
+        }
+    }
+}
+
+/* One world-space triangle through R2..R7. */
+static void draw_triangle(const Params* P, const Cam* cam, Frame* F, const float* t, uint32_t cls)
+{
+    V3 v[3];
+    for (int k = 0; k < 3; ++k) v[k] = to_view(cam, t[3 * k], t[3 * k + 1], t[3 * k + 2]);
+    int in[3];
+    int nin = 0;
+    for (int k = 0; k < 3; ++k) { in[k] = v[k].z >= P->nearp; nin += in[k]; }
+    if (nin == 0) return;
+    float pa, pb, pc;
+    if (!depth_plane(cam, P, t, &pa, &pb, &pc)) return;
+    V3 poly[4];
+    int np = 0;
+    if (nin == 3) {
+        poly[0] = v[0]; poly[1] = v[1]; poly[2] = v[2]; np = 3;
+    } else {
+        for (int k = 0; k < 3; ++k) {
+            V3 A = v[k], B = v[(k + 1) % 3];
+            int ia = in[k], ib = in[(k + 1) % 3];
+            if (ia) poly[np++] = A;
+            if (ia != ib) {
+                V3 I = ia ? A : B, O = ia ? B : A;
+                float t_ = (P->nearp - I.z) / (O.z - I.z);
+                V3 X;
+                X.x = fmaf(t_, O.x - I.x, I.x);
+                X.y = fmaf(t_, O.y - I.y, I.y);
+                X.z = P->nearp;
+                poly[np++] = X;
+            }
+        }
+    }
+    int32_t SX[4], SY[4];
+    for (int k = 0; k < np; ++k)
+        if (!snap(P, poly[k], &SX[k], &SY[k])) return;
+    for (int f = 1; f + 1 < np; ++f)
+        raster_tri(P, F, SX[0], SY[0], SX[f], SY[f], SX[f + 1], SY[f + 1], pa, pb, pc, cls);
+}
+
+static const int BOX_TRIS[12][3] = {
+    {0, 1, 3}, {0, 3, 2},   /* bottom */
+    {4, 5, 7}, {4, 7, 6},   /* top */
+    {0, 2, 6}, {0, 6, 4},   /* back  (a = -L/2) */
+    {1, 3, 7}, {1, 7, 5},   /* front (a = +L/2) */
+    {0, 1, 5}, {0, 5, 4},   /* right (b = -W/2) */
+    {2, 3, 7}, {2, 7, 6},   /* left  (b = +W/2) */
+};
+
+static void box_corners(float x, float y, float z0, float c, float s, float L, float Wd, float H, float out[8][3])
+{
+    float hl = 0.5f * L, hw = 0.5f * Wd;
+    for (int n = 0; n < 8; ++n) {
+        float a = (n & 1) ? hl : -hl;
+        float b = (n & 2) ? hw : -hw;
+        float ac = a * c, bs = b * s, as_ = a * s, bc = b * c;
+        float ox = ac - bs, oy = as_ + bc;
+        out[n][0] = x + ox;
+        out[n][1] = y + oy;
+        out[n][2] = (n & 4) ? (z0 + H) : z0;
+    }
+}
+
+static void init_params(Params* P, int W, int H, float fx, float fy, float cx, float cy, float nearp, float farp)
+{
+    P->W = W; P->H = H; P->fx = fx; P->fy = fy; P->cx = cx; P->cy = cy;
+    P->nearp = nearp; P->farp = farp;
+    P->fx256 = 256.0f * fx; P->fy256 = 256.0f * fy;
+    P->cx256 = 256.0f * cx; P->cy256 = 256.0f * cy;
+    P->rfx = 1.0f / fx; P->rfy = 1.0f / fy;
+    P->izfar = 1.0f / farp;
+    P->izcap = pow2_ceil(1.0f / nearp);
+    P->qbase = f2u(P->izcap) >> 3;
+}
+
+/* Camera of view v (R1). */
+static void make_cam(Cam* cam, int64_t g, const float* mount,
+                     const float* ax, const float* ay, const float* az0, const float* ac, const float* as_)
+{
+    float c = ac[g], s = as_[g];
+    float mx = mount[0], my = mount[1], mz = mount[2], cm = mount[3], sm = mount[4];
+    float t1 = mx * c, t2 = my * s, t3 = mx * s, t4 = my * c;
+    float ox = t1 - t2, oy = t3 + t4;
+    cam->cx_ = ax[g] + ox;
+    cam->cy_ = ay[g] + oy;
+    cam->cz_ = az0[g] + mz;
+    float u1 = c * cm, u2 = s * sm, u3 = s * cm, u4 = c * sm;
+    cam->cc = u1 - u2;
+    cam->sc = u3 + u4;
+}
+
+int oracle_render(int num_worlds, const int64_t* tri_offsets, const float* verts, const uint8_t* tcls,
+                  int agents_per_world, const float* ax, const float* ay, const float* az0,
+                  const float* acos, const float* asin, const float* alen, const float* awid,
+                  const float* ahgt, const uint8_t* acls,
+                  int num_cams, int W, int H, float fx, float fy, float cx, float cy,
+                  float nearp, float farp, const float* mount,
+                  int64_t num_sel, const int64_t* view_ids,
+                  uint8_t* out_cls, float* out_depth, uint8_t* out_flags, uint16_t* out_cover,
+                  int num_threads)
+{
+    Params P;
+    init_params(&P, W, H, fx, fy, cx, cy, nearp, farp);
+    const int64_t npx = (int64_t)W * H;
+    const int64_t per_world = (int64_t)agents_per_world * num_cams;
+    const int64_t total_views = per_world * num_worlds;
+    for (int64_t n = 0; n < num_sel; ++n)
+        if (view_ids[n] < 0 || view_ids[n] >= total_views) return -1;
+#ifdef _OPENMP
+    if (num_threads > 0) omp_set_num_threads(num_threads);
+#pragma omp parallel
+#endif
+    {
+        Frame F;
+        F.key = (uint32_t*)malloc(sizeof(uint32_t) * npx);
+        F.edge_key = (uint32_t*)malloc(sizeof(uint32_t) * npx);
+        F.k1 = (uint32_t*)malloc(sizeof(uint32_t) * npx);
+        F.k2 = (uint32_t*)malloc(sizeof(uint32_t) * npx);
+        F.cover = out_cover ? (uint16_t*)malloc(sizeof(uint16_t) * npx) : NULL;
+#ifdef _OPENMP
+#pragma omp for schedule(dynamic, 1)
+#endif
+        for (int64_t n = 0; n < num_sel; ++n) {
+            int64_t v = view_ids[n];
+            int64_t w = v / per_world;
+            int64_t a = (v / num_cams) % agents_per_world;
+            int64_t k = v % num_cams;
+            int64_t g = w * agents_per_world + a;
+            Cam cam;
+            make_cam(&cam, g, mount + 5 * k, ax, ay, az0, acos, asin);
+            for (int64_t p = 0; p < npx; ++p) {
+                F.key[p] = CLEAR_KEY;
+                F.edge_key[p] = 0xFFFFFFFFu;
+                F.k1[p] = CLEAR_KEY;
+                F.k2[p] = 0xFFFFFFFFu;
+                if (F.cover) F.cover[p] = 0;
+            }
+            for (int64_t t = tri_offsets[w]; t < tri_offsets[w + 1]; ++t)
+                draw_triangle(&P, &cam, &F, verts + 9 * t, tcls[t]);
+            for (int64_t b = 0; b < agents_per_world; ++b) {
+                int64_t h = w * agents_per_world + b;
+                if (h == g) continue; /* the ego's own body is not drawn */
+                float cor[8][3];
+                box_corners(ax[h], ay[h], az0[h], acos[h], asin[h], alen[h], awid[h], ahgt[h], cor);
+                for (int f = 0; f < 12; ++f) {
+                    float tri[9];
+                    for (int q = 0; q < 3; ++q) {
+                        tri[3 * q] = cor[BOX_TRIS[f][q]][0];
+                        tri[3 * q + 1] = cor[BOX_TRIS[f][q]][1];
+                        tri[3 * q + 2] = cor[BOX_TRIS[f][q]][2];
+                    }
+                    draw_triangle(&P, &cam, &F, tri, acls[h]);
+                }
+            }
+            for (int64_t p = 0; p < npx; ++p) {
+                uint32_t key = F.key[p];
+                uint32_t q = key >> 8;
+                out_cls[n * npx + p] = (uint8_t)(key & 255u);
+                if (q == 0xFFFFFFu) {
+                    out_depth[n * npx + p] = INFINITY;
+                } else {
+                    float izd = u2f(((P.qbase - q) << 3) | 4u);
+                    out_depth[n * npx + p] = 1.0f / izd;
+                }
+                if (out_flags) {
+                    uint8_t fl = 0;
+                    if (F.edge_key[p] <= key) fl |= 1;
+                    uint32_t k2 = F.k2[p];
+                    if (k2 != 0xFFFFFFFFu && (k2 >> 8) != 0xFFFFFFu && q != 0xFFFFFFu) {
+                        double z1 = 1.0 / (double)u2f(((P.qbase - q) << 3) | 4u);
+                        double z2 = 1.0 / (double)u2f(((P.qbase - (k2 >> 8)) << 3) | 4u);
+                        if (fabs(z2 - z1) <= 1e-4 * z1) fl |= 2;
+                    }
+                    out_flags[n * npx + p] = fl;
+                }
+                if (out_cover) out_cover[n * npx + p] = F.cover[p];
+            }
+        }
+        free(F.key); free(F.edge_key); free(F.k1); free(F.k2); free(F.cover);
+    }
+    return 0;
+}
+
+/* R7/R8 quantizer exposed for exhaustive checks. */
+void oracle_quantize(const float* iz, int64_t n, float nearp, float farp, uint32_t* q_out, float* depth_out)
+{
+    Params P;
+    init_params(&P, 1, 1, 1.0f, 1.0f, 0.5f, 0.5f, nearp, farp);
+    for (int64_t k = 0; k < n; ++k) {
+        float z = iz[k];
+        if (!(z >= P.izfar)) { q_out[k] = 0xFFFFFFu; depth_out[k] = INFINITY; continue; }
+        if (z > P.izcap) z = P.izcap;
+        uint32_t q = P.qbase - (f2u(z) >> 3);
+        q_out[k] = q;
+        depth_out[k] = 1.0f / u2f(((P.qbase - q) << 3) | 4u);
+    }
+}
+
+/*
+ * Uniform-grid binning of one scene: each triangle belongs to the cell that
+ * holds the centre of its xy bounding box (clamped into the grid); a cell
+ * records its triangle count and the 3-D bounding box of its members.
+ * Grid of world w: origin (bounds[w].xmin, bounds[w].ymin), square cells of
+ * `cell` metres, nx = max(1, ceil(width / cell)) columns, ny rows, cells
+ * numbered row-major (iy * nx + ix) after those of the previous worlds.
+ */
+int oracle_bin(int num_worlds, const int64_t* tri_offsets, const float* verts, const float* bounds,
+               float cell, int32_t* dims_out /*[nw][2]*/, int64_t* cell_base_out /*[nw+1]*/,
+               int64_t* home_out /*[T]*/, int32_t* count_out, float* aabb_out /*[cells][6]*/,
+               int64_t max_cells)
+{
+    int64_t base = 0;
+    for (int w = 0; w < num_worlds; ++w) {
+        float wx = bounds[4 * w + 2] - bounds[4 * w + 0];
+        float wy = bounds[4 * w + 3] - bounds[4 * w + 1];
+        float fnx = ceilf(wx / cell), fny = ceilf(wy / cell);
+        int32_t nx = fnx < 1.0f ? 1 : (int32_t)fnx;
+        int32_t ny = fny < 1.0f ? 1 : (int32_t)fny;
+        dims_out[2 * w] = nx;
+        dims_out[2 * w + 1] = ny;
+        cell_base_out[w] = base;
+        base += (int64_t)nx * ny;
+    }
+    cell_base_out[num_worlds] = base;
+    if (base > max_cells) return -1;
+    for (int64_t c = 0; c < base; ++c) {
+        count_out[c] = 0;
+        aabb_out[6 * c + 0] = aabb_out[6 * c + 1] = aabb_out[6 * c + 2] = INFINITY;
+        aabb_out[6 * c + 3] = aabb_out[6 * c + 4] = aabb_out[6 * c + 5] = -INFINITY;
+    }
+    for (int w = 0; w < num_worlds; ++w) {
+        int32_t nx = dims_out[2 * w], ny = dims_out[2 * w + 1];
+        for (int64_t t = tri_offsets[w]; t < tri_offsets[w + 1]; ++t) {
+            const float* v = verts + 9 * t;
+            float lo[3], hi[3];
+            for (int d = 0; d < 3; ++d) {
+                lo[d] = fminf(fminf(v[d], v[3 + d]), v[6 + d]);
+                hi[d] = fmaxf(fmaxf(v[d], v[3 + d]), v[6 + d]);
+            }
+            float mx = (lo[0] + hi[0]) * 0.5f, my = (lo[1] + hi[1]) * 0.5f;
+            float fx = floorf((mx - bounds[4 * w + 0]) / cell);
+            float fy = floorf((my - bounds[4 * w + 1]) / cell);
+            int32_t ix = !(fx >= 0.0f) ? 0 : (fx >= (float)(nx - 1) ? nx - 1 : (int32_t)fx);
+            int32_t iy = !(fy >= 0.0f) ? 0 : (fy >= (float)(ny - 1) ? ny - 1 : (int32_t)fy);
+            int64_t c = cell_base_out[w] + (int64_t)iy * nx + ix;
+            home_out[t] = c;
+            count_out[c]++;
+            for (int d = 0; d < 3; ++d) {
+                if (lo[d] < aabb_out[6 * c + d]) aabb_out[6 * c + d] = lo[d];
+                if (hi[d] > aabb_out[6 * c + 3 + d]) aabb_out[6 * c + 3 + d] = hi[d];
+            }
+        }
+    }
+    return 0;
+}
+
+/*
+ * Kinematic bicycle update (the per-step agent motion of the headline
+ * workload), in double precision:  v' = clamp(v + accel*dt, 0, vmax);
+ * psi' = psi + (v' / (0.6 L)) tan(steer) dt, wrapped into (-pi, pi];
+ * x' = x + v' cos(psi') dt, y' = y + v' sin(psi') dt.
+ */
+void oracle_agents_step(int64_t n, double* x, double* y, double* psi, double* v,
+                        const double* L, const double* steer, const double* accel,
+                        double dt, double vmax, double* cos_out, double* sin_out)
+{
+    const double PI = 3.14159265358979323846;
+    for (int64_t k = 0; k < n; ++k) {
+        double vn = v[k] + accel[k] * dt;
+        if (vn < 0.0) vn = 0.0;
+        if (vn > vmax) vn = vmax;
+        double p = psi[k] + vn / (0.6 * L[k]) * tan(steer[k]) * dt;
+        if (p > PI) p -= 2.0 * PI;
+        if (p <= -PI) p += 2.0 * PI;
+        x[k] += vn * cos(p) * dt;
+        y[k] += vn * sin(p) * dt;
+        psi[k] = p;
+        v[k] = vn;
+        cos_out[k] = cos(p);
+        sin_out[k] = sin(p);
+    }
+}
