@@ -1,0 +1,197 @@
+"""Benchmark: steady-state simulation steps of the headline workload on 1 GPU.
+
+One step = the kinematic bicycle update of every agent followed by rendering
+every agent's camera views (class + depth) through the C ABI.  Default
+workload: 1024 worlds x 64 agents x 4 cameras at 64x64 (262,144 views per
+step), ~37k static triangles per world, far plane 150 m, seeded synthetic
+inputs resident in HBM before timing.
+
+Prints one JSON line with agent-steps/s, images/s, the render kernel's HBM
+write roofline fraction (HIP events on the launch stream) and the CPU
+oracle timed on a bounded sample of the same workload.
+
+    python bench.py [--steps 100] [--warmup 10] [--config 4] [--no-cpu-baseline]
+"""
+import argparse
+import json
+import os
+import sys
+import time
+
+import numpy as np
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+HBM_PEAK_GBS = 8000.0   # MI355X HBM3E peak
+
+
+def parse():
+    ap = argparse.ArgumentParser()
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=100)
+    ap.add_argument("--warmup", type=int, default=10)
+    ap.add_argument("--config", type=int, default=4)
+    ap.add_argument("--worlds", type=int, default=None, help="use only the first N worlds (testing)")
+    ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="run only a plain device copy of known size (counter calibration)")
+    return ap.parse_args()
+
+
+def copy_calibration():
+    import torch
+    n = 1 << 30   # 1 GiB
+    a = torch.empty(n, dtype=torch.uint8, device="cuda")
+    a.fill_(1)
+    b = torch.empty_like(a)
+    torch.cuda.synchronize()
+    for _ in range(3):
+        b.copy_(a)
+    torch.cuda.synchronize()
+    print(json.dumps({"copy_bytes_per_launch": n, "launches": 3}))
+
+
+def cpu_baseline(wl, target_s):
+    from oracle import oracle as O
+    threads = os.cpu_count() or 1
+    env = os.environ.get("OMP_NUM_THREADS")
+    if env and env.isdigit():
+        threads = min(threads, int(env))
+    rng = np.random.default_rng(1234)
+    probe = np.sort(rng.choice(wl.num_views, size=min(2 * threads, wl.num_views), replace=False))
+    t0 = time.perf_counter()
+    O.render(wl.scene, wl.agents, wl.rig, view_ids=probe, want_flags=False, num_threads=threads)
+    dt = time.perf_counter() - t0
+    n = int(min(wl.num_views, max(len(probe), target_s / max(dt / len(probe), 1e-9))))
+    ids = np.sort(rng.choice(wl.num_views, size=n, replace=False))
+    t0 = time.perf_counter()
+    O.render(wl.scene, wl.agents, wl.rig, view_ids=ids, want_flags=False, num_threads=threads)
+    dt = time.perf_counter() - t0
+    images_s = n / dt
+    C = wl.rig.num_cams
+    return {"value": images_s / C, "unit": "agent-steps/s", "cores": threads, "kind": "oracle",
+            "images_per_s": images_s,
+            "sample": f"{n} seeded-random views of the same workload (brute force over every triangle of the "
+                      f"view's world + every other agent's box), {dt:.1f} s wall on {threads} threads; "
+                      f"agent-steps/s = images/s / {C} cameras"}
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(json.dumps({"error": "this build runs on one GPU only: the render path shards by world, "
+                                   "but no multi-GPU launch exists; use --gpus 1"}))
+        sys.exit(2)
+    import torch
+    if args.copy_calibration:
+        copy_calibration()
+        return
+    from paper_2607_26005_amd import pictura, scenegen as sg
+
+    t_gen = time.perf_counter()
+    wl = sg.make_config(args.config, num_worlds=args.worlds)
+    t_gen = time.perf_counter() - t_gen
+    K, Wm = args.steps, args.warmup
+    A = wl.agents.count
+    V = wl.num_views
+    H, W = wl.rig.height, wl.rig.width
+    print(f"# workload {wl.name}: {wl.scene.num_worlds} worlds, {wl.scene.num_tris} tris, {A} agents, "
+          f"{V} views {W}x{H}; generated in {t_gen:.1f} s", file=sys.stderr, flush=True)
+
+    r = pictura.Renderer(0)
+    r.upload(wl.scene, wl.cell_size)
+    da = pictura.DeviceAgents.from_host(wl.agents)
+    steer, accel = sg.controls(A, K + Wm, seed=wl.seed)
+    steer_d = torch.as_tensor(steer, device="cuda")
+    accel_d = torch.as_tensor(accel, device="cuda")
+    out_cls = torch.empty((V, H, W), dtype=torch.uint8, device="cuda")
+    out_depth = torch.empty((V, H, W), dtype=torch.float32, device="cuda")
+    moving = args.config == 4
+    torch.cuda.synchronize()
+
+    def step(s):
+        if moving:
+            r.agents_step(da, steer_d[s], accel_d[s], dt=0.1, vmax=20.0)
+        r.render(da, wl.rig, out_cls, out_depth)
+
+    for s in range(Wm):
+        step(s)
+    torch.cuda.synchronize()
+    print(f"# warmup done ({Wm} steps)", file=sys.stderr, flush=True)
+
+    stream = torch.cuda.current_stream()
+    ev_r0 = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
+    ev_r1 = [torch.cuda.Event(enable_timing=True) for _ in range(K)]
+    t_start = torch.cuda.Event(enable_timing=True)
+    t_end = torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    wall0 = time.perf_counter()
+    t_start.record(stream)
+    for s in range(K):
+        if moving:
+            r.agents_step(da, steer_d[Wm + s], accel_d[Wm + s], dt=0.1, vmax=20.0)
+        ev_r0[s].record(stream)
+        r.render(da, wl.rig, out_cls, out_depth)
+        ev_r1[s].record(stream)
+    t_end.record(stream)
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - wall0
+    total_ms = t_start.elapsed_time(t_end)
+    render_ms = [a.elapsed_time(b) for a, b in zip(ev_r0, ev_r1)]
+    ms_step = total_ms / K
+    avg_render_ms = float(np.mean(render_ms))
+    print(f"# timed {K} steps: {total_ms:.2f} ms (wall {wall * 1e3:.1f} ms); render avg {avg_render_ms:.4f} ms "
+          f"min {min(render_ms):.4f} max {max(render_ms):.4f}", file=sys.stderr, flush=True)
+
+    out_bytes = V * H * W * 5
+    achieved = out_bytes / (avg_render_ms * 1e-3) / 1e9
+    agent_steps_s = A * K / (total_ms * 1e-3)
+    images_s = V * K / (total_ms * 1e-3)
+    r.close()
+
+    cpu = None
+    if not args.no_cpu_baseline:
+        print("# cpu baseline (oracle) ...", file=sys.stderr, flush=True)
+        cpu = cpu_baseline(wl, args.cpu_seconds)
+
+    line = {
+        "metric": "agent-steps/s",
+        "value": agent_steps_s,
+        "unit": "agent-steps/s",
+        "images_per_s": images_s,
+        "n_gpus": 1,
+        "steps": K,
+        "warmup": Wm,
+        "ms_per_step": ms_step,
+        "render_ms": avg_render_ms,
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic (seeded generator; CARLA/WOMD stand-in)",
+        "config": {
+            "workload": f"{wl.name}: {wl.scene.num_worlds} worlds x {wl.agents.agents_per_world} agents x "
+                        f"{wl.rig.num_cams} cameras, {W}x{H} uint8 class + fp32 depth, "
+                        f"{wl.scene.num_tris // wl.scene.num_worlds} static tris/world, far {wl.rig.far:g} m",
+            "views_per_step": V,
+            "step": "bicycle update + render" if moving else "render",
+        },
+        "roofline": {
+            "bound": "hbm",
+            "kernel": "render_views_kernel",
+            "achieved": achieved,
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": achieved / HBM_PEAK_GBS,
+            "algorithmic_bytes_per_launch": out_bytes,
+            "traffic": None,
+        },
+        "cpu_baseline": cpu,
+    }
+    print(json.dumps(line), flush=True)
+
+
+if __name__ == "__main__":
+    main()

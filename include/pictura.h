@@ -1,0 +1,171 @@
+/*
+ * pictura.h -- C ABI of the MI355X (gfx950) batched class/depth view rasterizer.
+ *
+ * The library renders, for every agent of every world and every camera of
+ * the agent's rig, a perspective image of the surrounding agents' boxes and
+ * the static map triangles (paper Sec. 3.2, Eq. obs_pv: I_ik = Phi(A_i, W_i,
+ * K_ik); "only the surroundings are rendered", so a view never draws its own
+ * agent).  Each pixel receives the class ID of the nearest surface (uint8)
+ * and its view-space depth in metres (fp32, +inf for background).  The
+ * projection, near clipping, 8-bit-subpixel snapping, top-left fill rule and
+ * the 24-bit-depth|8-bit-class visibility key follow fixed rules (R1..R9 in
+ * the repository's design notes), so results do not depend on triangle order.
+ *
+ * Conventions
+ *  - Plain C99; no HIP/CUDA or C++ types.  A `void* stream` is a hipStream_t
+ *    (NULL = the device's null stream).  Device pointers are HIP device
+ *    allocations on the context's device; host pointers are ordinary memory.
+ *  - Every call returns a pictura_status.  Argument errors are detected on the
+ *    host and returned synchronously without launching anything; the context
+ *    stays usable after any error.  pictura_last_error() gives a message.
+ *  - Work is enqueued on `stream` and the calls return without synchronising,
+ *    except where a call says it copies to host memory.
+ *  - A context is not thread-safe: use one context per host thread.
+ */
+#ifndef PICTURA_H
+#define PICTURA_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef int32_t pictura_status;
+#define PICTURA_OK        0
+#define PICTURA_EINVAL   (-1) /* bad argument (null pointer, size, rig value) */
+#define PICTURA_ENOMEM   (-2) /* device allocation failed */
+#define PICTURA_EDEVICE  (-3) /* no usable HIP device, or a HIP call failed */
+#define PICTURA_ESTATE   (-4) /* call order violated (e.g. render before binning) */
+#define PICTURA_ERANGE   (-5) /* a size exceeds a supported limit */
+
+#define PICTURA_MAX_CAMS 8
+
+typedef struct pictura_ctx_s* pictura_ctx;
+
+/* Static scene of all worlds (host memory; the library copies it).
+ * Triangles are concatenated world by world: world w owns triangles
+ * [tri_offsets[w], tri_offsets[w+1]).  verts[t] = x0 y0 z0 x1 y1 z1 x2 y2 z2 in
+ * world metres (z up).  cls[t] is the class ID (0..254).  bounds[w] =
+ * xmin ymin xmax ymax is the rectangle the world's binning grid covers;
+ * triangles outside it are still drawn (they are binned into edge cells). */
+typedef struct {
+    int32_t num_worlds;
+    const int64_t* tri_offsets; /* host, [num_worlds + 1], non-decreasing, [0] == 0 */
+    const float* verts;         /* host, [T][9] */
+    const uint8_t* cls;         /* host, [T] */
+    const float* bounds;        /* host, [num_worlds][4] */
+} pictura_scene;
+
+/* Agents (device memory, caller-owned, structure of arrays).  Agent
+ * g = w * agents_per_world + a; (cos_h, sin_h) is its heading; the box spans
+ * length x width around (x, y) and z0 .. z0 + height. */
+typedef struct {
+    int32_t num_worlds;
+    int32_t agents_per_world;
+    const float* x;
+    const float* y;
+    const float* z0;
+    const float* cos_h;
+    const float* sin_h;
+    const float* length;
+    const float* width;
+    const float* height;
+    const uint8_t* cls;
+} pictura_agents;
+
+/* Camera rig shared by all agents (host, by value).  Pinhole intrinsics in
+ * pixels (x right, y down, pixel (i, j) centre at (i + 0.5, j + 0.5)); mount k
+ * = x y z cos_yaw sin_yaw in the ego frame (x forward, y left, z up; paper
+ * App. A.2, Tab. camera_rig).  near_m > 0, far_m > near_m. */
+typedef struct {
+    int32_t num_cams;
+    int32_t width;
+    int32_t height;
+    float fx, fy, cx, cy;
+    float near_m, far_m;
+    float mount[PICTURA_MAX_CAMS][5];
+} pictura_rig;
+
+/* Mutable kinematic-bicycle state (device memory, caller-owned). */
+typedef struct {
+    int32_t count;
+    float* x;
+    float* y;
+    float* psi;      /* heading angle, kept in (-pi, pi] */
+    float* speed;    /* m/s */
+    float* cos_h;    /* written: cos(psi) */
+    float* sin_h;    /* written: sin(psi) */
+    const float* length; /* wheelbase is 0.6 * length */
+} pictura_agent_state;
+
+/* Create a context on HIP device `device`.  Returns PICTURA_EDEVICE when no
+ * such device exists.  *out is set to NULL on failure. */
+pictura_status pictura_create(int32_t device, pictura_ctx* out);
+
+/* Release all device memory owned by the context.  NULL is ignored. */
+void pictura_destroy(pictura_ctx ctx);
+
+/* Message of the last error on this context ("" if none).  Owned by ctx. */
+const char* pictura_last_error(pictura_ctx ctx);
+
+/* Copy the static scene to device memory owned by the context (replacing any
+ * previous scene and invalidating its bins).  Enqueued on `stream`; the host
+ * arrays may be reused as soon as the call returns (the copy is staged).
+ * EINVAL: null pointers, num_worlds < 1, offsets not non-decreasing, a class
+ * ID of 255.  ERANGE: more than 2^31 - 1 triangles.  ENOMEM: allocation. */
+pictura_status pictura_scene_upload(pictura_ctx ctx, const pictura_scene* scene, void* stream);
+
+/* Build the uniform grid of every world: square cells of `cell_size_m`
+ * metres covering the world's bounds (ceil(extent / cell) cells per axis);
+ * each triangle belongs to the cell holding the centre of its xy bounding
+ * box (clamped into the grid); each cell records its triangle range and the
+ * 3-D bounding box of its triangles.  The library re-lays the triangles out
+ * in cell order.  ESTATE: no scene.  EINVAL: cell_size_m not > 0.
+ * ERANGE: more than 2^31 - 1 cells.  Enqueued on `stream`. */
+pictura_status pictura_bin_scene(pictura_ctx ctx, float cell_size_m, void* stream);
+
+/* Render all V = num_worlds * agents_per_world * num_cams views (paper
+ * Sec. 3.2, Eq. obs_pv).  View v = (w * agents_per_world + a) * num_cams + k
+ * writes out_cls[v][y][x] (uint8 class; 4 = sky for background) and
+ * out_depth[v][y][x] (fp32 view-space depth in metres, +inf for background),
+ * row-major, y down.  Both outputs are caller-owned device buffers of
+ * V * height * width elements.  ESTATE: scene not binned.  EINVAL: null
+ * pointers, num_worlds different from the scene's, rig values out of range
+ * (num_cams 1..8, width/height 1..4096, fx, fy > 0, 0 < near < far, far/near
+ * small enough for the 24-bit depth key).  Asynchronous on `stream`. */
+pictura_status pictura_render_views(pictura_ctx ctx, const pictura_agents* agents, const pictura_rig* rig,
+                                    uint8_t* out_cls, float* out_depth, void* stream);
+
+/* One kinematic-bicycle step for every agent (the per-step agent motion of
+ * the headline workload): v' = clamp(v + accel * dt, 0, vmax);
+ * psi' = psi + v' / (0.6 length) * tan(steer) * dt wrapped into (-pi, pi];
+ * x += v' cos(psi') dt; y += v' sin(psi') dt; cos_h/sin_h = cos/sin(psi').
+ * steer[count] (radians) and accel[count] (m/s^2) are device arrays.
+ * EINVAL: null pointers, count < 0, dt or vmax not finite.  Asynchronous. */
+pictura_status pictura_agents_step(pictura_ctx ctx, const pictura_agent_state* state, const float* steer,
+                                   const float* accel, float dt, float vmax, void* stream);
+
+/* ---- introspection and test controls -------------------------------------- */
+
+/* Grid geometry after pictura_bin_scene (host memory, synchronous: waits for
+ * the binning to finish).  dims[w] = nx, ny; cell_base[w] = first cell of
+ * world w (cell_base[num_worlds] = total cells).  Any pointer may be NULL. */
+pictura_status pictura_bins_info(pictura_ctx ctx, int32_t* dims, int64_t* cell_base, int64_t* total_cells);
+
+/* Copy the bins to host memory (synchronous).  cell_start[total_cells + 1]:
+ * first re-laid-out triangle of each cell; cell_aabb[total_cells][6]: xmin
+ * ymin zmin xmax ymax zmax of the cell's triangles (+inf/-inf when empty);
+ * perm[T]: original index of each re-laid-out triangle. */
+pictura_status pictura_bins_copy(pictura_ctx ctx, uint32_t* cell_start, float* cell_aabb, uint32_t* perm);
+
+#define PICTURA_OPT_CULL   1 /* 1 (default): cell + triangle frustum culling; 0: every triangle of the world */
+#define PICTURA_OPT_TILE   2 /* 0 (default): 64x64 LDS tiles; n in 8..64: force n x n tiles */
+/* Set a context option.  Results must not change with either option. */
+pictura_status pictura_set_option(pictura_ctx ctx, int32_t option, int32_t value);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* PICTURA_H */

@@ -27,7 +27,9 @@
  *              rd = 1/delta:  pa = (nx*rd)*(1/fx), pb = -(ny*rd)*(1/fy),
  *              pc = nz*rd, and at pixel (i, j):
  *              iz = fma(pa, i+0.5-cx, fma(pb, j+0.5-cy, pc))   (= 1/zv).
- *  R4 near     Sutherland-Hodgman against zv >= near, edges v0v1, v1v2, v2v0;
+ *  R4 near     a triangle with every vertex at zv < near, or every vertex at
+ *              zv > far, is not drawn.  Otherwise
+ *              Sutherland-Hodgman against zv >= near, edges v0v1, v1v2, v2v0;
  *              each crossing point is computed from the inside vertex I
  *              towards the outside vertex O: t = (near - I.z)/(O.z - I.z),
  *              x = fma(t, O.x - I.x, I.x), y likewise, z = near; the 3- or
@@ -249,6 +251,7 @@ static void draw_triangle(const Params* P, const Cam* cam, Frame* F, const float
     int nin = 0;
     for (int k = 0; k < 3; ++k) { in[k] = v[k].z >= P->nearp; nin += in[k]; }
     if (nin == 0) return;
+    if (v[0].z > P->farp && v[1].z > P->farp && v[2].z > P->farp) return;
     float pa, pb, pc;
     if (!depth_plane(cam, P, t, &pa, &pb, &pc)) return;
     V3 poly[4];

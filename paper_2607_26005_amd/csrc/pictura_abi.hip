@@ -1,0 +1,402 @@
+// C ABI of the batched class/depth view rasterizer: context, argument
+// validation, device memory of the scene and its bins, kernel launches.
+#include <cmath>
+#include <cstdarg>
+#include <cstdio>
+#include <cstring>
+#include <string>
+#include <vector>
+
+#include "../../include/pictura.h"
+#include "pictura_internal.h"
+
+using namespace pictura;
+
+struct pictura_ctx_s {
+    int device = 0;
+    std::string err;
+    // scene (original order)
+    int32_t num_worlds = 0;
+    int64_t T = 0;
+    std::vector<int64_t> offsets_h;
+    std::vector<float> bounds_h;
+    float* verts = nullptr;
+    uint8_t* cls = nullptr;
+    int64_t* offsets_d = nullptr;
+    bool have_scene = false;
+    // bins
+    bool binned = false;
+    float cell_size = 0.0f;
+    int64_t total_cells = 0;
+    std::vector<WorldGrid> grids_h;
+    WorldGrid* grids = nullptr;
+    uint32_t* home = nullptr;
+    uint32_t* rank = nullptr;
+    uint32_t* cell_start = nullptr;
+    uint32_t* aabb_bits = nullptr;
+    uint32_t* margin_bits = nullptr;
+    uint32_t* scan_tmp = nullptr;
+    float4* triA = nullptr;
+    float4* triB = nullptr;
+    float2* triC = nullptr;
+    uint32_t* perm = nullptr;
+    float4* cell_lo = nullptr;
+    float4* cell_hi = nullptr;
+    // options
+    int cull = 1;
+    int tile = 0;
+};
+
+namespace {
+
+pictura_status fail(pictura_ctx c, pictura_status st, const char* fmt, ...)
+{
+    char buf[512];
+    va_list ap;
+    va_start(ap, fmt);
+    vsnprintf(buf, sizeof buf, fmt, ap);
+    va_end(ap);
+    if (c) c->err = buf;
+    return st;
+}
+
+pictura_status hip_fail(pictura_ctx c, hipError_t e, const char* what)
+{
+    if (e == hipErrorOutOfMemory || e == hipErrorMemoryAllocation)
+        return fail(c, PICTURA_ENOMEM, "%s: %s", what, hipGetErrorString(e));
+    return fail(c, PICTURA_EDEVICE, "%s: %s", what, hipGetErrorString(e));
+}
+
+template <typename T>
+void dfree(T*& p)
+{
+    if (p) (void)hipFree((void*)p);
+    p = nullptr;
+}
+
+template <typename T>
+hipError_t dalloc(T*& p, size_t count)
+{
+    dfree(p);
+    if (count == 0) count = 1;
+    return hipMalloc((void**)&p, count * sizeof(T));
+}
+
+void free_bins(pictura_ctx c)
+{
+    dfree(c->grids); dfree(c->home); dfree(c->rank); dfree(c->cell_start); dfree(c->aabb_bits);
+    dfree(c->margin_bits); dfree(c->scan_tmp); dfree(c->triA); dfree(c->triB); dfree(c->triC);
+    dfree(c->perm); dfree(c->cell_lo); dfree(c->cell_hi);
+    c->binned = false;
+    c->total_cells = 0;
+    c->grids_h.clear();
+}
+
+void free_scene(pictura_ctx c)
+{
+    free_bins(c);
+    dfree(c->verts); dfree(c->cls); dfree(c->offsets_d);
+    c->have_scene = false;
+    c->T = 0;
+    c->num_worlds = 0;
+}
+
+struct DeviceGuard {
+    int prev = -1;
+    explicit DeviceGuard(int d) { if (hipGetDevice(&prev) != hipSuccess) prev = -1; (void)hipSetDevice(d); }
+    ~DeviceGuard() { if (prev >= 0) (void)hipSetDevice(prev); }
+};
+
+uint32_t f2u(float f) { uint32_t u; std::memcpy(&u, &f, 4); return u; }
+float u2f(uint32_t u) { float f; std::memcpy(&f, &u, 4); return f; }
+
+float pow2_ceil(float x)
+{
+    uint32_t u = f2u(x);
+    if ((u & 0x7FFFFFu) == 0) return x;
+    return u2f((u & 0x7F800000u) + 0x00800000u);
+}
+
+}  // namespace
+
+extern "C" {
+
+pictura_status pictura_create(int32_t device, pictura_ctx* out)
+{
+    if (!out) return PICTURA_EINVAL;
+    *out = nullptr;
+    int n = 0;
+    if (hipGetDeviceCount(&n) != hipSuccess || n <= 0) return PICTURA_EDEVICE;
+    if (device < 0 || device >= n) return PICTURA_EDEVICE;
+    auto* c = new (std::nothrow) pictura_ctx_s();
+    if (!c) return PICTURA_ENOMEM;
+    c->device = device;
+    *out = c;
+    return PICTURA_OK;
+}
+
+void pictura_destroy(pictura_ctx c)
+{
+    if (!c) return;
+    {
+        DeviceGuard g(c->device);
+        (void)hipDeviceSynchronize();
+        free_scene(c);
+    }
+    delete c;
+}
+
+const char* pictura_last_error(pictura_ctx c) { return c ? c->err.c_str() : "null context"; }
+
+pictura_status pictura_scene_upload(pictura_ctx c, const pictura_scene* s, void* stream)
+{
+    if (!c) return PICTURA_EINVAL;
+    c->err.clear();
+    if (!s || !s->tri_offsets || !s->bounds) return fail(c, PICTURA_EINVAL, "scene_upload: null scene pointer");
+    if (s->num_worlds < 1) return fail(c, PICTURA_EINVAL, "scene_upload: num_worlds must be >= 1");
+    const int nw = s->num_worlds;
+    if (s->tri_offsets[0] != 0) return fail(c, PICTURA_EINVAL, "scene_upload: tri_offsets[0] must be 0");
+    for (int w = 0; w < nw; ++w)
+        if (s->tri_offsets[w + 1] < s->tri_offsets[w])
+            return fail(c, PICTURA_EINVAL, "scene_upload: tri_offsets must be non-decreasing");
+    const int64_t T = s->tri_offsets[nw];
+    if (T > 0x7FFFFFFFll) return fail(c, PICTURA_ERANGE, "scene_upload: more than 2^31-1 triangles");
+    if (T > 0 && (!s->verts || !s->cls)) return fail(c, PICTURA_EINVAL, "scene_upload: null verts/cls");
+    for (int64_t t = 0; t < T; ++t)
+        if (s->cls[t] == 255) return fail(c, PICTURA_EINVAL, "scene_upload: class ID 255 is reserved");
+    for (int w = 0; w < nw; ++w) {
+        const float* b = s->bounds + 4 * w;
+        if (!(std::isfinite(b[0]) && std::isfinite(b[1]) && std::isfinite(b[2]) && std::isfinite(b[3])) ||
+            !(b[2] > b[0]) || !(b[3] > b[1]))
+            return fail(c, PICTURA_EINVAL, "scene_upload: bounds of world %d are not a finite rectangle", w);
+    }
+    DeviceGuard g(c->device);
+    hipStream_t st = (hipStream_t)stream;
+    free_scene(c);
+    hipError_t e;
+    if ((e = dalloc(c->verts, (size_t)T * 9)) != hipSuccess) return hip_fail(c, e, "scene_upload alloc");
+    if ((e = dalloc(c->cls, (size_t)T)) != hipSuccess) { free_scene(c); return hip_fail(c, e, "scene_upload alloc"); }
+    if ((e = dalloc(c->offsets_d, (size_t)nw + 1)) != hipSuccess) { free_scene(c); return hip_fail(c, e, "scene_upload alloc"); }
+    // Synchronous-from-the-caller's-view copies: pageable host memory is staged
+    // by the runtime before hipMemcpyAsync returns, so the caller may reuse it.
+    if (T > 0) {
+        if ((e = hipMemcpyAsync(c->verts, s->verts, (size_t)T * 9 * sizeof(float), hipMemcpyHostToDevice, st)) != hipSuccess ||
+            (e = hipMemcpyAsync(c->cls, s->cls, (size_t)T, hipMemcpyHostToDevice, st)) != hipSuccess) {
+            free_scene(c);
+            return hip_fail(c, e, "scene_upload copy");
+        }
+    }
+    if ((e = hipMemcpyAsync(c->offsets_d, s->tri_offsets, (size_t)(nw + 1) * sizeof(int64_t), hipMemcpyHostToDevice, st)) != hipSuccess) {
+        free_scene(c);
+        return hip_fail(c, e, "scene_upload copy");
+    }
+    if ((e = hipStreamSynchronize(st)) != hipSuccess) { free_scene(c); return hip_fail(c, e, "scene_upload sync"); }
+    c->offsets_h.assign(s->tri_offsets, s->tri_offsets + nw + 1);
+    c->bounds_h.assign(s->bounds, s->bounds + 4 * nw);
+    c->num_worlds = nw;
+    c->T = T;
+    c->have_scene = true;
+    return PICTURA_OK;
+}
+
+pictura_status pictura_bin_scene(pictura_ctx c, float cell, void* stream)
+{
+    if (!c) return PICTURA_EINVAL;
+    c->err.clear();
+    if (!c->have_scene) return fail(c, PICTURA_ESTATE, "bin_scene: no scene uploaded");
+    if (!(cell > 0.0f) || !std::isfinite(cell)) return fail(c, PICTURA_EINVAL, "bin_scene: cell size must be > 0");
+    const int nw = c->num_worlds;
+    std::vector<WorldGrid> grids(nw);
+    int64_t total = 0;
+    for (int w = 0; w < nw; ++w) {
+        const float* b = &c->bounds_h[4 * w];
+        const float wx = b[2] - b[0], wy = b[3] - b[1];
+        const float fnx = std::ceil(wx / cell), fny = std::ceil(wy / cell);
+        if (!(fnx < 1.0e9f) || !(fny < 1.0e9f)) return fail(c, PICTURA_ERANGE, "bin_scene: grid too large");
+        WorldGrid& g = grids[w];
+        g.ox = b[0]; g.oy = b[1];
+        g.nx = fnx < 1.0f ? 1 : (int32_t)fnx;
+        g.ny = fny < 1.0f ? 1 : (int32_t)fny;
+        g.cell_base = (int32_t)total;
+        g.margin = 0.0f;
+        g.pad0 = g.pad1 = 0;
+        total += (int64_t)g.nx * g.ny;
+        if (total >= 0x7FFFFFFFll) return fail(c, PICTURA_ERANGE, "bin_scene: more than 2^31-1 cells");
+    }
+    DeviceGuard dg(c->device);
+    hipStream_t st = (hipStream_t)stream;
+    free_bins(c);
+    const int64_t T = c->T;
+    hipError_t e = hipSuccess;
+    const int64_t ntmp = scan_tmp_needed(total + 1);
+    if ((e = dalloc(c->grids, (size_t)nw)) != hipSuccess || (e = dalloc(c->home, (size_t)T)) != hipSuccess ||
+        (e = dalloc(c->rank, (size_t)T)) != hipSuccess || (e = dalloc(c->cell_start, (size_t)total + 1)) != hipSuccess ||
+        (e = dalloc(c->aabb_bits, (size_t)total * 8)) != hipSuccess || (e = dalloc(c->margin_bits, (size_t)nw)) != hipSuccess ||
+        (e = dalloc(c->scan_tmp, (size_t)ntmp)) != hipSuccess || (e = dalloc(c->triA, (size_t)T)) != hipSuccess ||
+        (e = dalloc(c->triB, (size_t)T)) != hipSuccess || (e = dalloc(c->triC, (size_t)T)) != hipSuccess ||
+        (e = dalloc(c->perm, (size_t)T)) != hipSuccess || (e = dalloc(c->cell_lo, (size_t)total)) != hipSuccess ||
+        (e = dalloc(c->cell_hi, (size_t)total)) != hipSuccess) {
+        free_bins(c);
+        return hip_fail(c, e, "bin_scene alloc");
+    }
+    if ((e = hipMemcpyAsync(c->grids, grids.data(), sizeof(WorldGrid) * nw, hipMemcpyHostToDevice, st)) != hipSuccess) {
+        free_bins(c);
+        return hip_fail(c, e, "bin_scene copy");
+    }
+    BinWork W{};
+    W.verts = c->verts; W.cls = c->cls; W.tri_offsets = c->offsets_d; W.T = T; W.num_worlds = nw;
+    W.grids = c->grids; W.total_cells = total; W.cell_size = cell;
+    W.home = c->home; W.rank = c->rank; W.count = c->cell_start; W.aabb_bits = c->aabb_bits;
+    W.margin_bits = c->margin_bits; W.scan_tmp = c->scan_tmp; W.scan_tmp_len = ntmp;
+    W.triA = c->triA; W.triB = c->triB; W.triC = c->triC; W.perm = c->perm;
+    W.cell_lo = c->cell_lo; W.cell_hi = c->cell_hi;
+    if ((e = launch_bin(W, st)) != hipSuccess) { free_bins(c); return hip_fail(c, e, "bin_scene launch"); }
+    // the host copy of the grids is needed again for render's argument checks
+    if ((e = hipStreamSynchronize(st)) != hipSuccess) { free_bins(c); return hip_fail(c, e, "bin_scene sync"); }
+    c->grids_h = grids;
+    c->cell_size = cell;
+    c->total_cells = total;
+    c->binned = true;
+    return PICTURA_OK;
+}
+
+pictura_status pictura_render_views(pictura_ctx c, const pictura_agents* ag, const pictura_rig* rig,
+                                    uint8_t* out_cls, float* out_depth, void* stream)
+{
+    if (!c) return PICTURA_EINVAL;
+    c->err.clear();
+    if (!ag || !rig || !out_cls || !out_depth) return fail(c, PICTURA_EINVAL, "render_views: null argument");
+    if (!c->binned) return fail(c, PICTURA_ESTATE, "render_views: scene not binned");
+    if (ag->num_worlds != c->num_worlds)
+        return fail(c, PICTURA_EINVAL, "render_views: agents.num_worlds %d != scene num_worlds %d", ag->num_worlds, c->num_worlds);
+    if (ag->agents_per_world < 1) return fail(c, PICTURA_EINVAL, "render_views: agents_per_world must be >= 1");
+    if (!ag->x || !ag->y || !ag->z0 || !ag->cos_h || !ag->sin_h || !ag->length || !ag->width || !ag->height || !ag->cls)
+        return fail(c, PICTURA_EINVAL, "render_views: null agent array");
+    if (rig->num_cams < 1 || rig->num_cams > PICTURA_MAX_CAMS) return fail(c, PICTURA_EINVAL, "render_views: num_cams must be 1..8");
+    if (rig->width < 1 || rig->height < 1 || rig->width > 4096 || rig->height > 4096)
+        return fail(c, PICTURA_EINVAL, "render_views: width/height must be 1..4096");
+    if (!(rig->fx > 0.0f) || !(rig->fy > 0.0f) || !std::isfinite(rig->fx) || !std::isfinite(rig->fy) ||
+        !std::isfinite(rig->cx) || !std::isfinite(rig->cy))
+        return fail(c, PICTURA_EINVAL, "render_views: intrinsics must be finite with fx, fy > 0");
+    if (!(rig->near_m > 0.0f) || !(rig->far_m > rig->near_m) || !std::isfinite(rig->far_m))
+        return fail(c, PICTURA_EINVAL, "render_views: need 0 < near < far < inf");
+    for (int k = 0; k < rig->num_cams; ++k)
+        for (int q = 0; q < 5; ++q)
+            if (!std::isfinite(rig->mount[k][q])) return fail(c, PICTURA_EINVAL, "render_views: mount %d not finite", k);
+    const float izfar = 1.0f / rig->far_m;
+    const float izcap = pow2_ceil(1.0f / rig->near_m);
+    if (!(izfar > 0.0f) || !std::isfinite(izcap) || ((f2u(izcap) >> 3) - (f2u(izfar) >> 3)) >= 0xFFFFFFu)
+        return fail(c, PICTURA_EINVAL, "render_views: far/near ratio too large for the 24-bit depth key");
+    const int64_t V = (int64_t)c->num_worlds * ag->agents_per_world * rig->num_cams;
+    if (V == 0) return PICTURA_OK;
+
+    RenderParams P{};
+    P.scene.triA = c->triA; P.scene.triB = c->triB; P.scene.triC = c->triC;
+    P.scene.cell_start = c->cell_start; P.scene.cell_lo = c->cell_lo; P.scene.cell_hi = c->cell_hi;
+    P.scene.grids = c->grids; P.scene.cell_size = c->cell_size; P.scene.num_worlds = c->num_worlds;
+    P.ax = ag->x; P.ay = ag->y; P.az0 = ag->z0; P.ac = ag->cos_h; P.as = ag->sin_h;
+    P.al = ag->length; P.aw = ag->width; P.ah = ag->height; P.acls = ag->cls;
+    P.A = ag->agents_per_world; P.C = rig->num_cams;
+    P.W = rig->width; P.H = rig->height;
+    P.fx = rig->fx; P.fy = rig->fy; P.cx = rig->cx; P.cy = rig->cy; P.nearp = rig->near_m; P.farp = rig->far_m;
+    for (int k = 0; k < PICTURA_MAX_CAMS; ++k)
+        for (int q = 0; q < 5; ++q) P.mount[k][q] = k < rig->num_cams ? rig->mount[k][q] : 0.0f;
+    P.fx256 = 256.0f * P.fx; P.fy256 = 256.0f * P.fy; P.cx256 = 256.0f * P.cx; P.cy256 = 256.0f * P.cy;
+    P.rfx = 1.0f / P.fx; P.rfy = 1.0f / P.fy;
+    P.izfar = izfar; P.izcap = izcap; P.qbase = f2u(izcap) >> 3;
+    int tw = 64, th = 64;
+    if (c->tile > 0) { tw = c->tile; th = c->tile; }
+    tw = tw < P.W ? tw : P.W;
+    th = th < P.H ? th : P.H;
+    P.tile_w = tw; P.tile_h = th;
+    P.tiles_x = (P.W + tw - 1) / tw;
+    P.tiles_y = (P.H + th - 1) / th;
+    P.num_views = V;
+    P.num_blocks = V * P.tiles_x * P.tiles_y;
+    if (P.num_blocks > 0x7FFFFFFFll) return fail(c, PICTURA_ERANGE, "render_views: too many view tiles in one call");
+    P.out_cls = out_cls; P.out_depth = out_depth;
+    P.cull = c->cull;
+    P.vec_out = ((reinterpret_cast<uintptr_t>(out_cls) | reinterpret_cast<uintptr_t>(out_depth)) & 15u) == 0 ? 1 : 0;
+    DeviceGuard dg(c->device);
+    hipError_t e = launch_render(P, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(c, e, "render_views launch");
+    return PICTURA_OK;
+}
+
+pictura_status pictura_agents_step(pictura_ctx c, const pictura_agent_state* s, const float* steer,
+                                   const float* accel, float dt, float vmax, void* stream)
+{
+    if (!c) return PICTURA_EINVAL;
+    c->err.clear();
+    if (!s || !steer || !accel) return fail(c, PICTURA_EINVAL, "agents_step: null argument");
+    if (s->count < 0) return fail(c, PICTURA_EINVAL, "agents_step: count < 0");
+    if (s->count > 0 && (!s->x || !s->y || !s->psi || !s->speed || !s->cos_h || !s->sin_h || !s->length))
+        return fail(c, PICTURA_EINVAL, "agents_step: null state array");
+    if (!std::isfinite(dt) || !std::isfinite(vmax)) return fail(c, PICTURA_EINVAL, "agents_step: dt/vmax not finite");
+    AgentStepParams p{};
+    p.x = s->x; p.y = s->y; p.psi = s->psi; p.speed = s->speed; p.cos_h = s->cos_h; p.sin_h = s->sin_h;
+    p.length = s->length; p.steer = steer; p.accel = accel; p.dt = dt; p.vmax = vmax; p.count = s->count;
+    DeviceGuard dg(c->device);
+    hipError_t e = launch_agents_step(p, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(c, e, "agents_step launch");
+    return PICTURA_OK;
+}
+
+pictura_status pictura_bins_info(pictura_ctx c, int32_t* dims, int64_t* cell_base, int64_t* total_cells)
+{
+    if (!c) return PICTURA_EINVAL;
+    c->err.clear();
+    if (!c->binned) return fail(c, PICTURA_ESTATE, "bins_info: scene not binned");
+    for (int w = 0; w < c->num_worlds; ++w) {
+        if (dims) { dims[2 * w] = c->grids_h[w].nx; dims[2 * w + 1] = c->grids_h[w].ny; }
+        if (cell_base) cell_base[w] = c->grids_h[w].cell_base;
+    }
+    if (cell_base) cell_base[c->num_worlds] = c->total_cells;
+    if (total_cells) *total_cells = c->total_cells;
+    return PICTURA_OK;
+}
+
+pictura_status pictura_bins_copy(pictura_ctx c, uint32_t* cell_start, float* cell_aabb, uint32_t* perm)
+{
+    if (!c) return PICTURA_EINVAL;
+    c->err.clear();
+    if (!c->binned) return fail(c, PICTURA_ESTATE, "bins_copy: scene not binned");
+    DeviceGuard dg(c->device);
+    hipError_t e;
+    if ((e = hipDeviceSynchronize()) != hipSuccess) return hip_fail(c, e, "bins_copy sync");
+    const int64_t n = c->total_cells;
+    if (cell_start && (e = hipMemcpy(cell_start, c->cell_start, sizeof(uint32_t) * (n + 1), hipMemcpyDeviceToHost)) != hipSuccess)
+        return hip_fail(c, e, "bins_copy");
+    if (cell_aabb) {
+        std::vector<float4> lo(n), hi(n);
+        if ((e = hipMemcpy(lo.data(), c->cell_lo, sizeof(float4) * n, hipMemcpyDeviceToHost)) != hipSuccess ||
+            (e = hipMemcpy(hi.data(), c->cell_hi, sizeof(float4) * n, hipMemcpyDeviceToHost)) != hipSuccess)
+            return hip_fail(c, e, "bins_copy");
+        for (int64_t k = 0; k < n; ++k) {
+            float* o = cell_aabb + 6 * k;
+            o[0] = lo[k].x; o[1] = lo[k].y; o[2] = lo[k].z; o[3] = hi[k].x; o[4] = hi[k].y; o[5] = hi[k].z;
+        }
+    }
+    if (perm && c->T > 0 && (e = hipMemcpy(perm, c->perm, sizeof(uint32_t) * c->T, hipMemcpyDeviceToHost)) != hipSuccess)
+        return hip_fail(c, e, "bins_copy");
+    return PICTURA_OK;
+}
+
+pictura_status pictura_set_option(pictura_ctx c, int32_t option, int32_t value)
+{
+    if (!c) return PICTURA_EINVAL;
+    c->err.clear();
+    if (option == PICTURA_OPT_CULL) {
+        if (value != 0 && value != 1) return fail(c, PICTURA_EINVAL, "set_option: CULL must be 0 or 1");
+        c->cull = value;
+        return PICTURA_OK;
+    }
+    if (option == PICTURA_OPT_TILE) {
+        if (value != 0 && (value < 8 || value > 64)) return fail(c, PICTURA_EINVAL, "set_option: TILE must be 0 or 8..64");
+        c->tile = value;
+        return PICTURA_OK;
+    }
+    return fail(c, PICTURA_EINVAL, "set_option: unknown option %d", option);
+}
+
+}  // extern "C"

@@ -1,0 +1,102 @@
+// Internal structures of the HIP library: device scene layout, kernel
+// parameter blocks and launcher declarations.  Not part of the C ABI.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace pictura {
+
+constexpr int kBlock = 256;          // threads per render workgroup (4 wave64)
+constexpr int kTileMaxPx = 4096;     // LDS framebuffer capacity (u32 keys)
+constexpr int kCellCap = 512;        // visible cells gathered per batch
+constexpr int kBigCap = 64;          // LDS queue of large triangles
+constexpr int kSmallPx = 16;         // bbox pixel count rasterized by a single lane
+constexpr int kAgentBatch = 256;     // agents box-culled per batch
+
+// Grid of one world.  Cells are numbered row-major from cell_base.
+struct WorldGrid {
+    float ox, oy;        // grid origin (bounds xmin, ymin)
+    int32_t nx, ny;
+    int32_t cell_base;
+    float margin;        // how far any cell's triangle AABB reaches beyond its cell rectangle
+    int32_t pad0, pad1;
+};
+
+// Re-laid-out triangle t (cell order) is split over three arrays so that a
+// wave reading 64 consecutive triangles issues three coalesced loads:
+//   A[t] = (x0, y0, z0, x1), B[t] = (y1, z1, x2, y2), C[t] = (z2, bits(class)).
+struct SceneDev {
+    const float4* triA;
+    const float4* triB;
+    const float2* triC;
+    const uint32_t* cell_start;   // [cells + 1]
+    const float4* cell_lo;        // [cells] xmin ymin zmin -
+    const float4* cell_hi;        // [cells] xmax ymax zmax -
+    const WorldGrid* grids;       // [num_worlds]
+    float cell_size;
+    int32_t num_worlds;
+};
+
+struct RenderParams {
+    SceneDev scene;
+    // agents (SoA)
+    const float* ax; const float* ay; const float* az0;
+    const float* ac; const float* as; const float* al; const float* aw; const float* ah;
+    const uint8_t* acls;
+    int32_t A;          // agents per world
+    int32_t C;          // cameras per agent
+    // rig
+    int32_t W, H;
+    float fx, fy, cx, cy, nearp, farp;
+    float mount[8][5];
+    // derived constants
+    float fx256, fy256, cx256, cy256, rfx, rfy, izfar, izcap;
+    uint32_t qbase;
+    // tiling
+    int32_t tile_w, tile_h, tiles_x, tiles_y;
+    int64_t num_views;
+    int64_t num_blocks;
+    // outputs
+    uint8_t* out_cls;
+    float* out_depth;
+    int32_t cull;       // 1: cell + triangle + box frustum culling
+    int32_t vec_out;    // 1: output pointers are 16-byte aligned
+};
+
+struct AgentStepParams {
+    float* x; float* y; float* psi; float* speed; float* cos_h; float* sin_h;
+    const float* length;
+    const float* steer; const float* accel;
+    float dt, vmax;
+    int32_t count;
+};
+
+// Binning workspace (owned by the context).
+struct BinWork {
+    const float* verts;          // [T][9] original order
+    const uint8_t* cls;          // [T]
+    const int64_t* tri_offsets;  // [nw + 1] (device)
+    int64_t T;
+    int32_t num_worlds;
+    WorldGrid* grids;            // [nw]
+    int64_t total_cells;
+    float cell_size;
+    uint32_t* home;              // [T]
+    uint32_t* rank;              // [T]
+    uint32_t* count;             // [cells + 1] -> exclusive scan -> cell_start
+    uint32_t* aabb_bits;         // [cells][8] order-preserving bits (6 used)
+    uint32_t* margin_bits;       // [nw]
+    uint32_t* scan_tmp;          // block sums
+    int64_t scan_tmp_len;
+    float4* triA; float4* triB; float2* triC;
+    uint32_t* perm;              // [T]
+    float4* cell_lo; float4* cell_hi;
+};
+
+hipError_t launch_render(const RenderParams& p, hipStream_t s);
+hipError_t launch_bin(const BinWork& w, hipStream_t s);
+hipError_t launch_agents_step(const AgentStepParams& p, hipStream_t s);
+int64_t scan_tmp_needed(int64_t n);
+
+}  // namespace pictura

@@ -1,0 +1,267 @@
+"""Python binding of the HIP rasterizer library (libpictura.so).
+
+Argument marshalling only: every step of the path runs in the library's HIP
+kernels.  PyTorch provides device memory and the current HIP stream.  The
+functions carry the C ABI's names (include/pictura.h); `Renderer` wraps a
+context for convenience.  If the library is not built, importing this module
+raises: there is no fallback implementation.
+"""
+from __future__ import annotations
+
+import ctypes
+import dataclasses
+import os
+from typing import Optional
+
+import numpy as np
+
+HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(HERE, "libpictura.so")
+
+OK, EINVAL, ENOMEM, EDEVICE, ESTATE, ERANGE = 0, -1, -2, -3, -4, -5
+OPT_CULL, OPT_TILE = 1, 2
+MAX_CAMS = 8
+
+if not os.path.exists(LIB_PATH):
+    raise ImportError(f"{LIB_PATH} is missing: build the HIP library first (python __graft_entry__.py build)")
+
+_lib = ctypes.CDLL(LIB_PATH)
+
+
+class PicturaError(RuntimeError):
+    def __init__(self, status, msg):
+        super().__init__(f"pictura status {status}: {msg}")
+        self.status = status
+
+
+class _Scene(ctypes.Structure):
+    _fields_ = [("num_worlds", ctypes.c_int32), ("tri_offsets", ctypes.c_void_p), ("verts", ctypes.c_void_p),
+                ("cls", ctypes.c_void_p), ("bounds", ctypes.c_void_p)]
+
+
+class _Agents(ctypes.Structure):
+    _fields_ = [("num_worlds", ctypes.c_int32), ("agents_per_world", ctypes.c_int32)] + \
+               [(n, ctypes.c_void_p) for n in ("x", "y", "z0", "cos_h", "sin_h", "length", "width", "height", "cls")]
+
+
+class _Rig(ctypes.Structure):
+    _fields_ = [("num_cams", ctypes.c_int32), ("width", ctypes.c_int32), ("height", ctypes.c_int32),
+                ("fx", ctypes.c_float), ("fy", ctypes.c_float), ("cx", ctypes.c_float), ("cy", ctypes.c_float),
+                ("near_m", ctypes.c_float), ("far_m", ctypes.c_float),
+                ("mount", (ctypes.c_float * 5) * MAX_CAMS)]
+
+
+class _AgentState(ctypes.Structure):
+    _fields_ = [("count", ctypes.c_int32)] + \
+               [(n, ctypes.c_void_p) for n in ("x", "y", "psi", "speed", "cos_h", "sin_h", "length")]
+
+
+_P = ctypes.c_void_p
+_lib.pictura_create.argtypes = [ctypes.c_int32, ctypes.POINTER(_P)]
+_lib.pictura_create.restype = ctypes.c_int32
+_lib.pictura_destroy.argtypes = [_P]
+_lib.pictura_destroy.restype = None
+_lib.pictura_last_error.argtypes = [_P]
+_lib.pictura_last_error.restype = ctypes.c_char_p
+_lib.pictura_scene_upload.argtypes = [_P, ctypes.POINTER(_Scene), _P]
+_lib.pictura_scene_upload.restype = ctypes.c_int32
+_lib.pictura_bin_scene.argtypes = [_P, ctypes.c_float, _P]
+_lib.pictura_bin_scene.restype = ctypes.c_int32
+_lib.pictura_render_views.argtypes = [_P, ctypes.POINTER(_Agents), ctypes.POINTER(_Rig), _P, _P, _P]
+_lib.pictura_render_views.restype = ctypes.c_int32
+_lib.pictura_agents_step.argtypes = [_P, ctypes.POINTER(_AgentState), _P, _P, ctypes.c_float, ctypes.c_float, _P]
+_lib.pictura_agents_step.restype = ctypes.c_int32
+_lib.pictura_bins_info.argtypes = [_P, _P, _P, _P]
+_lib.pictura_bins_info.restype = ctypes.c_int32
+_lib.pictura_bins_copy.argtypes = [_P, _P, _P, _P]
+_lib.pictura_bins_copy.restype = ctypes.c_int32
+_lib.pictura_set_option.argtypes = [_P, ctypes.c_int32, ctypes.c_int32]
+_lib.pictura_set_option.restype = ctypes.c_int32
+
+EXPORTED = ["pictura_create", "pictura_destroy", "pictura_last_error", "pictura_scene_upload",
+            "pictura_bin_scene", "pictura_render_views", "pictura_agents_step", "pictura_bins_info",
+            "pictura_bins_copy", "pictura_set_option"]
+
+
+def _ptr(a) -> Optional[int]:
+    if a is None:
+        return None
+    if isinstance(a, np.ndarray):
+        return a.ctypes.data
+    return a.data_ptr()   # torch tensor
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is None:
+        import torch
+        return torch.cuda.current_stream().cuda_stream
+    if isinstance(stream, int):
+        return stream
+    return stream.cuda_stream
+
+
+def _check(ctx, st):
+    if st != OK:
+        msg = _lib.pictura_last_error(ctx).decode() if ctx else ""
+        raise PicturaError(st, msg)
+
+
+# --- functions with the C ABI's names ---------------------------------------
+
+def pictura_create(device: int = 0):
+    h = _P()
+    st = _lib.pictura_create(int(device), ctypes.byref(h))
+    if st != OK:
+        raise PicturaError(st, "pictura_create failed (no HIP device?)")
+    return h
+
+
+def pictura_destroy(ctx):
+    _lib.pictura_destroy(ctx)
+
+
+def pictura_last_error(ctx) -> str:
+    return _lib.pictura_last_error(ctx).decode()
+
+
+def pictura_scene_upload(ctx, scene, stream=None):
+    """scene: object with num_worlds, tri_offsets (int64), verts (float32 [T,9]),
+    cls (uint8), bounds (float32 [nw,4]) as host NumPy arrays."""
+    offs = np.ascontiguousarray(scene.tri_offsets, np.int64)
+    verts = np.ascontiguousarray(scene.verts, np.float32)
+    cls = np.ascontiguousarray(scene.cls, np.uint8)
+    bounds = np.ascontiguousarray(scene.bounds, np.float32)
+    s = _Scene(int(scene.num_worlds), offs.ctypes.data, verts.ctypes.data if verts.size else None,
+               cls.ctypes.data if cls.size else None, bounds.ctypes.data)
+    _check(ctx, _lib.pictura_scene_upload(ctx, ctypes.byref(s), _stream(stream)))
+
+
+def pictura_bin_scene(ctx, cell_size_m: float, stream=None):
+    _check(ctx, _lib.pictura_bin_scene(ctx, float(cell_size_m), _stream(stream)))
+
+
+def make_rig(rig) -> _Rig:
+    r = _Rig()
+    r.num_cams = int(rig.mount.shape[0])
+    r.width, r.height = int(rig.width), int(rig.height)
+    r.fx, r.fy, r.cx, r.cy = float(rig.fx), float(rig.fy), float(rig.cx), float(rig.cy)
+    r.near_m, r.far_m = float(rig.near), float(rig.far)
+    m = np.asarray(rig.mount, np.float32)
+    for k in range(min(r.num_cams, MAX_CAMS)):
+        for q in range(5):
+            r.mount[k][q] = float(m[k, q])
+    return r
+
+
+def pictura_render_views(ctx, agents, rig, out_cls, out_depth, stream=None):
+    """agents: DeviceAgents (torch CUDA tensors); rig: scenegen.Rig-like;
+    out_cls uint8 / out_depth float32 CUDA tensors of V*H*W elements."""
+    a = _Agents(int(agents.num_worlds), int(agents.agents_per_world),
+                *[_ptr(getattr(agents, n)) for n in ("x", "y", "z0", "cos_h", "sin_h", "length", "width", "height",
+                                                     "cls")])
+    r = make_rig(rig) if not isinstance(rig, _Rig) else rig
+    _check(ctx, _lib.pictura_render_views(ctx, ctypes.byref(a), ctypes.byref(r), _ptr(out_cls), _ptr(out_depth),
+                                          _stream(stream)))
+
+
+def pictura_agents_step(ctx, state, steer, accel, dt: float = 0.1, vmax: float = 20.0, stream=None):
+    s = _AgentState(int(state.x.numel()), *[_ptr(getattr(state, n)) for n in
+                                           ("x", "y", "psi", "speed", "cos_h", "sin_h", "length")])
+    _check(ctx, _lib.pictura_agents_step(ctx, ctypes.byref(s), _ptr(steer), _ptr(accel), float(dt), float(vmax),
+                                         _stream(stream)))
+
+
+def pictura_bins_info(ctx, num_worlds: int):
+    dims = np.empty((num_worlds, 2), np.int32)
+    base = np.empty(num_worlds + 1, np.int64)
+    total = ctypes.c_int64()
+    _check(ctx, _lib.pictura_bins_info(ctx, dims.ctypes.data, base.ctypes.data, ctypes.addressof(total)))
+    return dims, base, int(total.value)
+
+
+def pictura_bins_copy(ctx, total_cells: int, num_tris: int):
+    start = np.empty(total_cells + 1, np.uint32)
+    aabb = np.empty((total_cells, 6), np.float32)
+    perm = np.empty(max(num_tris, 1), np.uint32)
+    _check(ctx, _lib.pictura_bins_copy(ctx, start.ctypes.data, aabb.ctypes.data, perm.ctypes.data))
+    return start, aabb, perm[:num_tris]
+
+
+def pictura_set_option(ctx, option: int, value: int):
+    _check(ctx, _lib.pictura_set_option(ctx, int(option), int(value)))
+
+
+# --- device-resident agents ------------------------------------------------------
+
+@dataclasses.dataclass
+class DeviceAgents:
+    num_worlds: int
+    agents_per_world: int
+    x: "object"
+    y: "object"
+    z0: "object"
+    cos_h: "object"
+    sin_h: "object"
+    length: "object"
+    width: "object"
+    height: "object"
+    cls: "object"
+    psi: "object"
+    speed: "object"
+
+    @staticmethod
+    def from_host(agents, device="cuda"):
+        import torch
+        f = lambda a, dt=torch.float32: torch.as_tensor(np.ascontiguousarray(a), dtype=dt).to(device)
+        return DeviceAgents(int(agents.num_worlds), int(agents.agents_per_world),
+                            *[f(getattr(agents, n)) for n in ("x", "y", "z0", "cos_h", "sin_h", "length", "width",
+                                                             "height")],
+                            f(agents.cls, torch.uint8), f(agents.psi), f(agents.speed))
+
+
+class Renderer:
+    """Owns a library context, its scene and bins."""
+
+    def __init__(self, device: int = 0):
+        self.ctx = pictura_create(device)
+        self.num_worlds = 0
+        self.num_tris = 0
+
+    def close(self):
+        if self.ctx:
+            pictura_destroy(self.ctx)
+            self.ctx = None
+
+    def __del__(self):
+        try:
+            self.close()
+        except Exception:
+            pass
+
+    def upload(self, scene, cell_size: float, stream=None):
+        pictura_scene_upload(self.ctx, scene, stream)
+        pictura_bin_scene(self.ctx, cell_size, stream)
+        self.num_worlds = int(scene.num_worlds)
+        self.num_tris = int(scene.tri_offsets[-1])
+
+    def render(self, agents: DeviceAgents, rig, out_cls=None, out_depth=None, stream=None):
+        import torch
+        V = agents.num_worlds * agents.agents_per_world * int(rig.mount.shape[0])
+        shape = (V, int(rig.height), int(rig.width))
+        if out_cls is None:
+            out_cls = torch.empty(shape, dtype=torch.uint8, device=agents.x.device)
+        if out_depth is None:
+            out_depth = torch.empty(shape, dtype=torch.float32, device=agents.x.device)
+        pictura_render_views(self.ctx, agents, rig, out_cls, out_depth, stream)
+        return out_cls, out_depth
+
+    def agents_step(self, agents: DeviceAgents, steer, accel, dt=0.1, vmax=20.0, stream=None):
+        pictura_agents_step(self.ctx, agents, steer, accel, dt, vmax, stream)
+
+    def set_option(self, option, value):
+        pictura_set_option(self.ctx, option, value)
+
+    def bins(self):
+        dims, base, total = pictura_bins_info(self.ctx, self.num_worlds)
+        start, aabb, perm = pictura_bins_copy(self.ctx, total, self.num_tris)
+        return dict(dims=dims, cell_base=base, cell_start=start, aabb=aabb, perm=perm)

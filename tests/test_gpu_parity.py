@@ -1,0 +1,284 @@
+"""GPU parity: the HIP path (through the C ABI) against the CPU oracle.
+
+Every test renders on the GPU and compares with the oracle on the same seeded
+inputs: whole images for the small workloads, seeded samples of views for
+the large ones (the GPU renders every view of the batch in the same launch
+configuration the benchmark times; the oracle computes the sampled views one
+by one).
+"""
+import functools
+
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from paper_2607_26005_amd import scenegen as sg
+from tests.parity import assert_parity, compare
+from tests.scenes import make_agents, make_rig, make_scene, quad
+
+pytestmark = pytest.mark.gpu
+
+
+def _torch():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no HIP device")
+    return torch
+
+
+@functools.lru_cache(maxsize=None)
+def workload(cfg, worlds=None):
+    return sg.make_config(cfg, num_worlds=worlds)
+
+
+@pytest.fixture(scope="module")
+def lib():
+    _torch()
+    from paper_2607_26005_amd import pictura
+    return pictura
+
+
+def render_gpu(pictura, wl_scene, agents, rig, cell, cull=1, tile=0):
+    torch = _torch()
+    r = pictura.Renderer(0)
+    try:
+        r.set_option(pictura.OPT_CULL, cull)
+        r.set_option(pictura.OPT_TILE, tile)
+        r.upload(wl_scene, cell)
+        da = pictura.DeviceAgents.from_host(agents)
+        c, d = r.render(da, rig)
+        torch.cuda.synchronize()
+        return c, d
+    finally:
+        r.close()
+
+
+def check_views(pictura, wl, view_ids, label, cull=1, tile=0, cell=None):
+    cell = wl.cell_size if cell is None else cell
+    print(f"[{label}] render {wl.num_views} views {wl.rig.width}x{wl.rig.height} cull={cull} tile={tile}", flush=True)
+    c, d = render_gpu(pictura, wl.scene, wl.agents, wl.rig, cell, cull, tile)
+    idx = np.asarray(view_ids, np.int64)
+    import torch
+    ti = torch.as_tensor(idx, device=c.device)
+    gc = c.index_select(0, ti).cpu().numpy()
+    gd = d.index_select(0, ti).cpu().numpy()
+    del c, d
+    ora = O.render(wl.scene, wl.agents, wl.rig, view_ids=idx)
+    s = assert_parity(gc, gd, ora, label)
+    print(f"[{label}] {s}", flush=True)
+    return s
+
+
+def sample_views(n_views, k, seed):
+    rng = np.random.default_rng(seed)
+    if k >= n_views:
+        return np.arange(n_views)
+    return np.sort(rng.choice(n_views, size=k, replace=False))
+
+
+def test_tiny_all_views(lib):
+    wl = workload(1)
+    s = check_views(lib, wl, np.arange(wl.num_views), "tiny")
+    assert s["mismatches"] == 0
+
+
+def test_small_batch_sampled(lib):
+    wl = workload(2)
+    check_views(lib, wl, sample_views(wl.num_views, 384, 21), "small_batch")
+
+
+def test_dense_traffic_sampled(lib):
+    wl = workload(3)
+    check_views(lib, wl, sample_views(wl.num_views, 384, 22), "dense_traffic")
+
+
+def test_headline_full_size_sampled(lib):
+    # the benchmark's workload and launch: 1024 worlds x 64 agents x 4 cameras
+    wl = workload(4)
+    check_views(lib, wl, sample_views(wl.num_views, 256, 23), "headline")
+
+
+def test_highres_tiled_sampled(lib):
+    wl = workload(5, 4)   # first 4 worlds of the high-res workload (128x128, 2x2 tiles)
+    check_views(lib, wl, sample_views(wl.num_views, 48, 24), "highres")
+
+
+# ---- invariances: culling, tiling, cell size, permutation, duplication -------
+
+def _small():
+    return workload(2, 2)
+
+
+def test_cull_off_and_forced_tiles_identical(lib):
+    wl = _small()
+    base = render_gpu(lib, wl.scene, wl.agents, wl.rig, wl.cell_size)
+    for cull, tile, cell in ((0, 0, wl.cell_size), (1, 16, wl.cell_size), (1, 24, wl.cell_size),
+                             (1, 0, 8.0), (1, 0, 64.0), (0, 32, 32.0)):
+        print(f"[invariance] cull={cull} tile={tile} cell={cell}", flush=True)
+        c, d = render_gpu(lib, wl.scene, wl.agents, wl.rig, cell, cull, tile)
+        assert bool((c == base[0]).all()), (cull, tile, cell)
+        assert bool((d == base[1]).all()), (cull, tile, cell)
+
+
+def test_permutation_duplication_identical(lib):
+    wl = _small()
+    base = render_gpu(lib, wl.scene, wl.agents, wl.rig, wl.cell_size)
+    sc = wl.scene
+    rng = np.random.default_rng(3)
+    verts, cls, offs = [], [], [0]
+    for w in range(sc.num_worlds):
+        v, c = sc.world(w)
+        p = rng.permutation(len(v))
+        dup = rng.choice(len(v), size=len(v) // 10, replace=False)
+        verts.append(np.concatenate([v[p], v[dup]]))
+        cls.append(np.concatenate([c[p], c[dup]]))
+        offs.append(offs[-1] + len(verts[-1]))
+    sc2 = sg.Scene(sc.num_worlds, np.ascontiguousarray(np.concatenate(verts)), np.concatenate(cls),
+                   np.asarray(offs, np.int64), sc.bounds)
+    c, d = render_gpu(lib, sc2, wl.agents, wl.rig, wl.cell_size)
+    assert bool((c == base[0]).all())
+    assert bool((d == base[1]).all())
+
+
+# ---- edge cases ----------------------------------------------------------------
+
+def test_ragged_sizes_and_tiles(lib):
+    # non-square, not a multiple of 16 (scalar write path), ragged 64x64 tiles
+    wl = workload(2, 1)
+    for (W, H) in ((40, 24), (100, 70), (17, 129)):
+        rig = sg.Rig(width=W, height=H, fx=W / 2.0, fy=W / 2.0, cx=W / 2.0, cy=H / 2.0, near=0.5, far=100.0,
+                     mount=wl.rig.mount)
+        wl2 = sg.Workload(wl.name, 2, 1, wl.scene, wl.agents, rig, wl.cell_size, wl.world_size)
+        check_views(lib, wl2, sample_views(wl2.num_views, 64, W), f"ragged {W}x{H}")
+
+
+def test_empty_world_and_lone_agent(lib):
+    # world 0 has no triangles, world 1 one quad; one agent per world (no boxes)
+    q = np.asarray(quad((8.0, -2.0, -2.0), (8.0, 2.0, -2.0), (8.0, 2.0, 2.0), (8.0, -2.0, 2.0)), np.float32)
+    scene = sg.Scene(2, np.ascontiguousarray(q.reshape(-1, 9)), np.array([7, 7], np.uint8),
+                     np.array([0, 0, 2], np.int64), np.array([[-50, -50, 50, 50]] * 2, np.float32))
+    ag = make_agents([(0.0, 0.0, 0.0, 1.0, 0.0, 4.0, 2.0, 1.5, 3), (0.0, 0.0, 0.0, 1.0, 0.0, 4.0, 2.0, 1.5, 3)],
+                     num_worlds=2)
+    rig = make_rig(mounts=((0.0, 0.0, 0.0, 1.0, 0.0), (0.0, 0.0, 0.0, 0.0, 1.0)))
+    wl = sg.Workload("edge", 0, 0, scene, ag, rig, 16.0, 100.0)
+    check_views(lib, wl, np.arange(wl.num_views), "empty+lone")
+
+
+def test_camera_inside_box_and_near_clipped_ground(lib):
+    G = 1000.0
+    tris = quad((-G, -G, 0.0), (G, -G, 0.0), (G, G, 0.0), (-G, G, 0.0))
+    scene = make_scene(tris, [0, 0])
+    rows = [(0.0, 0.0, 0.0, 1.0, 0.0, 4.5, 1.9, 1.5, 3),
+            (1.0, 0.2, 0.0, 0.6, 0.8, 4.5, 1.9, 1.7, 6),   # camera of agent 0 is inside this box
+            (12.0, 3.0, 0.0, 0.0, 1.0, 4.5, 1.9, 1.5, 3)]
+    ag = make_agents(rows)
+    rig = make_rig(mounts=((0.0, 0.0, 1.5, 1.0, 0.0), (0.5, 0.1, 1.2, 0.0, -1.0)), far=100.0)
+    wl = sg.Workload("inside", 0, 0, scene, ag, rig, 16.0, 2000.0)
+    check_views(lib, wl, np.arange(wl.num_views), "inside-box")
+
+
+def test_random_small_scenes(lib):
+    from tests.test_oracle_pins import _random_scene
+    for seed in range(12):
+        scene, ag = _random_scene(seed)
+        rig = make_rig(res=32, near=0.5, far=30.0, mounts=((0.0, 0.0, 1.0, 1.0, 0.0), (0.0, 0.0, 1.0, -1.0, 0.0)))
+        wl = sg.Workload("random", 0, seed, scene, ag, rig, 4.0, 2000.0)
+        check_views(lib, wl, np.arange(wl.num_views), f"random seed {seed}")
+
+
+# ---- binner and agent step -----------------------------------------------------
+
+def test_binner_matches_oracle(lib):
+    wl = workload(2, 3)
+    sc = wl.scene
+    print("[binner] 3 worlds", flush=True)
+    r = lib.Renderer(0)
+    try:
+        r.upload(sc, 16.0)
+        b = r.bins()
+    finally:
+        r.close()
+    ob = O.bin_scene(sc, 16.0)
+    assert np.array_equal(b["dims"], ob["dims"])
+    assert np.array_equal(b["cell_base"], ob["cell_base"])
+    counts = np.diff(b["cell_start"].astype(np.int64))
+    assert np.array_equal(counts, ob["count"].astype(np.int64))
+    ne = counts > 0
+    assert np.array_equal(b["aabb"][ne], ob["aabb"][ne])
+    # each cell holds exactly the oracle's set of triangles
+    perm = b["perm"].astype(np.int64)
+    assert np.array_equal(np.sort(perm), np.arange(sc.num_tris))
+    cell_of_slot = np.repeat(np.arange(len(counts)), counts)
+    assert np.array_equal(ob["home"][perm], cell_of_slot)
+
+
+def test_agents_step_matches_oracle(lib):
+    torch = _torch()
+    wl = workload(4, 8)
+    ag = wl.agents.copy()
+    steer, accel = sg.controls(ag.count, 5, seed=3)
+    da = lib.DeviceAgents.from_host(ag)
+    r = lib.Renderer(0)
+    try:
+        for s in range(5):
+            print(f"[agents_step] step {s}", flush=True)
+            st = torch.as_tensor(steer[s], device="cuda")
+            ac = torch.as_tensor(accel[s], device="cuda")
+            r.agents_step(da, st, ac, dt=0.1, vmax=20.0)
+            out = O.agents_step(ag, steer[s], accel[s], dt=0.1, vmax=20.0)
+            torch.cuda.synchronize()
+            gx, gy = da.x.cpu().numpy(), da.y.cpu().numpy()
+            assert np.max(np.abs(gx - out["x"])) < 2e-4 * (s + 1)
+            assert np.max(np.abs(gy - out["y"])) < 2e-4 * (s + 1)
+            assert np.max(np.abs(da.speed.cpu().numpy() - out["speed"])) < 1e-5
+            dpsi = np.angle(np.exp(1j * (da.psi.cpu().numpy() - out["psi"])))
+            assert np.max(np.abs(dpsi)) < 1e-5 * (s + 1)
+            assert np.max(np.abs(da.cos_h.cpu().numpy() - out["cos_h"])) < 1e-5 * (s + 1)
+            assert np.max(np.abs(da.sin_h.cpu().numpy() - out["sin_h"])) < 1e-5 * (s + 1)
+            # continue both sides from their own state
+            ag.x, ag.y = out["x"].astype(np.float32), out["y"].astype(np.float32)
+            ag.psi, ag.speed = out["psi"].astype(np.float32), out["speed"].astype(np.float32)
+    finally:
+        r.close()
+
+
+# ---- C ABI error handling (host-side checks, no kernel launched) ---------------
+
+def test_abi_errors(lib):
+    _torch()
+    ctx = lib.pictura_create(0)
+    try:
+        wl = workload(1)
+        da = lib.DeviceAgents.from_host(wl.agents)
+        import torch
+        oc = torch.empty(8 * 64 * 64, dtype=torch.uint8, device="cuda")
+        od = torch.empty(8 * 64 * 64, dtype=torch.float32, device="cuda")
+        with pytest.raises(lib.PicturaError) as e:
+            lib.pictura_render_views(ctx, da, wl.rig, oc, od)
+        assert e.value.status == lib.ESTATE
+        with pytest.raises(lib.PicturaError) as e:
+            lib.pictura_bin_scene(ctx, 16.0)
+        assert e.value.status == lib.ESTATE
+        lib.pictura_scene_upload(ctx, wl.scene)
+        with pytest.raises(lib.PicturaError) as e:
+            lib.pictura_bin_scene(ctx, -1.0)
+        assert e.value.status == lib.EINVAL
+        lib.pictura_bin_scene(ctx, 16.0)
+        bad = sg.Rig(64, 64, 32.0, 32.0, 32.0, 32.0, 1.0, 0.5, wl.rig.mount)
+        with pytest.raises(lib.PicturaError) as e:
+            lib.pictura_render_views(ctx, da, bad, oc, od)
+        assert e.value.status == lib.EINVAL
+        huge = sg.Rig(64, 64, 32.0, 32.0, 32.0, 32.0, 1e-30, 1e30, wl.rig.mount)
+        with pytest.raises(lib.PicturaError) as e:
+            lib.pictura_render_views(ctx, da, huge, oc, od)
+        assert e.value.status == lib.EINVAL
+        with pytest.raises(lib.PicturaError) as e:
+            lib.pictura_set_option(ctx, lib.OPT_TILE, 3)
+        assert e.value.status == lib.EINVAL
+        # the context is still usable after errors
+        lib.pictura_render_views(ctx, da, wl.rig, oc, od)
+        torch.cuda.synchronize()
+        ora = O.render(wl.scene, wl.agents, wl.rig)
+        assert_parity(oc.view(8, 64, 64).cpu().numpy(), od.view(8, 64, 64).cpu().numpy(), ora, "after-errors")
+    finally:
+        lib.pictura_destroy(ctx)
