@@ -161,8 +161,30 @@ pictura_status pictura_bins_copy(pictura_ctx ctx, uint32_t* cell_start, float* c
 
 #define PICTURA_OPT_CULL   1 /* 1 (default): cell + triangle frustum culling; 0: every triangle of the world */
 #define PICTURA_OPT_TILE   2 /* 0 (default): 64x64 LDS tiles; n in 8..64: force n x n tiles */
-/* Set a context option.  Results must not change with either option. */
+#define PICTURA_OPT_STATS  3 /* 1: count the render kernel's work (cells, triangles, pixels); 0 (default): off */
+/* Set a context option.  Images never depend on any option. */
 pictura_status pictura_set_option(pictura_ctx ctx, int32_t option, int32_t value);
+
+/* Copy the render kernel's accumulated work counters (PICTURA_OPT_STATS) to
+ * host memory (synchronous): out[k], k < n, in this order: view tiles, cells
+ * in the gathered rectangles, cells passing the frustum test, triangles of
+ * those cells, boxes passing, box triangles, first-pass survivors, exact
+ * batches, triangles clipped at near, snapped triangles with pixels in the
+ * tile, of those with non-zero area and a depth plane, triangles queued for
+ * a whole wave, pixels tested by single lanes, (unused), wave-queue overflows,
+ * candidate passes, then shader-clock cycles summed over waves spent in:
+ * prologue, block-wide phase setup, first pass, exact pass, end-of-phase
+ * barriers, whole-wave raster (part of the exact pass), final barrier and
+ * write-out.  reset != 0 zeroes the counters. */
+pictura_status pictura_stats_copy(pictura_ctx ctx, uint64_t* out, int32_t n, int32_t reset);
+
+/* Device self-check of the reciprocal the kernels use in place of IEEE
+ * division where the argument lies in [2^-12, 2^20) (hardware reciprocal plus
+ * one fused Newton step): *mismatches receives the number of fp32 values x
+ * whose bit patterns lie in [lo_bits, lo_bits + count) for which it differs
+ * from the correctly rounded 1.0f / x.  Synchronous.  EINVAL: null output or
+ * a range reaching past the finite floats. */
+pictura_status pictura_selftest_rcp(pictura_ctx ctx, uint32_t lo_bits, uint32_t count, uint64_t* mismatches);
 
 #ifdef __cplusplus
 }

@@ -4,8 +4,9 @@ import subprocess
 
 HERE = os.path.dirname(os.path.abspath(__file__))
 CSRC = os.path.join(HERE, "csrc")
+INCLUDE = os.path.join(os.path.dirname(HERE), "include")
 LIB = os.path.join(HERE, "libpictura.so")
-SOURCES = ["pictura_kernels.hip", "pictura_abi.hip"]
+SOURCES = ["pictura_binner.hip", "pictura_render.hip", "pictura_abi.hip"]
 
 # fp32 rules need IEEE arithmetic: no contraction, correctly rounded division,
 # denormals kept.  Packed fp32 instructions are disabled.
@@ -24,7 +25,7 @@ def build(verbose: bool = False) -> str:
     procs = []
     for src in SOURCES:
         obj = os.path.join(CSRC, src.replace(".hip", ".o"))
-        cmd = [hipcc, *HIPCC_FLAGS, "-c", os.path.join(CSRC, src), "-o", obj]
+        cmd = [hipcc, *HIPCC_FLAGS, "-I", INCLUDE, "-c", os.path.join(CSRC, src), "-o", obj]
         if verbose:
             print(" ".join(cmd))
         procs.append(subprocess.Popen(cmd))

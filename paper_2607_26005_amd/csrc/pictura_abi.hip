@@ -7,7 +7,7 @@
 #include <string>
 #include <vector>
 
-#include "../../include/pictura.h"
+#include "pictura.h"
 #include "pictura_internal.h"
 
 using namespace pictura;
@@ -45,6 +45,8 @@ struct pictura_ctx_s {
     // options
     int cull = 1;
     int tile = 0;
+    int stats_on = 0;
+    unsigned long long* stats = nullptr;   // [kNumStats] device counters
 };
 
 namespace {
@@ -95,7 +97,7 @@ void free_bins(pictura_ctx c)
 void free_scene(pictura_ctx c)
 {
     free_bins(c);
-    dfree(c->verts); dfree(c->cls); dfree(c->offsets_d);
+    dfree(c->verts); dfree(c->cls); dfree(c->offsets_d); dfree(c->stats);
     c->have_scene = false;
     c->T = 0;
     c->num_worlds = 0;
@@ -269,7 +271,8 @@ pictura_status pictura_render_views(pictura_ctx c, const pictura_agents* ag, con
     if (!c->binned) return fail(c, PICTURA_ESTATE, "render_views: scene not binned");
     if (ag->num_worlds != c->num_worlds)
         return fail(c, PICTURA_EINVAL, "render_views: agents.num_worlds %d != scene num_worlds %d", ag->num_worlds, c->num_worlds);
-    if (ag->agents_per_world < 1) return fail(c, PICTURA_EINVAL, "render_views: agents_per_world must be >= 1");
+    if (ag->agents_per_world < 1 || ag->agents_per_world > (1 << 26))
+        return fail(c, PICTURA_EINVAL, "render_views: agents_per_world must be 1..2^26");
     if (!ag->x || !ag->y || !ag->z0 || !ag->cos_h || !ag->sin_h || !ag->length || !ag->width || !ag->height || !ag->cls)
         return fail(c, PICTURA_EINVAL, "render_views: null agent array");
     if (rig->num_cams < 1 || rig->num_cams > PICTURA_MAX_CAMS) return fail(c, PICTURA_EINVAL, "render_views: num_cams must be 1..8");
@@ -304,6 +307,9 @@ pictura_status pictura_render_views(pictura_ctx c, const pictura_agents* ag, con
     P.fx256 = 256.0f * P.fx; P.fy256 = 256.0f * P.fy; P.cx256 = 256.0f * P.cx; P.cy256 = 256.0f * P.cy;
     P.rfx = 1.0f / P.fx; P.rfy = 1.0f / P.fy;
     P.izfar = izfar; P.izcap = izcap; P.qbase = f2u(izcap) >> 3;
+    P.cabs = std::fabs(P.cx) > std::fabs(P.cy) ? std::fabs(P.cx) : std::fabs(P.cy);
+    // decoded inverse depths lie in [1/far (1 - 2^-20), IZCAP]
+    P.fast_decode = (izfar >= 0.000244140625f * 1.0000038f && izcap < 1048576.0f) ? 1 : 0;
     int tw = 64, th = 64;
     if (c->tile > 0) { tw = c->tile; th = c->tile; }
     tw = tw < P.W ? tw : P.W;
@@ -318,6 +324,15 @@ pictura_status pictura_render_views(pictura_ctx c, const pictura_agents* ag, con
     P.cull = c->cull;
     P.vec_out = ((reinterpret_cast<uintptr_t>(out_cls) | reinterpret_cast<uintptr_t>(out_depth)) & 15u) == 0 ? 1 : 0;
     DeviceGuard dg(c->device);
+    if (c->stats_on) {
+        hipError_t se = hipSuccess;
+        if (!c->stats) {
+            if ((se = dalloc(c->stats, (size_t)kNumStats)) != hipSuccess) return hip_fail(c, se, "render_views stats alloc");
+            if ((se = hipMemset(c->stats, 0, sizeof(unsigned long long) * kNumStats)) != hipSuccess)
+                return hip_fail(c, se, "render_views stats clear");
+        }
+        P.stats = c->stats;
+    }
     hipError_t e = launch_render(P, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(c, e, "render_views launch");
     return PICTURA_OK;
@@ -391,12 +406,55 @@ pictura_status pictura_set_option(pictura_ctx c, int32_t option, int32_t value)
         c->cull = value;
         return PICTURA_OK;
     }
+    if (option == PICTURA_OPT_STATS) {
+        if (value != 0 && value != 1) return fail(c, PICTURA_EINVAL, "set_option: STATS must be 0 or 1");
+        c->stats_on = value;
+        return PICTURA_OK;
+    }
     if (option == PICTURA_OPT_TILE) {
         if (value != 0 && (value < 8 || value > 64)) return fail(c, PICTURA_EINVAL, "set_option: TILE must be 0 or 8..64");
         c->tile = value;
         return PICTURA_OK;
     }
     return fail(c, PICTURA_EINVAL, "set_option: unknown option %d", option);
+}
+
+pictura_status pictura_selftest_rcp(pictura_ctx c, uint32_t lo_bits, uint32_t count, uint64_t* mismatches)
+{
+    if (!c) return PICTURA_EINVAL;
+    c->err.clear();
+    if (!mismatches) return fail(c, PICTURA_EINVAL, "selftest_rcp: null output");
+    if ((uint64_t)lo_bits + count > 0x7F800000ull) return fail(c, PICTURA_EINVAL, "selftest_rcp: range leaves the finite floats");
+    DeviceGuard dg(c->device);
+    unsigned long long* d = nullptr;
+    hipError_t e;
+    if ((e = hipMalloc((void**)&d, sizeof(unsigned long long))) != hipSuccess) return hip_fail(c, e, "selftest_rcp alloc");
+    unsigned long long h = 0;
+    if ((e = hipMemcpy(d, &h, sizeof h, hipMemcpyHostToDevice)) != hipSuccess ||
+        (e = launch_rcp_check(lo_bits, count, d, nullptr)) != hipSuccess ||
+        (e = hipMemcpy(&h, d, sizeof h, hipMemcpyDeviceToHost)) != hipSuccess) {
+        (void)hipFree(d);
+        return hip_fail(c, e, "selftest_rcp");
+    }
+    (void)hipFree(d);
+    *mismatches = (uint64_t)h;
+    return PICTURA_OK;
+}
+
+pictura_status pictura_stats_copy(pictura_ctx c, uint64_t* out, int32_t n, int32_t reset)
+{
+    if (!c) return PICTURA_EINVAL;
+    c->err.clear();
+    if (!out || n < 0) return fail(c, PICTURA_EINVAL, "stats_copy: bad output");
+    DeviceGuard dg(c->device);
+    hipError_t e;
+    if ((e = hipDeviceSynchronize()) != hipSuccess) return hip_fail(c, e, "stats_copy sync");
+    unsigned long long tmp[kNumStats] = {0};
+    if (c->stats && (e = hipMemcpy(tmp, c->stats, sizeof tmp, hipMemcpyDeviceToHost)) != hipSuccess)
+        return hip_fail(c, e, "stats_copy");
+    for (int k = 0; k < n; ++k) out[k] = k < kNumStats ? (uint64_t)tmp[k] : 0;
+    if (reset && c->stats && (e = hipMemset(c->stats, 0, sizeof tmp)) != hipSuccess) return hip_fail(c, e, "stats_copy reset");
+    return PICTURA_OK;
 }
 
 }  // extern "C"

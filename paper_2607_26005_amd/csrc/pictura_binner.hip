@@ -1,0 +1,216 @@
+// HIP kernels for gfx950: uniform-grid scene binner (count, exclusive scan,
+// scatter into cell order, per-cell bounding boxes) and the kinematic
+// bicycle step of the agents.
+#include "pictura_device.h"
+
+#pragma clang fp contract(off)
+
+namespace pictura {
+
+// ---------------------------------------------------------------------------
+// binner
+// ---------------------------------------------------------------------------
+
+__global__ void bin_init_kernel(uint32_t* count, uint32_t* aabb_bits, int64_t cells, uint32_t* margin_bits, int nw)
+{
+    int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (c <= cells) count[c] = 0;
+    if (c < cells) {
+        uint32_t* a = aabb_bits + 8 * c;
+        const uint32_t pinf = 0xFF800000u, ninf = 0x007FFFFFu; // ord(+inf), ord(-inf)
+        a[0] = pinf; a[1] = pinf; a[2] = pinf;
+        a[3] = ninf; a[4] = ninf; a[5] = ninf;
+    }
+    if (c < nw) margin_bits[c] = 0;
+}
+
+__device__ __forceinline__ int world_of(const int64_t* offs, int nw, int64_t t)
+{
+    int lo = 0, hi = nw - 1;   // largest w with offs[w] <= t
+    while (lo < hi) {
+        int mid = (lo + hi + 1) >> 1;
+        if (offs[mid] <= t) lo = mid; else hi = mid - 1;
+    }
+    return lo;
+}
+
+__global__ void bin_count_kernel(BinWork W)
+{
+    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= W.T) return;
+    const int w = world_of(W.tri_offsets, W.num_worlds, t);
+    const WorldGrid g = W.grids[w];
+    const float* v = W.verts + 9 * t;
+    float lo[3], hi[3];
+#pragma unroll
+    for (int d = 0; d < 3; ++d) {
+        lo[d] = fminf(fminf(v[d], v[3 + d]), v[6 + d]);
+        hi[d] = fmaxf(fmaxf(v[d], v[3 + d]), v[6 + d]);
+    }
+    const float mx = (lo[0] + hi[0]) * 0.5f, my = (lo[1] + hi[1]) * 0.5f;
+    const float fx = floorf((mx - g.ox) / W.cell_size);
+    const float fy = floorf((my - g.oy) / W.cell_size);
+    const int ix = !(fx >= 0.0f) ? 0 : (fx >= (float)(g.nx - 1) ? g.nx - 1 : (int)fx);
+    const int iy = !(fy >= 0.0f) ? 0 : (fy >= (float)(g.ny - 1) ? g.ny - 1 : (int)fy);
+    const uint32_t c = (uint32_t)(g.cell_base + iy * g.nx + ix);
+    W.home[t] = c;
+    W.rank[t] = atomicAdd(&W.count[c], 1u);
+    uint32_t* a = W.aabb_bits + 8 * (int64_t)c;
+#pragma unroll
+    for (int d = 0; d < 3; ++d) {
+        atomicMin(&a[d], ord_bits(lo[d]));
+        atomicMax(&a[3 + d], ord_bits(hi[d]));
+    }
+}
+
+// Three-phase exclusive scan over n = cells + 1 counters (in place).
+constexpr int kScanItems = 4;
+constexpr int kScanTile = kBlock * kScanItems;
+
+int64_t scan_tmp_needed(int64_t n) { return (n + kScanTile - 1) / kScanTile + 1; }
+
+__global__ __launch_bounds__(kBlock) void scan_tiles_kernel(uint32_t* data, int64_t n, uint32_t* tile_sums)
+{
+    __shared__ uint32_t s_wave[kBlock / 64];
+    const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
+    uint32_t v[kScanItems], sum = 0;
+#pragma unroll
+    for (int k = 0; k < kScanItems; ++k) {
+        v[k] = (base + k < n) ? data[base + k] : 0u;
+        sum += v[k];
+    }
+    uint32_t total;
+    uint32_t off = block_excl_scan(sum, s_wave, total);
+#pragma unroll
+    for (int k = 0; k < kScanItems; ++k) {
+        if (base + k < n) data[base + k] = off;
+        off += v[k];
+    }
+    if (threadIdx.x == 0) tile_sums[blockIdx.x] = total;
+}
+
+__global__ __launch_bounds__(kBlock) void scan_sums_kernel(uint32_t* sums, int64_t n)
+{
+    __shared__ uint32_t s_wave[kBlock / 64];
+    uint32_t carry = 0;
+    for (int64_t b = 0; b < n; b += kBlock) {
+        const int64_t i = b + threadIdx.x;
+        const uint32_t v = i < n ? sums[i] : 0u;
+        uint32_t total;
+        const uint32_t off = block_excl_scan(v, s_wave, total);
+        if (i < n) sums[i] = carry + off;
+        carry += total;
+    }
+}
+
+__global__ void scan_add_kernel(uint32_t* data, int64_t n, const uint32_t* tile_sums)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i < n) data[i] += tile_sums[i / kScanTile];
+}
+
+__global__ void bin_scatter_kernel(BinWork W)
+{
+    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (t >= W.T) return;
+    const uint32_t dst = W.count[W.home[t]] + W.rank[t];   // count[] now holds cell starts
+    const float* v = W.verts + 9 * t;
+    W.triA[dst] = make_float4(v[0], v[1], v[2], v[3]);
+    W.triB[dst] = make_float4(v[4], v[5], v[6], v[7]);
+    W.triC[dst] = make_float2(v[8], __uint_as_float((uint32_t)W.cls[t]));
+    W.perm[dst] = (uint32_t)t;
+}
+
+__device__ __forceinline__ int world_of_cell(const WorldGrid* g, int nw, int64_t c)
+{
+    int lo = 0, hi = nw - 1;
+    while (lo < hi) {
+        int mid = (lo + hi + 1) >> 1;
+        if ((int64_t)g[mid].cell_base <= c) lo = mid; else hi = mid - 1;
+    }
+    return lo;
+}
+
+__global__ void bin_finalize_kernel(BinWork W)
+{
+    const int64_t c = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (c >= W.total_cells) return;
+    const uint32_t* a = W.aabb_bits + 8 * c;
+    const float4 lo = make_float4(ord_float(a[0]), ord_float(a[1]), ord_float(a[2]), 0.0f);
+    const float4 hi = make_float4(ord_float(a[3]), ord_float(a[4]), ord_float(a[5]), 0.0f);
+    W.cell_lo[c] = lo;
+    W.cell_hi[c] = hi;
+    if (W.count[c + 1] == W.count[c]) return;   // empty cell
+    const int w = world_of_cell(W.grids, W.num_worlds, c);
+    const WorldGrid g = W.grids[w];
+    const int64_t local = c - g.cell_base;
+    const int ix = (int)(local % g.nx), iy = (int)(local / g.nx);
+    const float x0 = g.ox + (float)ix * W.cell_size, x1 = g.ox + (float)(ix + 1) * W.cell_size;
+    const float y0 = g.oy + (float)iy * W.cell_size, y1 = g.oy + (float)(iy + 1) * W.cell_size;
+    float ext = fmaxf(fmaxf(x0 - lo.x, hi.x - x1), fmaxf(y0 - lo.y, hi.y - y1));
+    ext = fmaxf(ext, 0.0f);
+    atomicMax(&W.margin_bits[w], __float_as_uint(ext));
+}
+
+__global__ void bin_margin_kernel(BinWork W)
+{
+    const int w = blockIdx.x * blockDim.x + threadIdx.x;
+    if (w >= W.num_worlds) return;
+    const float m = __uint_as_float(W.margin_bits[w]);
+    W.grids[w].margin = m * 1.0009765625f + 0.0009765625f;   // (1 + 2^-10) m + 2^-10
+}
+
+hipError_t launch_bin(const BinWork& W, hipStream_t s)
+{
+    const int64_t cells = W.total_cells;
+    const int64_t n = cells + 1;
+    auto blocks = [](int64_t m) { return (unsigned)((m + kBlock - 1) / kBlock); };
+    const int64_t init_n = (n > W.num_worlds ? n : W.num_worlds);
+    hipLaunchKernelGGL(bin_init_kernel, dim3(blocks(init_n)), dim3(kBlock), 0, s,
+                       W.count, W.aabb_bits, cells, W.margin_bits, W.num_worlds);
+    if (W.T > 0)
+        hipLaunchKernelGGL(bin_count_kernel, dim3(blocks(W.T)), dim3(kBlock), 0, s, W);
+    const int64_t tiles = (n + kScanTile - 1) / kScanTile;
+    hipLaunchKernelGGL(scan_tiles_kernel, dim3((unsigned)tiles), dim3(kBlock), 0, s, W.count, n, W.scan_tmp);
+    hipLaunchKernelGGL(scan_sums_kernel, dim3(1), dim3(kBlock), 0, s, W.scan_tmp, tiles);
+    hipLaunchKernelGGL(scan_add_kernel, dim3(blocks(n)), dim3(kBlock), 0, s, W.count, n, W.scan_tmp);
+    if (W.T > 0)
+        hipLaunchKernelGGL(bin_scatter_kernel, dim3(blocks(W.T)), dim3(kBlock), 0, s, W);
+    if (cells > 0)
+        hipLaunchKernelGGL(bin_finalize_kernel, dim3(blocks(cells)), dim3(kBlock), 0, s, W);
+    hipLaunchKernelGGL(bin_margin_kernel, dim3(blocks(W.num_worlds)), dim3(kBlock), 0, s, W);
+    return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// kinematic bicycle step
+// ---------------------------------------------------------------------------
+
+__global__ void agents_step_kernel(const AgentStepParams p)
+{
+    const int i = blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= p.count) return;
+    const float kPi = 3.14159265358979323846f;
+    float v = p.speed[i] + p.accel[i] * p.dt;
+    v = fminf(fmaxf(v, 0.0f), p.vmax);
+    float psi = p.psi[i] + v / (0.6f * p.length[i]) * tanf(p.steer[i]) * p.dt;
+    if (psi > kPi) psi -= 2.0f * kPi;
+    if (psi <= -kPi) psi += 2.0f * kPi;
+    float sn, cs;
+    sincosf(psi, &sn, &cs);
+    p.x[i] += v * cs * p.dt;
+    p.y[i] += v * sn * p.dt;
+    p.psi[i] = psi;
+    p.speed[i] = v;
+    p.cos_h[i] = cs;
+    p.sin_h[i] = sn;
+}
+
+hipError_t launch_agents_step(const AgentStepParams& p, hipStream_t s)
+{
+    if (p.count <= 0) return hipSuccess;
+    hipLaunchKernelGGL(agents_step_kernel, dim3((unsigned)((p.count + 255) / 256)), dim3(256), 0, s, p);
+    return hipGetLastError();
+}
+
+}  // namespace pictura

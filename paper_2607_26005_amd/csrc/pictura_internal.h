@@ -9,10 +9,12 @@ namespace pictura {
 
 constexpr int kBlock = 256;          // threads per render workgroup (4 wave64)
 constexpr int kTileMaxPx = 4096;     // LDS framebuffer capacity (u32 keys)
-constexpr int kCellCap = 512;        // visible cells gathered per batch
-constexpr int kBigCap = 64;          // LDS queue of large triangles
-constexpr int kSmallPx = 16;         // bbox pixel count rasterized by a single lane
+constexpr int kCandCap = 2048;       // candidate triangles mapped to cells per pass
+constexpr int kQCap = 128;           // per-wave LDS queue of first-pass survivors
+constexpr int kSmallPx = 8;          // bbox pixel count rasterized by a single lane
+constexpr int kBigCap = 192;         // block-wide LDS queue of larger triangles
 constexpr int kAgentBatch = 256;     // agents box-culled per batch
+constexpr int kNumStats = 24;        // optional work counters of the render kernel
 
 // Grid of one world.  Cells are numbered row-major from cell_base.
 struct WorldGrid {
@@ -52,6 +54,7 @@ struct RenderParams {
     float mount[8][5];
     // derived constants
     float fx256, fy256, cx256, cy256, rfx, rfy, izfar, izcap;
+    float cabs;         // max(|cx|, |cy|)
     uint32_t qbase;
     // tiling
     int32_t tile_w, tile_h, tiles_x, tiles_y;
@@ -62,6 +65,8 @@ struct RenderParams {
     float* out_depth;
     int32_t cull;       // 1: cell + triangle + box frustum culling
     int32_t vec_out;    // 1: output pointers are 16-byte aligned
+    int32_t fast_decode; // 1: every decoded 1/z lies where the fast reciprocal is exact
+    unsigned long long* stats;  // optional [kNumStats] work counters (null: off)
 };
 
 struct AgentStepParams {
@@ -98,5 +103,6 @@ hipError_t launch_render(const RenderParams& p, hipStream_t s);
 hipError_t launch_bin(const BinWork& w, hipStream_t s);
 hipError_t launch_agents_step(const AgentStepParams& p, hipStream_t s);
 int64_t scan_tmp_needed(int64_t n);
+hipError_t launch_rcp_check(uint32_t lo_bits, uint32_t n, unsigned long long* mismatches, hipStream_t s);
 
 }  // namespace pictura

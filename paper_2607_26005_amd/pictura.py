@@ -19,7 +19,7 @@ HERE = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(HERE, "libpictura.so")
 
 OK, EINVAL, ENOMEM, EDEVICE, ESTATE, ERANGE = 0, -1, -2, -3, -4, -5
-OPT_CULL, OPT_TILE = 1, 2
+OPT_CULL, OPT_TILE, OPT_STATS = 1, 2, 3
 MAX_CAMS = 8
 
 if not os.path.exists(LIB_PATH):
@@ -77,10 +77,20 @@ _lib.pictura_bins_copy.argtypes = [_P, _P, _P, _P]
 _lib.pictura_bins_copy.restype = ctypes.c_int32
 _lib.pictura_set_option.argtypes = [_P, ctypes.c_int32, ctypes.c_int32]
 _lib.pictura_set_option.restype = ctypes.c_int32
+_lib.pictura_stats_copy.argtypes = [_P, _P, ctypes.c_int32, ctypes.c_int32]
+_lib.pictura_stats_copy.restype = ctypes.c_int32
+_lib.pictura_selftest_rcp.argtypes = [_P, ctypes.c_uint32, ctypes.c_uint32, _P]
+_lib.pictura_selftest_rcp.restype = ctypes.c_int32
 
 EXPORTED = ["pictura_create", "pictura_destroy", "pictura_last_error", "pictura_scene_upload",
             "pictura_bin_scene", "pictura_render_views", "pictura_agents_step", "pictura_bins_info",
-            "pictura_bins_copy", "pictura_set_option"]
+            "pictura_bins_copy", "pictura_set_option", "pictura_stats_copy", "pictura_selftest_rcp"]
+
+STAT_NAMES = ["view_tiles", "cells_in_rect", "cells_visible", "cand_tris", "boxes_visible", "box_tris",
+              "first_pass_survivors", "exact_batches", "clipped", "raster_tris", "area_ok", "wave_tris",
+              "lane_px", "wave_covered_px", "big_queue_overflow", "cand_passes",
+              "cyc_prologue", "cyc_phase_setup", "cyc_first_pass", "cyc_exact", "cyc_phase_barrier",
+              "cyc_wave_raster", "wave_lane_slots", "cyc_writeout"]
 
 
 def _ptr(a) -> Optional[int]:
@@ -189,6 +199,18 @@ def pictura_bins_copy(ctx, total_cells: int, num_tris: int):
 
 def pictura_set_option(ctx, option: int, value: int):
     _check(ctx, _lib.pictura_set_option(ctx, int(option), int(value)))
+
+
+def pictura_selftest_rcp(ctx, lo_bits: int, count: int) -> int:
+    out = ctypes.c_uint64()
+    _check(ctx, _lib.pictura_selftest_rcp(ctx, int(lo_bits), int(count), ctypes.addressof(out)))
+    return int(out.value)
+
+
+def pictura_stats_copy(ctx, reset: bool = True):
+    out = np.zeros(len(STAT_NAMES), np.uint64)
+    _check(ctx, _lib.pictura_stats_copy(ctx, out.ctypes.data, len(out), int(bool(reset))))
+    return dict(zip(STAT_NAMES, (int(x) for x in out)))
 
 
 # --- device-resident agents ------------------------------------------------------

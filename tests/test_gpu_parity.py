@@ -282,3 +282,18 @@ def test_abi_errors(lib):
         assert_parity(oc.view(8, 64, 64).cpu().numpy(), od.view(8, 64, 64).cpu().numpy(), ora, "after-errors")
     finally:
         lib.pictura_destroy(ctx)
+
+
+def test_fast_reciprocal_is_correctly_rounded(lib):
+    # The kernels replace IEEE division by rcp + one fused Newton step where
+    # the argument lies in [2^-12, 2^20); check every fp32 value there.
+    ctx = lib.pictura_create(0)
+    try:
+        lo = int(np.float32(2.0 ** -12).view(np.uint32))
+        hi = int(np.float32(2.0 ** 20).view(np.uint32))
+        bad = 0
+        for start in range(lo, hi, 1 << 26):
+            bad += lib.pictura_selftest_rcp(ctx, start, min(1 << 26, hi - start))
+        assert bad == 0
+    finally:
+        lib.pictura_destroy(ctx)
