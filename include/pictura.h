@@ -167,15 +167,17 @@ pictura_status pictura_set_option(pictura_ctx ctx, int32_t option, int32_t value
 
 /* Copy the render kernel's accumulated work counters (PICTURA_OPT_STATS) to
  * host memory (synchronous): out[k], k < n, in this order: view tiles, cells
- * in the gathered rectangles, cells passing the frustum test, triangles of
- * those cells, boxes passing, box triangles, first-pass survivors, exact
- * batches, triangles clipped at near, snapped triangles with pixels in the
- * tile, of those with non-zero area and a depth plane, triangles queued for
- * a whole wave, pixels tested by single lanes, (unused), wave-queue overflows,
- * candidate passes, then shader-clock cycles summed over waves spent in:
- * prologue, block-wide phase setup, first pass, exact pass, end-of-phase
- * barriers, whole-wave raster (part of the exact pass), final barrier and
- * write-out.  reset != 0 zeroes the counters. */
+ * in the gathered rectangles, cells passing the rectangle prefilter, cells
+ * passing the frustum test, triangles of those cells, boxes passing, box
+ * triangles, first-pass survivors, exact batches, triangles clipped at near,
+ * snapped triangles with pixels in the tile, of those rasterized by one lane,
+ * pixels those lanes tested, triangles rasterized as records, of those on
+ * the fp64 edge path, 8x8 blocks tested, blocks passing, first-pass
+ * chunks of 64 candidates, then shader-clock cycles summed over waves spent
+ * in:
+ * prologue, cell and agent tests, first pass, exact pass (with records),
+ * record raster (part of the exact pass), final barrier and write-out.
+ * reset != 0 zeroes the counters. */
 pictura_status pictura_stats_copy(pictura_ctx ctx, uint64_t* out, int32_t n, int32_t reset);
 
 /* Device self-check of the reciprocal the kernels use in place of IEEE

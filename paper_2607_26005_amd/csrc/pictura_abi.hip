@@ -308,6 +308,12 @@ pictura_status pictura_render_views(pictura_ctx c, const pictura_agents* ag, con
     P.rfx = 1.0f / P.fx; P.rfy = 1.0f / P.fy;
     P.izfar = izfar; P.izcap = izcap; P.qbase = f2u(izcap) >> 3;
     P.cabs = std::fabs(P.cx) > std::fabs(P.cy) ? std::fabs(P.cx) : std::fabs(P.cy);
+    // pixel-centre offsets: with c a multiple of 2^-8 below 2^14 in magnitude,
+    // 0.5 - c and i + (0.5 - c) (i < 4096) are exact in fp32
+    P.hx = 0.5f - P.cx;
+    P.hy = 0.5f - P.cy;
+    auto eighth_bit = [](float c) { const double s = (double)c * 256.0; return std::fabs(c) < 16384.0f && s == std::rint(s); };
+    P.pix_exact = (eighth_bit(P.cx) && eighth_bit(P.cy)) ? 1 : 0;
     // decoded inverse depths lie in [1/far (1 - 2^-20), IZCAP]
     P.fast_decode = (izfar >= 0.000244140625f * 1.0000038f && izcap < 1048576.0f) ? 1 : 0;
     int tw = 64, th = 64;

@@ -7,13 +7,7 @@
 
 namespace pictura {
 
-constexpr int kBlock = 256;          // threads per render workgroup (4 wave64)
-constexpr int kTileMaxPx = 4096;     // LDS framebuffer capacity (u32 keys)
-constexpr int kCandCap = 2048;       // candidate triangles mapped to cells per pass
-constexpr int kQCap = 128;           // per-wave LDS queue of first-pass survivors
-constexpr int kSmallPx = 8;          // bbox pixel count rasterized by a single lane
-constexpr int kBigCap = 192;         // block-wide LDS queue of larger triangles
-constexpr int kAgentBatch = 256;     // agents box-culled per batch
+constexpr int kBlock = 256;          // threads per workgroup of the binning kernels
 constexpr int kNumStats = 24;        // optional work counters of the render kernel
 
 // Grid of one world.  Cells are numbered row-major from cell_base.
@@ -55,6 +49,8 @@ struct RenderParams {
     // derived constants
     float fx256, fy256, cx256, cy256, rfx, rfy, izfar, izcap;
     float cabs;         // max(|cx|, |cy|)
+    float hx, hy;       // 0.5 - cx, 0.5 - cy
+    int32_t pix_exact;  // 1: (i + 0.5) - cx equals i + hx exactly for every pixel index (same for y)
     uint32_t qbase;
     // tiling
     int32_t tile_w, tile_h, tiles_x, tiles_y;

@@ -1,39 +1,52 @@
-// Batched class/depth view rasterizer for gfx950: one 256-thread workgroup
-// per view tile (at most 64x64 pixels) whose framebuffer of 32-bit keys lives
-// in LDS.
+// Batched class/depth view rasterizer for gfx950.  One workgroup renders one
+// view tile (at most 64x64 pixels) into a framebuffer of 32-bit keys in LDS;
+// the workgroup has kViewWaves waves that share the framebuffer and split the
+// tile's cells and agents between them, each running the whole pipeline on
+// its share with no barrier until the write-out:
 //
-// Per tile:
-//  1. cells of the world grid around the tile frustum are tested (one lane
-//     per cell) against the frustum planes and, when the whole cell is in
-//     front of the near plane, against the tile's pixel centres through a
-//     conservative projection of the cell's bounding box; visible cells are
-//     compacted with a ballot and their triangle counts prefix-summed;
-//  2. candidate triangles are mapped to their cell by a max-scan of cell
-//     start markers; each wave runs a cheap first pass over 64 at a time
-//     (view transform, the near/far rule, a conservative approximate test
-//     that the snapped triangle can hold a pixel centre of the tile) and
-//     compacts the survivors (ballot + mbcnt) into its own LDS queue;
-//  3. each full queue of 64 survivors goes through the exact pass: near
-//     clipping, 8-bit subpixel snap, setup, depth plane.  Triangles with a
-//     small bounding box are rasterized by their own lane; larger ones are
-//     pushed to a block-wide queue that all waves drain, one triangle per
-//     wave, the wave tiling the bounding box as (power-of-two columns) x
-//     (64 / columns) rows with incremental edge functions;
-//  4. leftover survivors of all waves are pooled into full batches at the
-//     end;
-//  5. visibility is an LDS atomicMin of (24-bit depth | 8-bit class), so the
+//  1. cells of the world grid in the rectangle around the tile frustum are
+//     taken 64 at a time (one lane per cell): a cheap test of the cell
+//     rectangle (widened by the world's margin) against the side, near and
+//     far planes, then the cell's triangle range and bounding box are loaded
+//     and tested against all six planes and, when the box lies in front of the
+//     near plane, against the tile's pixel centres through a conservative
+//     projection.  Visible cells are compacted with a ballot and their
+//     triangle counts prefix-summed across the wave;
+//  2. candidate triangles (then the twelve triangles of every visible agent
+//     box) go through a first pass 64 at a time: view transform, the near/far
+//     rule and a conservative test that the snapped triangle can hold a pixel
+//     centre of the tile; survivors are appended to the wave's LDS queue;
+//  3. every 64 survivors go through the exact pass, one lane per triangle:
+//     near clipping, 8-bit subpixel snap, orientation, depth plane.  A
+//     triangle whose bounding box has at most kSmallPx pixels is rasterized
+//     by its own lane.  For the others the lane computes a raster record
+//     (exact edge functions at the tile origin, box, depth plane) that the
+//     wave then reads lane by lane into scalar registers: every lane tests
+//     one 8x8 pixel block of the record's bounding box against its three
+//     edges, and the passing blocks are rasterized one per step, lane l
+//     handling pixel (l & 7, l >> 3) of the block;
+//  4. visibility is an LDS atomicMin of (24-bit depth | 8-bit class), so the
 //     order in which lanes and waves finish does not matter;
-//  6. the tile is resolved and written with 16-byte non-temporal stores.
+//  5. the tile is resolved and written with 16-byte non-temporal stores.
 //
 // The exact pass evaluates the rasterization rules (camera R1, view
 // transform R2, depth plane R3, near clip R4, snap R5, fill R6, key R7,
 // resolve R8, boxes R9) in fp32 with no contraction and correctly rounded
-// reciprocals and divisions, so every key equals a brute-force evaluation of
-// the rules over all triangles of the world.  Everything before it only
-// skips triangles that cannot set a key.
+// reciprocals and divisions.  Edge functions are exact: int32 (24-bit
+// multiplies) when every value over the tile fits, otherwise fp64 fused
+// multiply-adds whose sign is exact for every pixel of the tile.  So every
+// key equals a brute-force evaluation of the rules over all triangles of the
+// world; everything before the exact pass only skips triangles that cannot
+// set a key.
+#include <type_traits>
+
 #include "pictura_device.h"
 
 #pragma clang fp contract(off)
+
+#ifndef PICTURA_VIEW_WAVES
+#define PICTURA_VIEW_WAVES 1
+#endif
 
 namespace pictura {
 
@@ -41,8 +54,16 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr uint32_t kClearKey = (0xFFFFFFu << 8) | 4u;
-constexpr int kWaves = kBlock / 64;
 constexpr uint32_t kBoxFlag = 0x80000000u;
+constexpr int kViewWaves = PICTURA_VIEW_WAVES;   // waves per view tile
+constexpr int kThreads = 64 * kViewWaves;
+constexpr int kMinBlocks = kViewWaves >= 2 ? 1 : 2; // at least two waves per SIMD fit the register budget
+constexpr int kSmallPx = 8;       // bounding boxes of at most this many pixels are rasterized by one lane
+constexpr int kQueue = 128;       // per-wave queue of first-pass survivors
+// Framebuffer rows are padded to a pitch of 4 mod 32 words, so the 64 lanes
+// of an 8x8 block hit every LDS bank exactly twice.
+constexpr int kFbCap = 64 * 68;
+static_assert(kViewWaves == 1 || kViewWaves == 2 || kViewWaves == 4, "1, 2 or 4 waves per view tile");
 
 struct Cam {
     float x, y, z;     // camera centre (R1)
@@ -55,35 +76,51 @@ struct Cam {
 //   top   kt*zv - fy*yv     bottom fy*yv - kb*zv
 struct Tile {
     int x0, y0, w, h;
+    int pitch;         // framebuffer words per row
     float kl, kr, kt, kb;
 };
 
-// A snapped triangle queued for whole-wave rasterization.
-struct BigTri {
-    int X0, Y0, X1, Y1, X2, Y2;   // oriented (area2 > 0)
-    float pa, pb, pc;             // depth plane (R3)
-    uint32_t box;                 // class | i0 << 8 | i1 << 16 | j0 << 24 (tile-local bounding box)
-    uint32_t j1;                  // tile-local last row
+// Raster record of a snapped, oriented triangle with more than kSmallPx
+// pixels in its tile bounding box.  Edge k (v1->v2, v2->v0, v0->v1) at tile
+// pixel (i, j) is
+//   E_k = c_k + a_k i + b_k j,   a_k = -256 dy_k,  b_k = 256 dx_k,
+// with c_k its value at the tile's pixel (0, 0) plus the top-left bias;
+// covered iff every E_k >= 0.  The exact pass leaves a record in the lane of
+// its triangle as twelve words: the int32 path (every value over the tile
+// fits) holds a0 a1 a2 b0 b1 b2 c0 c1 c2; the fp64 path holds c_k as doubles
+// (words 0..5) and dx_k, dy_k (words 6..11).  c_k is an integer below 2^61:
+// as a double it is exact below 2^53, and beyond that its rounding keeps the
+// sign, which no pixel of the tile can change.
+
+// Per-wave LDS: the visible-cell (or agent) list of a refill and the queue
+// of first-pass survivors.
+struct alignas(16) WaveLds {
+    union {
+        struct {
+            uint32_t start[64];
+            uint32_t count[64];
+        } cells;
+        uint32_t agents[64];
+    } u;
+    uint32_t q[kQueue];
 };
 
 struct alignas(16) Shared {
-    uint32_t fb[kTileMaxPx];
-    uint32_t cl_start[kBlock];
-    uint32_t cl_pre[kBlock + 1];
-    union {
-        uint16_t mark[kCandCap];       // static phase: cell slot + 1 of each candidate
-        uint32_t vis[kAgentBatch];     // box phase: visible agents
-    } u;
-    uint32_t q[kWaves][kQCap];         // per-wave survivor queues
-    BigTri big[kBigCap];               // block-wide queue of large triangles
-    uint32_t s_wave[kWaves];
-    uint32_t nq_w[kWaves];
-    uint32_t n_cells, n_vis, n_big, big_next;
+    uint32_t fb[kFbCap];
+    WaveLds wv[kViewWaves];
     uint32_t stat[kNumStats];
 };
 
+enum Stat {
+    kStTiles = 0, kStCellsRect, kStCellsPre, kStCellsVis, kStCand, kStBoxesVis, kStBoxTris, kStSurv,
+    kStExact, kStClipped, kStRasterTris, kStLaneTris, kStLanePx, kStRecTris, kStRecWide, kStBlocksTested,
+    kStBlocksPassed, kStChunks, kCycPrologue, kCycSource, kCycFirst, kCycExact, kCycRecords, kCycWriteout
+};
+static_assert(kCycWriteout + 1 == kNumStats, "stat count");
+
 // Optional work counters (P.stats non-null): LDS per block, flushed once.
 #define STAT(k, n) do { if (P.stats) atomicAdd(&S.stat[(k)], (uint32_t)(n)); } while (0)
+#define STAT1(k, n) do { if (P.stats && lane_id() == 0) atomicAdd(&S.stat[(k)], (uint32_t)(n)); } while (0)
 // Phase timers of the stats mode: shader-clock cycles seen by lane 0 of every wave.
 #define TSTART(t) long long t = P.stats ? (long long)__builtin_amdgcn_s_memtime() : 0ll
 #define TACC(k, t) do { if (P.stats && lane_id() == 0) atomicAdd(&S.stat[(k)], (uint32_t)((long long)__builtin_amdgcn_s_memtime() - (t))); } while (0)
@@ -103,6 +140,39 @@ __device__ __forceinline__ float rcp_rn(float x)
 }
 
 __device__ __forceinline__ bool rcp_rn_ok(float x) { return x >= 0.000244140625f && x < 1048576.0f; }
+
+__device__ __forceinline__ uint32_t mbcnt(uint64_t m)
+{
+    return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+
+__device__ __forceinline__ uint32_t readlane(uint32_t v, int l)
+{
+    return (uint32_t)__builtin_amdgcn_readlane((int)v, l);
+}
+
+__device__ __forceinline__ float readlane_f(float v, int l) { return __uint_as_float(readlane(__float_as_uint(v), l)); }
+
+__device__ __forceinline__ double readlane_d(double v, int l)
+{
+    const unsigned long long b = (unsigned long long)__double_as_longlong(v);
+    const unsigned long long lo = readlane((uint32_t)b, l), hi = readlane((uint32_t)(b >> 32), l);
+    return __longlong_as_double((long long)((hi << 32) | lo));
+}
+
+// Exclusive prefix sum over the wave; `total` receives the sum of all lanes.
+__device__ __forceinline__ uint32_t wave_excl_scan(uint32_t v, uint32_t& total)
+{
+    const int lane = lane_id();
+    uint32_t x = v;
+#pragma unroll
+    for (int o = 1; o < 64; o <<= 1) {
+        const uint32_t y = __shfl_up(x, o);
+        if (lane >= o) x += y;
+    }
+    total = readlane(x, 63);
+    return x - v;
+}
 
 // ---------------------------------------------------------------------------
 // geometry rules
@@ -311,7 +381,7 @@ __device__ __forceinline__ void raster_lane(const RenderParams& P, Shared& S, co
     for (int j = j0; j <= j1; ++j) {
         I g0 = f0, g1 = f1, g2 = f2;
         const float pyf = ((float)j + 0.5f) - P.cy;
-        uint32_t* row = &S.fb[(j - T.y0) * T.w - T.x0];
+        uint32_t* row = &S.fb[(j - T.y0) * T.pitch - T.x0];
         for (int i = i0; i <= i1; ++i) {
             if ((g0 | g1 | g2) >= 0) {
                 const float pxf = ((float)i + 0.5f) - P.cx;
@@ -323,60 +393,109 @@ __device__ __forceinline__ void raster_lane(const RenderParams& P, Shared& S, co
     }
 }
 
-// One queued triangle rasterized by a whole wave: lanes tile its bounding
-// box as cw columns (the next power of two >= its width) by 64 / cw rows and
-// step down the rows with incremental edge functions.
-template <typename I>
-__device__ __forceinline__ void raster_wave(const RenderParams& P, Shared& S, const Tile& T, const BigTri& b)
+// Rasterize one record with the whole wave.  Lane b tests 8x8 block b of
+// the bounding box (a tile has at most 8 x 8 blocks): the edge value at the
+// block corner that maximises it must be >= 0 for all three edges.  The
+// passing blocks are then rasterized one per step, lane l handling pixel
+// (l & 7, l >> 3): its edge values at that pixel of block (0, 0) plus the
+// block's offsets, which the lane that tested the block computed.
+//
+// int32 path (I32): |dx|, |dy| < 2^15 and |c| < 2^30, so a_k, b_k fit a
+// 24-bit multiply and |E| < 2^30 + 2 * 63 * 2^23 < 2^31 anywhere in the tile.
+// fp64 path: |a_k|, |b_k| <= 2^38, so with tile coordinates below 64 every
+// product and partial sum is an exact integer when |c| < 2^52; otherwise |c|
+// exceeds the sum of all other terms by 2^9 and fixes the sign of every sum.
+// Fast: the tile is a whole number of blocks and pixel-centre offsets are
+// exact sums (P.pix_exact), so no lane leaves the tile and the offset of a
+// pixel centre is the lane's own plus the block's.  Rejected lanes take part
+// in the atomic with the neutral key, at an address inside the framebuffer.
+template <bool I32, bool Fast>
+__device__ __forceinline__ void raster_blocks(const RenderParams& P, Shared& S, const Tile& T, const uint32_t* u,
+                                              float pa, float pb, float pc, uint32_t box, uint32_t j1w,
+                                              float pxl, float pyl, int loff4)
 {
-    const int lane = lane_id();
-    const int i0 = T.x0 + (int)((b.box >> 8) & 255u), i1 = T.x0 + (int)((b.box >> 16) & 255u);
-    const int j0 = T.y0 + (int)(b.box >> 24), j1 = T.y0 + (int)b.j1;
-    const uint32_t cls = b.box & 255u;
-    const int bw = i1 - i0 + 1, bh = j1 - j0 + 1;
-    const int lcw = bw > 1 ? 32 - __clz(bw - 1) : 0;   // log2 of the column count
-    const int lx = lane & ((1 << lcw) - 1), ly = lane >> lcw;
-    const int rows = 64 >> lcw;
-    const int i = i0 + lx;
-    const bool colok = lx < bw;
-    I f0 = edge_f<I>(b.X1, b.Y1, b.X2, b.Y2, i, j0 + ly);
-    I f1 = edge_f<I>(b.X2, b.Y2, b.X0, b.Y0, i, j0 + ly);
-    I f2 = edge_f<I>(b.X0, b.Y0, b.X1, b.Y1, i, j0 + ly);
-    const I st0 = (I)(b.X2 - b.X1) * (I)(256 * rows);
-    const I st1 = (I)(b.X0 - b.X2) * (I)(256 * rows);
-    const I st2 = (I)(b.X1 - b.X0) * (I)(256 * rows);
-    const float pxf = ((float)i + 0.5f) - P.cx;
-    uint32_t* col = &S.fb[i - T.x0];
-    for (int jr = ly; jr < bh; jr += rows) {
-        const int j = j0 + jr;
-        if (P.stats && lane == 0) atomicAdd(&S.stat[22], 64u);
-        if (colok && (f0 | f1 | f2) >= 0) {
-            const float pyf = ((float)j + 0.5f) - P.cy;
-            if (P.stats) atomicAdd(&S.stat[13], 1u);
-            atomicMin(&col[(j - T.y0) * T.w], pixel_key(P, pxf, pyf, b.pa, b.pb, b.pc, cls));
+    typedef typename std::conditional<I32, int, double>::type E;
+    const int lane = lane_id(), lx = lane & 7, ly = lane >> 3;
+    const uint32_t cls = box & 255u;
+    const int i0 = (int)((box >> 8) & 255u), i1 = (int)((box >> 16) & 255u);
+    const int j0 = (int)(box >> 24), j1 = (int)(j1w & 255u);
+    const int bx0 = i0 >> 3, by0 = j0 >> 3;
+    const int nbx = (i1 >> 3) - bx0 + 1, nb = nbx * ((j1 >> 3) - by0 + 1);
+    // b / nbx == (b * rinv) >> 16 for b < 64 and nbx <= 8
+    const uint32_t rinv = nbx == 1 ? 65536u : nbx == 2 ? 32768u : nbx == 3 ? 21846u : nbx == 4 ? 16384u
+                        : nbx == 5 ? 13108u : nbx == 6 ? 10923u : nbx == 7 ? 9363u : 8192u;
+    E A[3], B[3], Cc[3], Eb[3], off[3];
+#pragma unroll
+    for (int k = 0; k < 3; ++k) {
+        if constexpr (I32) {
+            A[k] = (int)u[k];
+            B[k] = (int)u[3 + k];
+            Cc[k] = (int)u[6 + k];
+            Eb[k] = __mul24(A[k], lx) + (__mul24(B[k], ly) + Cc[k]);
+        } else {
+            A[k] = -(double)(int)u[9 + k] * 256.0;
+            B[k] = (double)(int)u[6 + k] * 256.0;
+            Cc[k] = __longlong_as_double((long long)(((unsigned long long)u[2 * k + 1] << 32) | u[2 * k]));
+            Eb[k] = fma(A[k], (double)lx, fma(B[k], (double)ly, Cc[k]));
         }
-        f0 += st0; f1 += st1; f2 += st2;
     }
-}
-
-// Drain the block-wide queue of large triangles: each wave takes the next
-// one until none is left.  Called by the whole block.
-__device__ __forceinline__ void drain_big(const RenderParams& P, Shared& S, const Tile& T)
-{
-    TSTART(tw);
-    const uint32_t n = min(S.n_big, (uint32_t)kBigCap);
-    for (;;) {
-        uint32_t e = 0;
-        if (lane_id() == 0) e = atomicAdd(&S.big_next, 1u);
-        e = __builtin_amdgcn_readfirstlane(e);
-        if (e >= n) break;
-        const BigTri b = S.big[e];
-        const int minX = min(b.X0, min(b.X1, b.X2)), maxX = max(b.X0, max(b.X1, b.X2));
-        const int minY = min(b.Y0, min(b.Y1, b.Y2)), maxY = max(b.Y0, max(b.Y1, b.Y2));
-        if ((maxX - minX) < 16384 && (maxY - minY) < 16384) raster_wave<int>(P, S, T, b);
-        else raster_wave<long long>(P, S, T, b);
+    // lane b: block b of the box
+    const int eby = (int)(((uint32_t)lane * rinv) >> 16), ebx = lane - eby * nbx;
+    const int X = (bx0 + ebx) * 8, Y = (by0 + eby) * 8;
+    bool pass = lane < nb;
+#pragma unroll
+    for (int k = 0; k < 3; ++k) {
+        if constexpr (I32) {
+            off[k] = __mul24(A[k], X) + __mul24(B[k], Y);
+            const int d = 7 * (max(A[k], 0) + max(B[k], 0));
+            pass = pass & ((Cc[k] + d) + off[k] >= 0);
+        } else {
+            off[k] = fma(A[k], (double)X, B[k] * (double)Y);
+            const double d = 7.0 * (fmax(A[k], 0.0) + fmax(B[k], 0.0));
+            pass = pass & ((Cc[k] + d) + off[k] >= 0.0);
+        }
     }
-    TACC(21, tw);
+    const int base4 = (Y * T.pitch + X) * 4;
+    const float pxu = (float)(T.x0 + X), pyu = (float)(T.y0 + Y);
+    const uint32_t xy = (uint32_t)X | ((uint32_t)Y << 8);
+    uint64_t m = __ballot(pass);
+    if (P.stats && lane == 0) {
+        atomicAdd(&S.stat[kStBlocksTested], (uint32_t)nb);
+        atomicAdd(&S.stat[kStBlocksPassed], (uint32_t)__popcll(m));
+    }
+    while (m) {
+        const int b = __builtin_ctzll(m);
+        m &= m - 1;
+        bool cov;
+        if constexpr (I32) {
+            const int e0 = Eb[0] + (int)readlane((uint32_t)off[0], b);
+            const int e1 = Eb[1] + (int)readlane((uint32_t)off[1], b);
+            const int e2 = Eb[2] + (int)readlane((uint32_t)off[2], b);
+            cov = (e0 | e1 | e2) >= 0;
+        } else {
+            const double e0 = Eb[0] + readlane_d(off[0], b);
+            const double e1 = Eb[1] + readlane_d(off[1], b);
+            const double e2 = Eb[2] + readlane_d(off[2], b);
+            cov = (e0 >= 0.0) & (e1 >= 0.0) & (e2 >= 0.0);
+        }
+        float pxf, pyf;
+        if constexpr (Fast) {
+            pxf = pxl + readlane_f(pxu, b);
+            pyf = pyl + readlane_f(pyu, b);
+        } else {
+            const uint32_t q = readlane(xy, b);
+            const int bX = (int)(q & 255u), bY = (int)(q >> 8);
+            cov = cov & (lx < T.w - bX) & (ly < T.h - bY);
+            pxf = ((float)(T.x0 + bX + lx) + 0.5f) - P.cx;
+            pyf = ((float)(T.y0 + bY + ly) + 0.5f) - P.cy;
+        }
+        const float iz = fmaf(pa, pxf, fmaf(pb, pyf, pc));
+        const uint32_t bits = min(__float_as_uint(iz), __float_as_uint(P.izcap));
+        const uint32_t key = ((P.qbase - (bits >> 3)) << 8) | cls;
+        const bool ok = cov && iz >= P.izfar;
+        const int addr = (int)readlane((uint32_t)base4, b) + loff4;
+        atomicMin((uint32_t*)((char*)S.fb + addr), ok ? key : 0xFFFFFFFFu);
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -384,9 +503,10 @@ __device__ __forceinline__ void drain_big(const RenderParams& P, Shared& S, cons
 // ---------------------------------------------------------------------------
 
 __device__ __forceinline__ void exact_pass(const RenderParams& P, Shared& S, const Tile& T, const Cam& cam,
-                                           bool live, uint32_t entry, int64_t abase_w)
+                                           bool live, uint32_t entry, int64_t abase_w, float pxl, float pyl,
+                                           int loff4)
 {
-    float tri[9];
+    float tri[9] = {};
     uint32_t cls = 0;
     int np = 0;
     int X0 = 0, Y0 = 0, X1 = 0, Y1 = 0, X2 = 0, Y2 = 0, X3 = 0, Y3 = 0;
@@ -404,7 +524,7 @@ __device__ __forceinline__ void exact_pass(const RenderParams& P, Shared& S, con
         } else {
             // R4: Sutherland-Hodgman output of the six straddling cases, in
             // the order in which v0v1, v1v2, v2v0 visit the edges.
-            STAT(8, 1);
+            STAT(kStClipped, 1);
             float x01 = 0, y01 = 0, x12 = 0, y12 = 0, x20 = 0, y20 = 0;
             if (in0 != in1) {
                 if (in0) near_cross(P, xv[0], yv[0], zv[0], xv[1], yv[1], zv[1], x01, y01);
@@ -439,100 +559,127 @@ __device__ __forceinline__ void exact_pass(const RenderParams& P, Shared& S, con
         }
         if (!ok) np = 0;
     }
+    const int nfan = __ballot(np == 4) != 0 ? 2 : 1;
     bool have_plane = false, plane_bad = false;
     float pa = 0.0f, pb = 0.0f, pc = 0.0f;
+    const int px0 = 256 * T.x0 + 128, py0 = 256 * T.y0 + 128;
     // fan triangles (p0, p1, p2) and (p0, p2, p3)
 #pragma unroll 1
-    for (int f = 0; f < 2; ++f) {
-        if (!(live && f + 2 < np && !plane_bad)) continue;
+    for (int f = 0; f < nfan; ++f) {
+        bool big = false;
         const int ax = X0, ay = Y0;
         int bx = f == 0 ? X1 : X2, by = f == 0 ? Y1 : Y2;
         int cx = f == 0 ? X2 : X3, cy = f == 0 ? Y2 : Y3;
-        const int minX = min(ax, min(bx, cx)), maxX = max(ax, max(bx, cx));
-        const int minY = min(ay, min(by, cy)), maxY = max(ay, max(by, cy));
-        const int i0 = max((minX - 128 + 255) >> 8, T.x0), i1 = min((maxX - 128) >> 8, T.x0 + T.w - 1);
-        const int j0 = max((minY - 128 + 255) >> 8, T.y0), j1 = min((maxY - 128) >> 8, T.y0 + T.h - 1);
-        if (i0 > i1 || j0 > j1) continue;
-        STAT(9, 1);
-        const bool small_span = (maxX - minX) < 16384 && (maxY - minY) < 16384;
-        long long area2;
-        if (small_span) area2 = (long long)(__mul24(bx - ax, cy - ay) - __mul24(by - ay, cx - ax));
-        else area2 = (long long)(bx - ax) * (long long)(cy - ay) - (long long)(by - ay) * (long long)(cx - ax);
-        if (area2 == 0) continue;
-        if (area2 < 0) {
-            const int tx = bx, ty = by;
-            bx = cx; by = cy; cx = tx; cy = ty;
-        }
-        if (!have_plane) {
-            have_plane = depth_plane(P, cam, tri, pa, pb, pc);
-            plane_bad = !have_plane;
-            if (plane_bad) continue;
-        }
-        STAT(10, 1);
-        const int npx = (i1 - i0 + 1) * (j1 - j0 + 1);
-        if (npx > kSmallPx) {
-            const uint32_t slot = atomicAdd(&S.n_big, 1u);
-            if (slot < (uint32_t)kBigCap) {
-                STAT(11, 1);
-                BigTri& q = S.big[slot];
-                q.X0 = ax; q.Y0 = ay; q.X1 = bx; q.Y1 = by; q.X2 = cx; q.Y2 = cy;
-                q.pa = pa; q.pb = pb; q.pc = pc;
-                q.box = cls | (uint32_t)(i0 - T.x0) << 8 | (uint32_t)(i1 - T.x0) << 16 | (uint32_t)(j0 - T.y0) << 24;
-                q.j1 = (uint32_t)(j1 - T.y0);
-                continue;
+        int i0 = 0, i1 = -1, j0 = 0, j1 = -1;
+        if (live && f + 2 < np && !plane_bad) {
+            const int minX = min(ax, min(bx, cx)), maxX = max(ax, max(bx, cx));
+            const int minY = min(ay, min(by, cy)), maxY = max(ay, max(by, cy));
+            i0 = max((minX - 128 + 255) >> 8, T.x0); i1 = min((maxX - 128) >> 8, T.x0 + T.w - 1);
+            j0 = max((minY - 128 + 255) >> 8, T.y0); j1 = min((maxY - 128) >> 8, T.y0 + T.h - 1);
+            if (i0 <= i1 && j0 <= j1) {
+                STAT(kStRasterTris, 1);
+                const bool small_span = (maxX - minX) < 16384 && (maxY - minY) < 16384;
+                long long area2;
+                if (small_span) area2 = (long long)(__mul24(bx - ax, cy - ay) - __mul24(by - ay, cx - ax));
+                else area2 = (long long)(bx - ax) * (long long)(cy - ay) - (long long)(by - ay) * (long long)(cx - ax);
+                if (area2 != 0) {
+                    if (area2 < 0) {
+                        const int tx = bx, ty = by;
+                        bx = cx; by = cy; cx = tx; cy = ty;
+                    }
+                    if (!have_plane) {
+                        have_plane = depth_plane(P, cam, tri, pa, pb, pc);
+                        plane_bad = !have_plane;
+                    }
+                    if (have_plane) {
+                        const int npx = (i1 - i0 + 1) * (j1 - j0 + 1);
+                        if (npx > kSmallPx) {
+                            big = true;
+                        } else {
+                            STAT(kStLaneTris, 1);
+                            STAT(kStLanePx, npx);
+                            if (small_span)
+                                raster_lane<int>(P, S, T, ax, ay, bx, by, cx, cy, i0, i1, j0, j1, pa, pb, pc, cls);
+                            else
+                                raster_lane<long long>(P, S, T, ax, ay, bx, by, cx, cy, i0, i1, j0, j1, pa, pb, pc,
+                                                       cls);
+                        }
+                    }
+                }
             }
-            STAT(14, 1);   // queue full: rasterized by this lane instead
         }
-        STAT(12, npx);
-        if (small_span) raster_lane<int>(P, S, T, ax, ay, bx, by, cx, cy, i0, i1, j0, j1, pa, pb, pc, cls);
-        else raster_lane<long long>(P, S, T, ax, ay, bx, by, cx, cy, i0, i1, j0, j1, pa, pb, pc, cls);
+        uint64_t m = __ballot(big);
+        if (m == 0) continue;
+        // record of this lane's triangle: edges v1->v2, v2->v0, v0->v1 at the tile's pixel (0, 0)
+        uint32_t rv[12] = {0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
+        uint32_t rbox = 0, rj1 = 0;
+        if (big) {
+            bool e32 = true;
+            const int ex[3] = {bx, cx, ax}, ey[3] = {by, cy, ay};
+            const int fx[3] = {cx, ax, bx}, fy[3] = {cy, ay, by};
+            long long cv[3];
+            int dxs[3], dys[3];
+#pragma unroll
+            for (int k = 0; k < 3; ++k) {
+                const int dx = fx[k] - ex[k], dy = fy[k] - ey[k];
+                const int tl = (dy < 0) || (dy == 0 && dx > 0);
+                cv[k] = (long long)dx * (long long)(py0 - ey[k]) - (long long)dy * (long long)(px0 - ex[k]) +
+                        (long long)(tl - 1);
+                e32 = e32 && dx > -32768 && dx < 32768 && dy > -32768 && dy < 32768 && cv[k] > -1073741824ll &&
+                      cv[k] < 1073741824ll;
+                dxs[k] = dx;
+                dys[k] = dy;
+            }
+#pragma unroll
+            for (int k = 0; k < 3; ++k) {
+                if (e32) {
+                    rv[k] = (uint32_t)(-(dys[k] * 256));
+                    rv[3 + k] = (uint32_t)(dxs[k] * 256);
+                    rv[6 + k] = (uint32_t)(int)cv[k];
+                } else {
+                    const unsigned long long cb = (unsigned long long)__double_as_longlong((double)cv[k]);
+                    rv[2 * k] = (uint32_t)cb;
+                    rv[2 * k + 1] = (uint32_t)(cb >> 32);
+                    rv[6 + k] = (uint32_t)dxs[k];
+                    rv[9 + k] = (uint32_t)dys[k];
+                }
+            }
+            rbox = cls | (uint32_t)(i0 - T.x0) << 8 | (uint32_t)(i1 - T.x0) << 16 | (uint32_t)(j0 - T.y0) << 24;
+            rj1 = (uint32_t)(j1 - T.y0) | (e32 ? 256u : 0u);
+            STAT(kStRecTris, 1);
+            if (!e32) STAT(kStRecWide, 1);
+        }
+        const bool fast = P.pix_exact && (T.w & 7) == 0 && (T.h & 7) == 0;
+        TSTART(t_rec);
+        while (m) {
+            const int l = __builtin_ctzll(m);
+            m &= m - 1;
+            const float rpa = readlane_f(pa, l), rpb = readlane_f(pb, l), rpc = readlane_f(pc, l);
+            const uint32_t rb = readlane(rbox, l), rj = readlane(rj1, l);
+            uint32_t uw[12];
+            if (rj & 256u) {
+#pragma unroll
+                for (int q = 0; q < 9; ++q) uw[q] = readlane(rv[q], l);
+                if (fast) raster_blocks<true, true>(P, S, T, uw, rpa, rpb, rpc, rb, rj, pxl, pyl, loff4);
+                else raster_blocks<true, false>(P, S, T, uw, rpa, rpb, rpc, rb, rj, pxl, pyl, loff4);
+            } else {
+#pragma unroll
+                for (int q = 0; q < 12; ++q) uw[q] = readlane(rv[q], l);
+                if (fast) raster_blocks<false, true>(P, S, T, uw, rpa, rpb, rpc, rb, rj, pxl, pyl, loff4);
+                else raster_blocks<false, false>(P, S, T, uw, rpa, rpb, rpc, rb, rj, pxl, pyl, loff4);
+            }
+        }
+        TACC(kCycRecords, t_rec);
     }
 }
 
 // Append the lanes with `pred` to this wave's queue (ballot + mbcnt, no
 // atomics); returns the new depth, which is uniform across the wave.
-__device__ __forceinline__ int queue_push(Shared& S, int wid, int nq, bool pred, uint32_t val)
+__device__ __forceinline__ int queue_push(WaveLds& L, int nq, bool pred, uint32_t val)
 {
     const uint64_t m = __ballot(pred);
-    const uint32_t rank = __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
-    if (pred) S.q[wid][nq + rank] = val;
+    if (pred) L.q[nq + mbcnt(m)] = val;
     return nq + (int)__popcll(m);
-}
-
-// In-place inclusive max-scan of the candidate markers mark[0, kCandCap):
-// thread t owns the kMarksPerThread consecutive markers starting at
-// t * kMarksPerThread, so the block covers exactly kCandCap of them.
-constexpr int kMarksPerThread = kCandCap / kBlock;
-static_assert(kMarksPerThread * kBlock == kCandCap, "every marker must belong to one thread");
-static_assert(kMarksPerThread % 2 == 0, "markers are cleared two at a time");
-
-__device__ __forceinline__ void max_scan_marks(Shared& S)
-{
-    const int tid = threadIdx.x, lane = lane_id(), wid = tid >> 6;
-    uint16_t* m = S.u.mark + kMarksPerThread * tid;
-    uint32_t v[kMarksPerThread];
-#pragma unroll
-    for (int q = 0; q < kMarksPerThread; ++q) v[q] = m[q];
-#pragma unroll
-    for (int q = 1; q < kMarksPerThread; ++q) v[q] = max(v[q], v[q - 1]);
-    uint32_t x = v[kMarksPerThread - 1];
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        const uint32_t y = __shfl_up(x, o);
-        if (lane >= o) x = max(x, y);
-    }
-    if (lane == 63) S.s_wave[wid] = x;
-    __syncthreads();
-    uint32_t pre = 0;
-#pragma unroll
-    for (int w = 0; w < kWaves; ++w)
-        if (w < wid) pre = max(pre, S.s_wave[w]);
-    uint32_t xe = __shfl_up(x, 1);
-    if (lane == 0) xe = 0;
-    const uint32_t base = max(pre, xe);
-#pragma unroll
-    for (int q = 0; q < kMarksPerThread; ++q) m[q] = (uint16_t)max(v[q], base);
-    __syncthreads();
 }
 
 // Conservative AABB-vs-plane test: true if the box lies entirely on the
@@ -543,6 +690,14 @@ __device__ __forceinline__ bool box_outside(float cx, float cy, float cz, float 
     const float v = nx * cx + ny * cy + nz * cz + fabsf(nx) * hx + fabsf(ny) * hy + fabsf(nz) * hz + o;
     const float mag = fabsf(nx) * (fabsf(cx) + hx) + fabsf(ny) * (fabsf(cy) + hy) + fabsf(nz) * (fabsf(cz) + hz)
                       + fabsf(o);
+    return v < -1e-4f * mag;
+}
+
+// The same test for a rectangle in the xy plane against a plane with nz = 0.
+__device__ __forceinline__ bool rect_outside(float cx, float cy, float h, float nx, float ny, float o)
+{
+    const float v = nx * cx + ny * cy + (fabsf(nx) + fabsf(ny)) * h + o;
+    const float mag = fabsf(nx) * (fabsf(cx) + h) + fabsf(ny) * (fabsf(cy) + h) + fabsf(o);
     return v < -1e-4f * mag;
 }
 
@@ -600,10 +755,11 @@ __device__ __forceinline__ float decode_depth(const RenderParams& P, uint32_t ke
     return P.fast_decode ? rcp_rn(d) : 1.0f / d;
 }
 
-__global__ __launch_bounds__(kBlock, 4) void render_views_kernel(const RenderParams P)
+__global__ __launch_bounds__(kThreads, kMinBlocks) void render_views_kernel(const RenderParams P)
 {
     __shared__ Shared S;
     const int tid = threadIdx.x, lane = lane_id(), wid = tid >> 6;
+    WaveLds& L = S.wv[wid];
     TSTART(t_kernel);
     const int64_t blk = xcd_remap((int64_t)blockIdx.x, P.num_blocks);
     const int tiles = P.tiles_x * P.tiles_y;
@@ -635,20 +791,24 @@ __global__ __launch_bounds__(kBlock, 4) void render_views_kernel(const RenderPar
     T.y0 = (tile / P.tiles_x) * P.tile_h;
     T.w = min(P.tile_w, P.W - T.x0);
     T.h = min(P.tile_h, P.H - T.y0);
+    T.pitch = ((T.w + 31) & ~31) + 4;
     T.kl = ((float)T.x0 - 0.5f) - P.cx;
     T.kr = ((float)(T.x0 + T.w) + 0.5f) - P.cx;
     T.kt = P.cy - ((float)T.y0 - 0.5f);
     T.kb = P.cy - ((float)(T.y0 + T.h) + 0.5f);
     const int npx = T.w * T.h;
+    static_assert(sizeof(Shared) <= 65536, "LDS");
     const bool cull = P.cull != 0;
 
     {
+        // whole padded rows (the pitch is a multiple of 4)
         const u32x4 clr = {kClearKey, kClearKey, kClearKey, kClearKey};
-        const int n4 = npx & ~3;
-        for (int p = 4 * tid; p < n4; p += 4 * kBlock) *(u32x4*)&S.fb[p] = clr;
-        if (tid < npx - n4) S.fb[n4 + tid] = kClearKey;
+        const int n4 = T.h * T.pitch;
+        for (int p = 4 * tid; p < n4; p += 4 * kThreads) *(u32x4*)&S.fb[p] = clr;
     }
-    if (tid == 0) { S.n_cells = 0; S.n_vis = 0; S.n_big = 0; S.big_next = 0; }
+    // per-lane constants of the 8x8 block raster: pixel (lane & 7, lane >> 3)
+    const float pxl = (float)(lane & 7) + P.hx, pyl = (float)(lane >> 3) + P.hy;
+    const int loff4 = ((lane >> 3) * T.pitch + (lane & 7)) * 4;
     if (P.stats && tid < kNumStats) S.stat[tid] = 0;
 
     // world-space frustum planes of the tile: four side planes through the
@@ -685,32 +845,51 @@ __global__ __launch_bounds__(kBlock, 4) void render_views_kernel(const RenderPar
     }
     const int rw = ix1 - ix0 + 1, rh = iy1 - iy0 + 1;
     const int nrect = (rw > 0 && rh > 0) ? rw * rh : 0;
+    const float rrw = rw > 0 ? 1.0f / (float)rw : 0.0f;
+    const float hc = 0.5f * cs + grid.margin;   // half extent of a cell rectangle widened by the margin
     const int64_t abase_w = (int64_t)w * P.A;
-    int nq = 0;   // depth of this wave's survivor queue (wave-uniform)
+    if (tid == 0) { STAT(kStTiles, 1); STAT(kStCellsRect, nrect); }
     __syncthreads();
-    if (tid == 0) { STAT(0, 1); STAT(1, nrect); }
-    TACC(16, t_kernel);
+    TACC(kCycPrologue, t_kernel);
 
-    // ---- candidates: static triangles, then agent boxes, then drain ------
-    // One phase = one block-wide setup (with barriers) followed by per-wave
-    // work without barriers.  A single loop keeps a single inlined copy of
-    // the first and exact passes (instruction-cache footprint).
-    enum { kStatic = 0, kBoxes = 1, kDrain = 2 };
-    int rb = 0, ab = 0;
-    uint32_t total = 0, kb = 0, nc = 0;
-    bool static_done = nrect == 0;
+    // ---- per-wave pipeline: sources -> first pass -> queue -> exact pass ----
+    // One loop with one inlined copy of the first and exact passes keeps the
+    // whole kernel in the instruction cache.
+    enum { kStatic = 0, kBoxes = 1, kDone = 2 };
+    int phase = kStatic;
+    // wave w of the view takes the cells (and agents) whose index is w mod kViewWaves
+    int chunk = 0;                   // next 64-cell chunk of this wave
+    int achunk = 0;                  // next 64-agent chunk of this wave
+    uint32_t total = 0, s0 = 0;      // candidate slots of the current chunk, next slot
+    uint32_t my_start = 0, my_pre = 0;   // lane i: visible cell i (first triangle, exclusive prefix) or agent i
+    int nvis = 0, cfirst = 0;
+    int nq = 0;                      // depth of this wave's survivor queue (wave-uniform)
     for (;;) {
-        int kind = kDrain;
-        uint32_t nphase = 0;
-        TSTART(t_setup);
-        if (!static_done) {
-            while (kb >= total && rb < nrect) {
-                // test one cell per thread, compact the visible ones
-                const int r = rb + tid;
-                bool vis = false;
-                uint32_t start = 0, cnt = 0;
-                if (r < nrect) {
-                    const int c = grid.cell_base + (iy0 + r / rw) * grid.nx + (ix0 + r % rw);
+        TSTART(t_src);
+        // refill: the next chunk of cells (then of agents) with a visible member
+        while (phase == kStatic && s0 >= total) {
+            if (chunk * 64 * kViewWaves >= nrect) { phase = kBoxes; total = 0; s0 = 0; break; }
+            const int r = (chunk * 64 + lane) * kViewWaves + wid;
+            ++chunk;
+            bool vis = false;
+            uint32_t start = 0, cnt = 0;
+            if (r < nrect) {
+                int iy = (int)(((float)r + 0.5f) * rrw);
+                int ix = r - iy * rw;
+                if (ix < 0) { --iy; ix += rw; }
+                if (ix >= rw) { ++iy; ix -= rw; }
+                bool pre = true;
+                if (cull) {
+                    const float ccx = (grid.ox + ((float)(ix0 + ix) + 0.5f) * cs) - cam.x;
+                    const float ccy = (grid.oy + ((float)(iy0 + iy) + 0.5f) * cs) - cam.y;
+                    pre = !rect_outside(ccx, ccy, hc, F.n[0][0], F.n[0][1], F.o[0]) &&
+                          !rect_outside(ccx, ccy, hc, F.n[1][0], F.n[1][1], F.o[1]) &&
+                          !rect_outside(ccx, ccy, hc, F.n[4][0], F.n[4][1], F.o[4]) &&
+                          !rect_outside(ccx, ccy, hc, F.n[5][0], F.n[5][1], F.o[5]);
+                }
+                if (pre) {
+                    STAT(kStCellsPre, 1);
+                    const int c = grid.cell_base + (iy0 + iy) * grid.nx + (ix0 + ix);
                     start = P.scene.cell_start[c];
                     cnt = P.scene.cell_start[c + 1] - start;
                     if (cnt > 0) {
@@ -721,156 +900,105 @@ __global__ __launch_bounds__(kBlock, 4) void render_views_kernel(const RenderPar
                         }
                     }
                 }
-                const uint32_t slot = wave_append(vis, &S.n_cells);
-                if (vis) { S.cl_start[slot] = start; S.cl_pre[slot] = cnt; STAT(2, 1); STAT(3, cnt); }
-                __syncthreads();
-                nc = S.n_cells;
-                {
-                    const uint32_t cn = tid < (int)nc ? S.cl_pre[tid] : 0u;
-                    uint32_t tot;
-                    const uint32_t off = block_excl_scan(cn, S.s_wave, tot);
-                    if (tid < (int)nc) S.cl_pre[tid] = off;
-                    if (tid == 0) { S.cl_pre[nc] = tot; S.n_cells = 0; }
-                }
-                __syncthreads();
-                total = S.cl_pre[nc];
-                kb = 0;
-                rb += kBlock;
-                __syncthreads();   // the list may be rewritten by the next batch
             }
-            if (kb < total) {
-                kind = kStatic;
-                nphase = min(total - kb, (uint32_t)kCandCap);
-                if (tid == 0) STAT(15, 1);
-                for (int q = tid; q < kCandCap / 2; q += kBlock) ((uint32_t*)S.u.mark)[q] = 0u;
-                __syncthreads();
-                if (tid < (int)nc) {
-                    const uint32_t ca = S.cl_pre[tid], ce = S.cl_pre[tid + 1];
-                    if (ce > kb && ca < kb + nphase) S.u.mark[ca > kb ? ca - kb : 0u] = (uint16_t)(tid + 1);
-                }
-                __syncthreads();
-                max_scan_marks(S);
-            } else {
-                static_done = true;
+            const uint64_t m = __ballot(vis);
+            nvis = __popcll(m);
+            if (nvis == 0) continue;
+            if (vis) {
+                const uint32_t slot = mbcnt(m);
+                L.u.cells.start[slot] = start;
+                L.u.cells.count[slot] = cnt;
+                STAT(kStCellsVis, 1);
+                STAT(kStCand, cnt);
             }
+            __builtin_amdgcn_wave_barrier();
+            const uint32_t cn = lane < nvis ? L.u.cells.count[lane] : 0u;
+            my_start = lane < nvis ? L.u.cells.start[lane] : 0u;
+            my_pre = wave_excl_scan(cn, total);
+            s0 = 0;
+            cfirst = 0;
+            __builtin_amdgcn_wave_barrier();
         }
-        if (static_done) {
-            if (ab < P.A) {
-                // box cull of one batch of agents, ballot compaction
-                kind = kBoxes;
-                const int ai = ab + tid;
-                bool vis = false;
-                if (ai < P.A && ai != a) {
-                    vis = true;
-                    if (cull) {
-                        const int64_t h = abase_w + ai;
-                        const float x = P.ax[h], y = P.ay[h], z0 = P.az0[h];
-                        const float R = 0.5f * (P.al[h] + P.aw[h]) * 1.0009765625f + 0.0009765625f;
-                        vis = aabb_visible(P, T, F, cam, x - R, y - R, z0, x + R, y + R, z0 + P.ah[h]);
-                    }
+        while (phase == kBoxes && s0 >= total) {
+            if (achunk * 64 * kViewWaves >= P.A) { phase = kDone; break; }
+            const int ai = (achunk * 64 + lane) * kViewWaves + wid;
+            ++achunk;
+            bool vis = false;
+            if (ai < P.A && ai != a) {
+                vis = true;
+                if (cull) {
+                    const int64_t h = abase_w + ai;
+                    const float x = P.ax[h], y = P.ay[h], z0 = P.az0[h];
+                    const float R = 0.5f * (P.al[h] + P.aw[h]) * 1.0009765625f + 0.0009765625f;
+                    vis = aabb_visible(P, T, F, cam, x - R, y - R, z0, x + R, y + R, z0 + P.ah[h]);
                 }
-                const uint32_t slot = wave_append(vis, &S.n_vis);
-                if (vis) { S.u.vis[slot] = (uint32_t)ai; STAT(4, 1); STAT(5, 12); }
-                __syncthreads();
-                nphase = S.n_vis * 12u;
-                ab += kAgentBatch;
-            } else {
-                // drain: pool the leftover survivors of all waves
-                if (lane == 0) S.nq_w[wid] = (uint32_t)nq;
-                __syncthreads();
             }
+            const uint64_t m = __ballot(vis);
+            nvis = __popcll(m);
+            if (nvis == 0) continue;
+            if (vis) {
+                L.u.agents[mbcnt(m)] = (uint32_t)ai;
+                STAT(kStBoxesVis, 1);
+                STAT(kStBoxTris, 12);
+            }
+            __builtin_amdgcn_wave_barrier();
+            my_start = lane < nvis ? L.u.agents[lane] : 0u;
+            total = 12u * (uint32_t)nvis;
+            s0 = 0;
+            __builtin_amdgcn_wave_barrier();
         }
-        TACC(17, t_setup);
-        // per-wave work: first pass over 64 candidates at a time and an exact
-        // pass on every 64 survivors; when draining, exact passes over the
-        // pooled leftovers
-        long long t_exact_sum = 0;
-        TSTART(t_work);
-        uint32_t pw[kWaves + 1];
-        uint32_t nbatch = 0;
-        pw[0] = 0;
-        if (kind == kDrain) {
-#pragma unroll
-            for (int q = 0; q < kWaves; ++q) pw[q + 1] = pw[q] + S.nq_w[q];
-            nbatch = (pw[kWaves] + 63u) / 64u;
-        }
-        for (uint32_t it = 0;; ++it) {
-            bool run = false, live = false;
+        TACC(kCycSource, t_src);
+        if (phase != kDone) {
+            // first pass over candidate slots s0 .. s0 + 63
+            TSTART(t_first);
+            const uint32_t slot = s0 + (uint32_t)lane;
             uint32_t entry = 0;
-            if (kind != kDrain) {
-                const uint32_t bb = 64u * (wid + kWaves * it);
-                if (bb >= nphase) break;
-                const uint32_t kk = bb + lane;
-                bool surv = false;
-                uint32_t val = 0;
-                if (kk < nphase) {
-                    float tri[9];
-                    uint32_t cls;
-                    if (kind == kStatic) {
-                        // (the clamp only turns a mapping slip into a parity failure, never an OOB read)
-                        const uint32_t j = min((uint32_t)S.u.mark[kk] - 1u, nc - 1u);
-                        val = S.cl_start[j] + (kb + kk - S.cl_pre[j]);
-                        load_static(P, val, tri, cls);
-                    } else {
-                        const uint32_t aj = S.u.vis[kk / 12u];
-                        const uint32_t face = kk % 12u;
-                        load_box(P, abase_w + aj, (int)face, tri, cls);
-                        val = kBoxFlag | (aj << 4) | face;
-                    }
-                    surv = first_pass(P, T, cam, tri, cull);
+            float tri[9] = {};
+            uint32_t cls = 0;
+            if (phase == kStatic) {
+                // cells overlapping the slots (every visible cell holds a triangle)
+                uint32_t bstart = 0, bpre = 0;
+                int c = cfirst;
+                for (; c < nvis; ++c) {
+                    const uint32_t pc = readlane(my_pre, c);
+                    if (pc >= s0 + 64u) break;
+                    const uint32_t sc = readlane(my_start, c);
+                    if (slot >= pc) { bstart = sc; bpre = pc; }
                 }
-                if (surv) STAT(6, 1);
-                nq = queue_push(S, wid, nq, surv, val);
-                if (nq >= 64) {
-                    nq -= 64;
-                    run = true;
-                    live = true;
-                    entry = S.q[wid][nq + lane];
-                }
+                // the cell holding slot s0 + 64: the one that ended the loop if it starts there, else the last visited
+                cfirst = (c < nvis && readlane(my_pre, c) == s0 + 64u) ? c : max(c - 1, 0);
+                entry = bstart + (slot - bpre);
+                if (slot < total) load_static(P, entry, tri, cls);
             } else {
-                const uint32_t batch = wid + kWaves * it;
-                if (batch >= nbatch) break;
-                const uint32_t e = 64u * batch + lane;
-                run = true;
-                live = e < pw[kWaves];
-                if (live) {
-                    int src = 0;
-#pragma unroll
-                    for (int q = 1; q < kWaves; ++q)
-                        if (e >= pw[q]) src = q;
-                    entry = S.q[src][e - pw[src]];
-                }
+                // slot = 12 * (visible agent) + face; the multiply-shift divides exactly for slot < 831
+                const uint32_t vi = (slot * 43691u) >> 19;
+                const uint32_t face = slot - 12u * vi;
+                const uint32_t ai = (uint32_t)__shfl((int)my_start, (int)min(vi, 63u));
+                entry = kBoxFlag | (ai << 4) | face;
+                if (slot < total) load_box(P, abase_w + ai, (int)face, tri, cls);
             }
-            if (run) {
-                if (lane == 0) STAT(7, 1);
-                TSTART(t_ex);
-                exact_pass(P, S, T, cam, live, entry, abase_w);
-                if (P.stats) t_exact_sum += (long long)__builtin_amdgcn_s_memtime() - t_ex;
-            }
+            const bool surv = slot < total && first_pass(P, T, cam, tri, cull);
+            if (surv) STAT(kStSurv, 1);
+            STAT1(kStChunks, 1);
+            nq = queue_push(L, nq, surv, entry);
+            s0 += 64;
+            TACC(kCycFirst, t_first);
         }
-        if (P.stats && lane == 0) {
-            atomicAdd(&S.stat[19], (uint32_t)t_exact_sum);
-            atomicAdd(&S.stat[18], (uint32_t)((long long)__builtin_amdgcn_s_memtime() - t_work - t_exact_sum));
+        if (nq >= 64 || (phase == kDone && nq > 0)) {
+            // exact pass over the newest 64 survivors (or all that are left)
+            const int n = min(nq, 64);
+            const bool live = lane < n;
+            const uint32_t entry = live ? L.q[nq - n + lane] : 0u;
+            nq -= n;
+            __builtin_amdgcn_wave_barrier();
+            STAT1(kStExact, 1);
+            TSTART(t_ex);
+            exact_pass(P, S, T, cam, live, entry, abase_w, pxl, pyl, loff4);
+            TACC(kCycExact, t_ex);
         }
-        TSTART(t_bar);
-        __syncthreads();
-        TACC(20, t_bar);
-        // rasterize the queued large triangles once the queue is half full,
-        // and at the end
-        if (kind == kDrain || S.n_big >= (uint32_t)(kBigCap / 2)) {
-            drain_big(P, S, T);
-            __syncthreads();
-            if (tid == 0) { S.n_big = 0; S.big_next = 0; }
-            __syncthreads();
-        }
-        if (kind == kDrain) break;
-        if (kind == kStatic) {
-            kb += kCandCap;
-        } else {
-            if (tid == 0) S.n_vis = 0;
-            __syncthreads();
-        }
+        if (phase == kDone && nq == 0) break;
     }
+    __syncthreads();
 
     // ---- R8 resolve + coalesced write-out of the tile ----
     TSTART(t_out);
@@ -879,9 +1007,9 @@ __global__ __launch_bounds__(kBlock, 4) void render_views_kernel(const RenderPar
     float* odep = P.out_depth + v * view_px;
     if (P.vec_out && (P.W % 16) == 0 && (T.w % 16) == 0) {
         const int u16 = T.w / 16, n16 = u16 * T.h;
-        for (int u = tid; u < n16; u += kBlock) {
+        for (int u = tid; u < n16; u += kThreads) {
             const int row = u / u16, c16 = u % u16;
-            const u32x4* src = (const u32x4*)&S.fb[row * T.w + 16 * c16];
+            const u32x4* src = (const u32x4*)&S.fb[row * T.pitch + 16 * c16];
             uint32_t wd[4];
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
@@ -893,9 +1021,9 @@ __global__ __launch_bounds__(kBlock, 4) void render_views_kernel(const RenderPar
         }
         const int u4 = T.w / 4, n4 = u4 * T.h;
         const float inf = __uint_as_float(0x7F800000u);
-        for (int u = tid; u < n4; u += kBlock) {
+        for (int u = tid; u < n4; u += kThreads) {
             const int row = u / u4, c4 = u % u4;
-            const u32x4 kq = *(const u32x4*)&S.fb[row * T.w + 4 * c4];
+            const u32x4 kq = *(const u32x4*)&S.fb[row * T.pitch + 4 * c4];
             f32x4 d = {inf, inf, inf, inf};
             if ((kq.x & kq.y & kq.z & kq.w) >> 8 != 0xFFFFFFu) {   // not all background
                 d.x = (kq.x >> 8) == 0xFFFFFFu ? inf : decode_depth(P, kq.x);
@@ -906,16 +1034,16 @@ __global__ __launch_bounds__(kBlock, 4) void render_views_kernel(const RenderPar
             __builtin_nontemporal_store(d, (f32x4*)(odep + (int64_t)(T.y0 + row) * P.W + T.x0 + 4 * c4));
         }
     } else {
-        for (int p = tid; p < npx; p += kBlock) {
+        for (int p = tid; p < npx; p += kThreads) {
             const int row = p / T.w, col = p % T.w;
-            const uint32_t key = S.fb[p];
+            const uint32_t key = S.fb[row * T.pitch + col];
             const int64_t o = (int64_t)(T.y0 + row) * P.W + T.x0 + col;
             ocls[o] = (uint8_t)(key & 255u);
             odep[o] = (key >> 8) == 0xFFFFFFu ? __uint_as_float(0x7F800000u) : decode_depth(P, key);
         }
     }
     if (P.stats) {
-        TACC(23, t_out);
+        TACC(kCycWriteout, t_out);
         __syncthreads();
         if (tid < kNumStats) atomicAdd(&P.stats[tid], (unsigned long long)S.stat[tid]);
     }
@@ -924,7 +1052,7 @@ __global__ __launch_bounds__(kBlock, 4) void render_views_kernel(const RenderPar
 hipError_t launch_render(const RenderParams& p, hipStream_t s)
 {
     if (p.num_blocks <= 0) return hipSuccess;
-    hipLaunchKernelGGL(render_views_kernel, dim3((unsigned)p.num_blocks), dim3(kBlock), 0, s, p);
+    hipLaunchKernelGGL(render_views_kernel, dim3((unsigned)p.num_blocks), dim3(kThreads), 0, s, p);
     return hipGetLastError();
 }
 

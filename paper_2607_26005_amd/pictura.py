@@ -86,11 +86,10 @@ EXPORTED = ["pictura_create", "pictura_destroy", "pictura_last_error", "pictura_
             "pictura_bin_scene", "pictura_render_views", "pictura_agents_step", "pictura_bins_info",
             "pictura_bins_copy", "pictura_set_option", "pictura_stats_copy", "pictura_selftest_rcp"]
 
-STAT_NAMES = ["view_tiles", "cells_in_rect", "cells_visible", "cand_tris", "boxes_visible", "box_tris",
-              "first_pass_survivors", "exact_batches", "clipped", "raster_tris", "area_ok", "wave_tris",
-              "lane_px", "wave_covered_px", "big_queue_overflow", "cand_passes",
-              "cyc_prologue", "cyc_phase_setup", "cyc_first_pass", "cyc_exact", "cyc_phase_barrier",
-              "cyc_wave_raster", "wave_lane_slots", "cyc_writeout"]
+STAT_NAMES = ["view_tiles", "cells_in_rect", "cells_prefiltered", "cells_visible", "cand_tris", "boxes_visible",
+              "box_tris", "first_pass_survivors", "exact_batches", "clipped", "raster_tris", "lane_tris",
+              "lane_px", "record_tris", "record_tris_fp64", "blocks_tested", "blocks_passed", "first_pass_chunks",
+              "cyc_prologue", "cyc_sources", "cyc_first_pass", "cyc_exact", "cyc_records", "cyc_writeout"]
 
 
 def _ptr(a) -> Optional[int]:
