@@ -45,7 +45,10 @@
 #pragma clang fp contract(off)
 
 #ifndef PICTURA_VIEW_WAVES
-#define PICTURA_VIEW_WAVES 1
+#define PICTURA_VIEW_WAVES 2
+#endif
+#ifndef PICTURA_SMALL_PX
+#define PICTURA_SMALL_PX 32
 #endif
 
 namespace pictura {
@@ -57,8 +60,8 @@ constexpr uint32_t kClearKey = (0xFFFFFFu << 8) | 4u;
 constexpr uint32_t kBoxFlag = 0x80000000u;
 constexpr int kViewWaves = PICTURA_VIEW_WAVES;   // waves per view tile
 constexpr int kThreads = 64 * kViewWaves;
-constexpr int kMinBlocks = kViewWaves >= 2 ? 1 : 2; // at least two waves per SIMD fit the register budget
-constexpr int kSmallPx = 8;       // bounding boxes of at most this many pixels are rasterized by one lane
+constexpr int kWavesPerSimd = 4;  // register budget: four waves per SIMD (as many as the LDS admits)
+constexpr int kSmallPx = PICTURA_SMALL_PX;   // bounding boxes of at most this many pixels are rasterized by one lane
 constexpr int kQueue = 128;       // per-wave queue of first-pass survivors
 // Framebuffer rows are padded to a pitch of 4 mod 32 words, so the 64 lanes
 // of an 8x8 block hit every LDS bank exactly twice.
@@ -367,8 +370,10 @@ __device__ __forceinline__ I edge_f(int ax, int ay, int bx, int by, int i, int j
     return imul<I>(dx, 256 * j + 128 - ay) - imul<I>(dy, 256 * i + 128 - ax) + (I)(tl - 1);
 }
 
-// A small triangle rasterized by its own lane over its bounding box.
-template <typename I>
+// A small triangle rasterized by its own lane over its bounding box.  With
+// Exact (P.pix_exact) the pixel-centre offset of the next column is the
+// previous one plus 1, exactly.
+template <typename I, bool Exact>
 __device__ __forceinline__ void raster_lane(const RenderParams& P, Shared& S, const Tile& T, int X0, int Y0, int X1,
                                             int Y1, int X2, int Y2, int i0, int i1, int j0, int j1, float pa,
                                             float pb, float pc, uint32_t cls)
@@ -378,16 +383,22 @@ __device__ __forceinline__ void raster_lane(const RenderParams& P, Shared& S, co
     I f2 = edge_f<I>(X0, Y0, X1, Y1, i0, j0);
     const I sx0 = (I)(Y1 - Y2) * 256, sx1 = (I)(Y2 - Y0) * 256, sx2 = (I)(Y0 - Y1) * 256;
     const I sy0 = (I)(X2 - X1) * 256, sy1 = (I)(X0 - X2) * 256, sy2 = (I)(X1 - X0) * 256;
+    const uint32_t kcls = cls;
+    const float px0 = ((float)i0 + 0.5f) - P.cx;
     for (int j = j0; j <= j1; ++j) {
         I g0 = f0, g1 = f1, g2 = f2;
         const float pyf = ((float)j + 0.5f) - P.cy;
+        const float inner = fmaf(pb, pyf, pc);
         uint32_t* row = &S.fb[(j - T.y0) * T.pitch - T.x0];
+        float pxf = px0;
         for (int i = i0; i <= i1; ++i) {
-            if ((g0 | g1 | g2) >= 0) {
-                const float pxf = ((float)i + 0.5f) - P.cx;
-                atomicMin(&row[i], pixel_key(P, pxf, pyf, pa, pb, pc, cls));
-            }
+            if constexpr (!Exact) pxf = ((float)i + 0.5f) - P.cx;
+            const float iz = fmaf(pa, pxf, inner);
+            const uint32_t bits = min(__float_as_uint(iz), __float_as_uint(P.izcap));
+            const uint32_t key = ((P.qbase - (bits >> 3)) << 8) | kcls;
+            if (((g0 | g1 | g2) >= 0) & (iz >= P.izfar)) atomicMin(&row[i], key);
             g0 += sx0; g1 += sx1; g2 += sx2;
+            if constexpr (Exact) pxf += 1.0f;
         }
         f0 += sy0; f1 += sy1; f2 += sy2;
     }
@@ -407,8 +418,7 @@ __device__ __forceinline__ void raster_lane(const RenderParams& P, Shared& S, co
 // exceeds the sum of all other terms by 2^9 and fixes the sign of every sum.
 // Fast: the tile is a whole number of blocks and pixel-centre offsets are
 // exact sums (P.pix_exact), so no lane leaves the tile and the offset of a
-// pixel centre is the lane's own plus the block's.  Rejected lanes take part
-// in the atomic with the neutral key, at an address inside the framebuffer.
+// pixel centre is the lane's own plus the block's.
 template <bool I32, bool Fast>
 __device__ __forceinline__ void raster_blocks(const RenderParams& P, Shared& S, const Tile& T, const uint32_t* u,
                                               float pa, float pb, float pc, uint32_t box, uint32_t j1w,
@@ -455,7 +465,6 @@ __device__ __forceinline__ void raster_blocks(const RenderParams& P, Shared& S, 
             pass = pass & ((Cc[k] + d) + off[k] >= 0.0);
         }
     }
-    const int base4 = (Y * T.pitch + X) * 4;
     const float pxu = (float)(T.x0 + X), pyu = (float)(T.y0 + Y);
     const uint32_t xy = (uint32_t)X | ((uint32_t)Y << 8);
     uint64_t m = __ballot(pass);
@@ -466,11 +475,13 @@ __device__ __forceinline__ void raster_blocks(const RenderParams& P, Shared& S, 
     while (m) {
         const int b = __builtin_ctzll(m);
         m &= m - 1;
+        const uint32_t q = readlane(xy, b);
+        const int bX = (int)(q & 255u), bY = (int)(q >> 8);
         bool cov;
         if constexpr (I32) {
-            const int e0 = Eb[0] + (int)readlane((uint32_t)off[0], b);
-            const int e1 = Eb[1] + (int)readlane((uint32_t)off[1], b);
-            const int e2 = Eb[2] + (int)readlane((uint32_t)off[2], b);
+            const int e0 = Eb[0] + (A[0] * bX + B[0] * bY);
+            const int e1 = Eb[1] + (A[1] * bX + B[1] * bY);
+            const int e2 = Eb[2] + (A[2] * bX + B[2] * bY);
             cov = (e0 | e1 | e2) >= 0;
         } else {
             const double e0 = Eb[0] + readlane_d(off[0], b);
@@ -483,8 +494,6 @@ __device__ __forceinline__ void raster_blocks(const RenderParams& P, Shared& S, 
             pxf = pxl + readlane_f(pxu, b);
             pyf = pyl + readlane_f(pyu, b);
         } else {
-            const uint32_t q = readlane(xy, b);
-            const int bX = (int)(q & 255u), bY = (int)(q >> 8);
             cov = cov & (lx < T.w - bX) & (ly < T.h - bY);
             pxf = ((float)(T.x0 + bX + lx) + 0.5f) - P.cx;
             pyf = ((float)(T.y0 + bY + ly) + 0.5f) - P.cy;
@@ -492,9 +501,7 @@ __device__ __forceinline__ void raster_blocks(const RenderParams& P, Shared& S, 
         const float iz = fmaf(pa, pxf, fmaf(pb, pyf, pc));
         const uint32_t bits = min(__float_as_uint(iz), __float_as_uint(P.izcap));
         const uint32_t key = ((P.qbase - (bits >> 3)) << 8) | cls;
-        const bool ok = cov && iz >= P.izfar;
-        const int addr = (int)readlane((uint32_t)base4, b) + loff4;
-        atomicMin((uint32_t*)((char*)S.fb + addr), ok ? key : 0xFFFFFFFFu);
+        if (cov && iz >= P.izfar) atomicMin((uint32_t*)((char*)S.fb + ((bY * T.pitch + bX) * 4 + loff4)), key);
     }
 }
 
@@ -598,11 +605,15 @@ __device__ __forceinline__ void exact_pass(const RenderParams& P, Shared& S, con
                         } else {
                             STAT(kStLaneTris, 1);
                             STAT(kStLanePx, npx);
-                            if (small_span)
-                                raster_lane<int>(P, S, T, ax, ay, bx, by, cx, cy, i0, i1, j0, j1, pa, pb, pc, cls);
-                            else
-                                raster_lane<long long>(P, S, T, ax, ay, bx, by, cx, cy, i0, i1, j0, j1, pa, pb, pc,
+                            if (small_span && P.pix_exact)
+                                raster_lane<int, true>(P, S, T, ax, ay, bx, by, cx, cy, i0, i1, j0, j1, pa, pb, pc,
                                                        cls);
+                            else if (small_span)
+                                raster_lane<int, false>(P, S, T, ax, ay, bx, by, cx, cy, i0, i1, j0, j1, pa, pb, pc,
+                                                        cls);
+                            else
+                                raster_lane<long long, false>(P, S, T, ax, ay, bx, by, cx, cy, i0, i1, j0, j1, pa,
+                                                              pb, pc, cls);
                         }
                     }
                 }
@@ -755,7 +766,7 @@ __device__ __forceinline__ float decode_depth(const RenderParams& P, uint32_t ke
     return P.fast_decode ? rcp_rn(d) : 1.0f / d;
 }
 
-__global__ __launch_bounds__(kThreads, kMinBlocks) void render_views_kernel(const RenderParams P)
+__global__ __launch_bounds__(kThreads, kWavesPerSimd) void render_views_kernel(const RenderParams P)
 {
     __shared__ Shared S;
     const int tid = threadIdx.x, lane = lane_id(), wid = tid >> 6;
@@ -857,7 +868,8 @@ __global__ __launch_bounds__(kThreads, kMinBlocks) void render_views_kernel(cons
     // whole kernel in the instruction cache.
     enum { kStatic = 0, kBoxes = 1, kDone = 2 };
     int phase = kStatic;
-    // wave w of the view takes the cells (and agents) whose index is w mod kViewWaves
+    // wave w of the view takes the cells (and agents) whose index is w mod
+    // kViewWaves; each wave exact-passes its own survivors
     int chunk = 0;                   // next 64-cell chunk of this wave
     int achunk = 0;                  // next 64-agent chunk of this wave
     uint32_t total = 0, s0 = 0;      // candidate slots of the current chunk, next slot
