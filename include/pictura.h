@@ -181,11 +181,11 @@ pictura_status pictura_set_option(pictura_ctx ctx, int32_t option, int32_t value
 pictura_status pictura_stats_copy(pictura_ctx ctx, uint64_t* out, int32_t n, int32_t reset);
 
 /* Device self-check of the reciprocal the kernels use in place of IEEE
- * division where the argument lies in [2^-12, 2^20) (hardware reciprocal plus
+ * division where |argument| lies in [2^-12, 2^20) (hardware reciprocal plus
  * one fused Newton step): *mismatches receives the number of fp32 values x
  * whose bit patterns lie in [lo_bits, lo_bits + count) for which it differs
  * from the correctly rounded 1.0f / x.  Synchronous.  EINVAL: null output or
- * a range reaching past the finite floats. */
+ * a range reaching past the finite floats of lo_bits' sign. */
 pictura_status pictura_selftest_rcp(pictura_ctx ctx, uint32_t lo_bits, uint32_t count, uint64_t* mismatches);
 
 #ifdef __cplusplus

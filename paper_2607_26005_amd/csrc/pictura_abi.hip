@@ -430,7 +430,8 @@ pictura_status pictura_selftest_rcp(pictura_ctx c, uint32_t lo_bits, uint32_t co
     if (!c) return PICTURA_EINVAL;
     c->err.clear();
     if (!mismatches) return fail(c, PICTURA_EINVAL, "selftest_rcp: null output");
-    if ((uint64_t)lo_bits + count > 0x7F800000ull) return fail(c, PICTURA_EINVAL, "selftest_rcp: range leaves the finite floats");
+    if ((uint64_t)(lo_bits & 0x7FFFFFFFu) + count > 0x7F800000ull)
+        return fail(c, PICTURA_EINVAL, "selftest_rcp: range leaves the finite floats of one sign");
     DeviceGuard dg(c->device);
     unsigned long long* d = nullptr;
     hipError_t e;

@@ -88,12 +88,15 @@ struct Tile {
 // pixel (i, j) is
 //   E_k = c_k + a_k i + b_k j,   a_k = -256 dy_k,  b_k = 256 dx_k,
 // with c_k its value at the tile's pixel (0, 0) plus the top-left bias;
-// covered iff every E_k >= 0.  The exact pass leaves a record in the lane of
-// its triangle as twelve words: the int32 path (every value over the tile
-// fits) holds a0 a1 a2 b0 b1 b2 c0 c1 c2; the fp64 path holds c_k as doubles
-// (words 0..5) and dx_k, dy_k (words 6..11).  c_k is an integer below 2^61:
-// as a double it is exact below 2^53, and beyond that its rounding keeps the
-// sign, which no pixel of the tile can change.
+// covered iff every E_k >= 0.  Since a_k and b_k are multiples of 256,
+//   floor(E_k / 256) = floor(c_k / 256) - dy_k i + dx_k j
+// exactly, and it has the sign of E_k: the int32 path tests that instead.
+// The exact pass leaves a record in the lane of its triangle as twelve
+// words: the int32 path (every value over the tile fits) holds -dy_k, dx_k,
+// floor(c_k / 256) in words 0..8; the fp64 path holds c_k as doubles (words
+// 0..5) and dx_k, dy_k (words 6..11).  c_k is an integer below 2^61: as a
+// double it is exact below 2^53, and beyond that its rounding keeps the sign,
+// which no pixel of the tile can change.
 
 // Per-wave LDS: the visible-cell (or agent) list of a refill and the queue
 // of first-pass survivors.
@@ -132,9 +135,10 @@ static_assert(kCycWriteout + 1 == kNumStats, "stat count");
 // arithmetic
 // ---------------------------------------------------------------------------
 
-// Correctly rounded 1/x for x in [2^-12, 2^20): hardware reciprocal plus one
-// Newton step with fused residual.  Equality with IEEE division over every
-// fp32 value of that range is checked on the device (pictura_selftest_rcp).
+// Correctly rounded 1/x for |x| in [2^-12, 2^20): hardware reciprocal plus
+// one Newton step with fused residual.  Equality with IEEE division over
+// every fp32 value of that range, of either sign, is checked on the device
+// (pictura_selftest_rcp).
 __device__ __forceinline__ float rcp_rn(float x)
 {
     const float r = __builtin_amdgcn_rcpf(x);
@@ -143,6 +147,15 @@ __device__ __forceinline__ float rcp_rn(float x)
 }
 
 __device__ __forceinline__ bool rcp_rn_ok(float x) { return x >= 0.000244140625f && x < 1048576.0f; }
+
+// Correctly rounded 1/x for any x: the division runs only when a lane of the
+// wave needs it.
+__device__ __forceinline__ float recip_rn(float x)
+{
+    const bool ok = rcp_rn_ok(fabsf(x));
+    if (__ballot(!ok) == 0) return rcp_rn(x);
+    return ok ? rcp_rn(x) : 1.0f / x;
+}
 
 __device__ __forceinline__ uint32_t mbcnt(uint64_t m)
 {
@@ -207,7 +220,7 @@ __device__ __forceinline__ bool depth_plane(const RenderParams& P, const Cam& c,
     const float nz = Nx * c.cc + Ny * c.sc;
     const float delta = (Nx * d0x + Ny * d0y) + Nz * d0z;
     if (delta == 0.0f || !isfinite(delta)) return false;
-    const float rd = 1.0f / delta;
+    const float rd = recip_rn(delta);
     pa = (nx * rd) * P.rfx;
     pb = -((ny * rd) * P.rfy);
     pc = nz * rd;
@@ -217,7 +230,7 @@ __device__ __forceinline__ bool depth_plane(const RenderParams& P, const Cam& c,
 // R5
 __device__ __forceinline__ bool snap_vertex(const RenderParams& P, float xv, float yv, float zv, int& X, int& Y)
 {
-    const float rz = rcp_rn_ok(zv) ? rcp_rn(zv) : 1.0f / zv;
+    const float rz = recip_rn(zv);
     const float qx = xv * rz, qy = yv * rz;
     const float mx = P.fx256 * qx, my = P.fy256 * qy;
     const float sx = P.cx256 + mx, sy = P.cy256 - my;
@@ -411,8 +424,9 @@ __device__ __forceinline__ void raster_lane(const RenderParams& P, Shared& S, co
 // (l & 7, l >> 3): its edge values at that pixel of block (0, 0) plus the
 // block's offsets, which the lane that tested the block computed.
 //
-// int32 path (I32): |dx|, |dy| < 2^15 and |c| < 2^30, so a_k, b_k fit a
-// 24-bit multiply and |E| < 2^30 + 2 * 63 * 2^23 < 2^31 anywhere in the tile.
+// int32 path (I32): the scaled edge floor(E / 256) with |dx|, |dy| < 2^22 and
+// |floor(c / 256)| < 2^30, so dx, dy fit a 24-bit multiply and the value stays
+// below 2^30 + 2 * 63 * 2^22 < 2^31 anywhere in the tile.
 // fp64 path: |a_k|, |b_k| <= 2^38, so with tile coordinates below 64 every
 // product and partial sum is an exact integer when |c| < 2^52; otherwise |c|
 // exceeds the sum of all other terms by 2^9 and fixes the sign of every sum.
@@ -636,17 +650,18 @@ __device__ __forceinline__ void exact_pass(const RenderParams& P, Shared& S, con
                 const int tl = (dy < 0) || (dy == 0 && dx > 0);
                 cv[k] = (long long)dx * (long long)(py0 - ey[k]) - (long long)dy * (long long)(px0 - ex[k]) +
                         (long long)(tl - 1);
-                e32 = e32 && dx > -32768 && dx < 32768 && dy > -32768 && dy < 32768 && cv[k] > -1073741824ll &&
-                      cv[k] < 1073741824ll;
+                const long long c8 = cv[k] >> 8;   // floor(c / 256)
+                e32 = e32 && dx > -4194304 && dx < 4194304 && dy > -4194304 && dy < 4194304 &&
+                      c8 > -1073741824ll && c8 < 1073741824ll;
                 dxs[k] = dx;
                 dys[k] = dy;
             }
 #pragma unroll
             for (int k = 0; k < 3; ++k) {
                 if (e32) {
-                    rv[k] = (uint32_t)(-(dys[k] * 256));
-                    rv[3 + k] = (uint32_t)(dxs[k] * 256);
-                    rv[6 + k] = (uint32_t)(int)cv[k];
+                    rv[k] = (uint32_t)(-dys[k]);
+                    rv[3 + k] = (uint32_t)dxs[k];
+                    rv[6 + k] = (uint32_t)(int)(cv[k] >> 8);
                 } else {
                     const unsigned long long cb = (unsigned long long)__double_as_longlong((double)cv[k]);
                     rv[2 * k] = (uint32_t)cb;

@@ -177,6 +177,40 @@ def test_camera_inside_box_and_near_clipped_ground(lib):
     check_views(lib, wl, np.arange(wl.num_views), "inside-box")
 
 
+def test_edge_paths_all_exercised(lib):
+    """A 2 km ground quad seen from 1.5 m, a mid-size box and small far
+    boxes: near-clipped ground triangles reach 2^22 subpixels per edge (fp64
+    edge path), the box faces take the int32 record path and the far boxes the
+    single-lane raster.  The kernel's own counters show every path ran."""
+    torch = _torch()
+    G = 1000.0
+    tris = quad((-G, -G, 0.0), (G, -G, 0.0), (G, G, 0.0), (-G, G, 0.0))
+    scene = make_scene(tris, [0, 0])
+    rows = [(0.0, 0.0, 0.0, 1.0, 0.0, 4.5, 1.9, 1.5, 3),
+            (9.0, 1.0, 0.0, 1.0, 0.0, 4.5, 1.9, 1.5, 3)] + \
+           [(60.0 + 7.0 * k, -20.0 + 9.0 * k, 0.0, 0.6, 0.8, 1.0, 0.8, 1.2, 6) for k in range(6)]
+    ag = make_agents(rows)
+    rig = make_rig(mounts=((0.0, 0.0, 1.5, 1.0, 0.0),), far=100.0)
+    wl = sg.Workload("paths", 0, 0, scene, ag, rig, 16.0, 2000.0)
+    r = lib.Renderer(0)
+    try:
+        r.set_option(lib.OPT_STATS, 1)
+        r.upload(wl.scene, 16.0)
+        da = lib.DeviceAgents.from_host(wl.agents)
+        c, d = r.render(da, wl.rig)
+        torch.cuda.synchronize()
+        st = lib.pictura_stats_copy(r.ctx)
+    finally:
+        r.close()
+    print(f"[paths] {st}", flush=True)
+    assert st["record_tris_fp64"] > 0
+    assert st["record_tris"] - st["record_tris_fp64"] > 0
+    assert st["lane_tris"] > 0
+    ora = O.render(wl.scene, wl.agents, wl.rig)
+    s = assert_parity(c.cpu().numpy(), d.cpu().numpy(), ora, "paths")
+    print(f"[paths] {s}", flush=True)
+
+
 def test_random_small_scenes(lib):
     from tests.test_oracle_pins import _random_scene
     for seed in range(12):
@@ -286,14 +320,16 @@ def test_abi_errors(lib):
 
 def test_fast_reciprocal_is_correctly_rounded(lib):
     # The kernels replace IEEE division by rcp + one fused Newton step where
-    # the argument lies in [2^-12, 2^20); check every fp32 value there.
+    # |argument| lies in [2^-12, 2^20); check every fp32 value there, of
+    # both signs (the sign bit is 0x80000000).
     ctx = lib.pictura_create(0)
     try:
         lo = int(np.float32(2.0 ** -12).view(np.uint32))
         hi = int(np.float32(2.0 ** 20).view(np.uint32))
         bad = 0
-        for start in range(lo, hi, 1 << 26):
-            bad += lib.pictura_selftest_rcp(ctx, start, min(1 << 26, hi - start))
+        for sign in (0, 0x80000000):
+            for start in range(lo, hi, 1 << 26):
+                bad += lib.pictura_selftest_rcp(ctx, sign | start, min(1 << 26, hi - start))
         assert bad == 0
     finally:
         lib.pictura_destroy(ctx)
