@@ -48,7 +48,7 @@
 #define PICTURA_VIEW_WAVES 2
 #endif
 #ifndef PICTURA_SMALL_PX
-#define PICTURA_SMALL_PX 32
+#define PICTURA_SMALL_PX 64
 #endif
 
 namespace pictura {
@@ -174,6 +174,38 @@ __device__ __forceinline__ double readlane_d(double v, int l)
     const unsigned long long b = (unsigned long long)__double_as_longlong(v);
     const unsigned long long lo = readlane((uint32_t)b, l), hi = readlane((uint32_t)(b >> 32), l);
     return __longlong_as_double((long long)((hi << 32) | lo));
+}
+
+// Inclusive scans over the wave with DPP row shifts and row broadcasts (no
+// LDS round trip): shifts by 1, 2, 4, 8 within each row of 16 lanes (lanes
+// shifted in read 0), then the last lane of row 0 (and of row 2) into rows 1
+// and 3, then the last lane of row 1 into rows 2 and 3.
+template <int Ctrl, int RowMask, bool BoundZero>
+__device__ __forceinline__ uint32_t dpp_mov(uint32_t x)
+{
+    return (uint32_t)__builtin_amdgcn_update_dpp(0, (int)x, Ctrl, RowMask, 0xf, BoundZero);
+}
+
+__device__ __forceinline__ uint32_t wave_incl_max(uint32_t x)
+{
+    x = max(x, dpp_mov<0x111, 0xf, true>(x));
+    x = max(x, dpp_mov<0x112, 0xf, true>(x));
+    x = max(x, dpp_mov<0x114, 0xf, true>(x));
+    x = max(x, dpp_mov<0x118, 0xf, true>(x));
+    x = max(x, dpp_mov<0x142, 0xa, false>(x));
+    x = max(x, dpp_mov<0x143, 0xc, false>(x));
+    return x;
+}
+
+__device__ __forceinline__ uint32_t wave_incl_sum(uint32_t x)
+{
+    x += dpp_mov<0x111, 0xf, true>(x);
+    x += dpp_mov<0x112, 0xf, true>(x);
+    x += dpp_mov<0x114, 0xf, true>(x);
+    x += dpp_mov<0x118, 0xf, true>(x);
+    x += dpp_mov<0x142, 0xa, false>(x);
+    x += dpp_mov<0x143, 0xc, false>(x);
+    return x;
 }
 
 // Exclusive prefix sum over the wave; `total` receives the sum of all lanes.
@@ -417,6 +449,73 @@ __device__ __forceinline__ void raster_lane(const RenderParams& P, Shared& S, co
     }
 }
 
+// Rasterize the small triangles of the wave's lanes together: the pixels of
+// their bounding boxes are numbered consecutively (exclusive prefix over the
+// lanes) and every step hands 64 of them to the 64 lanes.  The lane owning
+// slot k is found by marking where each triangle's range starts and taking
+// a running maximum over the wave; its setup (edge values at the box corner
+// and per-column / per-row steps, exact in int32 because the triangle spans
+// fewer than 2^14 subpixels) is fetched from that lane with ds_bpermute.
+__device__ __forceinline__ uint32_t bperm(int owner, uint32_t v)
+{
+    return (uint32_t)__builtin_amdgcn_ds_bpermute(owner * 4, (int)v);
+}
+
+__device__ __forceinline__ void raster_packed(const RenderParams& P, Shared& S, WaveLds& L, const Tile& T, bool on,
+                                              int X0, int Y0, int X1, int Y1, int X2, int Y2, int i0, int i1, int j0,
+                                              int j1, float pa, float pb, float pc, uint32_t cls)
+{
+    const int lane = lane_id();
+    const int w = i1 - i0 + 1;
+    const uint32_t npx = on ? (uint32_t)(w * (j1 - j0 + 1)) : 0u;
+    const uint32_t incl = wave_incl_sum(npx);
+    const uint32_t n = readlane(incl, 63), pre = incl - npx;
+    const int f0 = edge_f<int>(X1, Y1, X2, Y2, i0, j0);
+    const int f1 = edge_f<int>(X2, Y2, X0, Y0, i0, j0);
+    const int f2 = edge_f<int>(X0, Y0, X1, Y1, i0, j0);
+    const int sx0 = (Y1 - Y2) * 256, sx1 = (Y2 - Y0) * 256, sx2 = (Y0 - Y1) * 256;
+    const int sy0 = (X2 - X1) * 256, sy1 = (X0 - X2) * 256, sy2 = (X1 - X0) * 256;
+    const uint32_t geo = (uint32_t)(i0 - T.x0) | (uint32_t)(j0 - T.y0) << 8 | (uint32_t)w << 16 | cls << 24;
+    const float rw = __builtin_amdgcn_rcpf((float)w);   // row = floor((p + 0.5) / w) for p < 2^12
+    uint32_t carry = 0;
+    uint32_t* mark = L.u.cells.start;
+    for (uint32_t s0 = 0; s0 < n; s0 += 64) {
+        mark[lane] = 0u;
+        __builtin_amdgcn_wave_barrier();
+        if (npx != 0 && pre >= s0 && pre < s0 + 64u) mark[pre - s0] = (uint32_t)lane + 1u;
+        __builtin_amdgcn_wave_barrier();
+        const uint32_t o = wave_incl_max(max(mark[lane], carry));
+        carry = readlane(o, 63);
+        const int t = (int)o - 1;
+        const uint32_t slot = s0 + (uint32_t)lane;
+        const int p = (int)(slot - bperm(t, pre));
+        const uint32_t g = bperm(t, geo);
+        const int tw = (int)((g >> 16) & 255u);
+        const int tn = (int)bperm(t, npx);
+        const int jj = (int)(((float)p + 0.5f) * __uint_as_float(bperm(t, __float_as_uint(rw))));
+        const int ii = p - jj * tw;
+        const int e0 = (int)bperm(t, (uint32_t)f0) + __mul24(ii, (int)bperm(t, (uint32_t)sx0)) +
+                       __mul24(jj, (int)bperm(t, (uint32_t)sy0));
+        const int e1 = (int)bperm(t, (uint32_t)f1) + __mul24(ii, (int)bperm(t, (uint32_t)sx1)) +
+                       __mul24(jj, (int)bperm(t, (uint32_t)sy1));
+        const int e2 = (int)bperm(t, (uint32_t)f2) + __mul24(ii, (int)bperm(t, (uint32_t)sx2)) +
+                       __mul24(jj, (int)bperm(t, (uint32_t)sy2));
+        const int x = (int)(g & 255u) + ii, y = (int)((g >> 8) & 255u) + jj;
+        const float pxf = ((float)(T.x0 + x) + 0.5f) - P.cx;
+        const float pyf = ((float)(T.y0 + y) + 0.5f) - P.cy;
+        const float tpa = __uint_as_float(bperm(t, __float_as_uint(pa)));
+        const float tpb = __uint_as_float(bperm(t, __float_as_uint(pb)));
+        const float tpc = __uint_as_float(bperm(t, __float_as_uint(pc)));
+        const float iz = fmaf(tpa, pxf, fmaf(tpb, pyf, tpc));
+        const uint32_t bits = min(__float_as_uint(iz), __float_as_uint(P.izcap));
+        const uint32_t key = ((P.qbase - (bits >> 3)) << 8) | (g >> 24);
+        // (p in range keeps the address inside the tile whatever the owner search found)
+        if ((slot < n) & (p >= 0) & (p < tn) & ((e0 | e1 | e2) >= 0) & (iz >= P.izfar))
+            atomicMin(&S.fb[y * T.pitch + x], key);
+        __builtin_amdgcn_wave_barrier();
+    }
+}
+
 // Rasterize one record with the whole wave.  Lane b tests 8x8 block b of
 // the bounding box (a tile has at most 8 x 8 blocks): the edge value at the
 // block corner that maximises it must be >= 0 for all three edges.  The
@@ -523,7 +622,7 @@ __device__ __forceinline__ void raster_blocks(const RenderParams& P, Shared& S, 
 // exact pass: one queued survivor per live lane
 // ---------------------------------------------------------------------------
 
-__device__ __forceinline__ void exact_pass(const RenderParams& P, Shared& S, const Tile& T, const Cam& cam,
+__device__ __forceinline__ void exact_pass(const RenderParams& P, Shared& S, WaveLds& L, const Tile& T, const Cam& cam,
                                            bool live, uint32_t entry, int64_t abase_w, float pxl, float pyl,
                                            int loff4)
 {
@@ -587,7 +686,7 @@ __device__ __forceinline__ void exact_pass(const RenderParams& P, Shared& S, con
     // fan triangles (p0, p1, p2) and (p0, p2, p3)
 #pragma unroll 1
     for (int f = 0; f < nfan; ++f) {
-        bool big = false;
+        bool big = false, packed = false;
         const int ax = X0, ay = Y0;
         int bx = f == 0 ? X1 : X2, by = f == 0 ? Y1 : Y2;
         int cx = f == 0 ? X2 : X3, cy = f == 0 ? Y2 : Y3;
@@ -619,12 +718,8 @@ __device__ __forceinline__ void exact_pass(const RenderParams& P, Shared& S, con
                         } else {
                             STAT(kStLaneTris, 1);
                             STAT(kStLanePx, npx);
-                            if (small_span && P.pix_exact)
-                                raster_lane<int, true>(P, S, T, ax, ay, bx, by, cx, cy, i0, i1, j0, j1, pa, pb, pc,
-                                                       cls);
-                            else if (small_span)
-                                raster_lane<int, false>(P, S, T, ax, ay, bx, by, cx, cy, i0, i1, j0, j1, pa, pb, pc,
-                                                        cls);
+                            if (small_span)
+                                packed = true;
                             else
                                 raster_lane<long long, false>(P, S, T, ax, ay, bx, by, cx, cy, i0, i1, j0, j1, pa,
                                                               pb, pc, cls);
@@ -633,6 +728,8 @@ __device__ __forceinline__ void exact_pass(const RenderParams& P, Shared& S, con
                 }
             }
         }
+        if (__ballot(packed) != 0)
+            raster_packed(P, S, L, T, packed, ax, ay, bx, by, cx, cy, i0, i1, j0, j1, pa, pb, pc, cls);
         uint64_t m = __ballot(big);
         if (m == 0) continue;
         // record of this lane's triangle: edges v1->v2, v2->v0, v0->v1 at the tile's pixel (0, 0)
@@ -1020,7 +1117,7 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd) void render_views_kernel(c
             __builtin_amdgcn_wave_barrier();
             STAT1(kStExact, 1);
             TSTART(t_ex);
-            exact_pass(P, S, T, cam, live, entry, abase_w, pxl, pyl, loff4);
+            exact_pass(P, S, L, T, cam, live, entry, abase_w, pxl, pyl, loff4);
             TACC(kCycExact, t_ex);
         }
         if (phase == kDone && nq == 0) break;
