@@ -453,28 +453,22 @@ __device__ __forceinline__ void raster_lane(const RenderParams& P, Shared& S, co
 // their bounding boxes are numbered consecutively (exclusive prefix over the
 // lanes) and every step hands 64 of them to the 64 lanes.  The lane owning
 // slot k is found by marking where each triangle's range starts and taking
-// a running maximum over the wave; its setup (edge values at the box corner
-// and per-column / per-row steps, exact in int32 because the triangle spans
-// fewer than 2^14 subpixels) is fetched from that lane with ds_bpermute.
+// a running maximum over the wave; its setup (the int32 record words, see
+// above) is fetched from that lane with ds_bpermute.
 __device__ __forceinline__ uint32_t bperm(int owner, uint32_t v)
 {
     return (uint32_t)__builtin_amdgcn_ds_bpermute(owner * 4, (int)v);
 }
 
 __device__ __forceinline__ void raster_packed(const RenderParams& P, Shared& S, WaveLds& L, const Tile& T, bool on,
-                                              int X0, int Y0, int X1, int Y1, int X2, int Y2, int i0, int i1, int j0,
-                                              int j1, float pa, float pb, float pc, uint32_t cls)
+                                              const uint32_t* rv, int i0, int i1, int j0, int j1, float pa,
+                                              float pb, float pc, uint32_t cls)
 {
     const int lane = lane_id();
     const int w = i1 - i0 + 1;
     const uint32_t npx = on ? (uint32_t)(w * (j1 - j0 + 1)) : 0u;
     const uint32_t incl = wave_incl_sum(npx);
     const uint32_t n = readlane(incl, 63), pre = incl - npx;
-    const int f0 = edge_f<int>(X1, Y1, X2, Y2, i0, j0);
-    const int f1 = edge_f<int>(X2, Y2, X0, Y0, i0, j0);
-    const int f2 = edge_f<int>(X0, Y0, X1, Y1, i0, j0);
-    const int sx0 = (Y1 - Y2) * 256, sx1 = (Y2 - Y0) * 256, sx2 = (Y0 - Y1) * 256;
-    const int sy0 = (X2 - X1) * 256, sy1 = (X0 - X2) * 256, sy2 = (X1 - X0) * 256;
     const uint32_t geo = (uint32_t)(i0 - T.x0) | (uint32_t)(j0 - T.y0) << 8 | (uint32_t)w << 16 | cls << 24;
     const float rw = __builtin_amdgcn_rcpf((float)w);   // row = floor((p + 0.5) / w) for p < 2^12
     uint32_t carry = 0;
@@ -494,13 +488,11 @@ __device__ __forceinline__ void raster_packed(const RenderParams& P, Shared& S, 
         const int tn = (int)bperm(t, npx);
         const int jj = (int)(((float)p + 0.5f) * __uint_as_float(bperm(t, __float_as_uint(rw))));
         const int ii = p - jj * tw;
-        const int e0 = (int)bperm(t, (uint32_t)f0) + __mul24(ii, (int)bperm(t, (uint32_t)sx0)) +
-                       __mul24(jj, (int)bperm(t, (uint32_t)sy0));
-        const int e1 = (int)bperm(t, (uint32_t)f1) + __mul24(ii, (int)bperm(t, (uint32_t)sx1)) +
-                       __mul24(jj, (int)bperm(t, (uint32_t)sy1));
-        const int e2 = (int)bperm(t, (uint32_t)f2) + __mul24(ii, (int)bperm(t, (uint32_t)sx2)) +
-                       __mul24(jj, (int)bperm(t, (uint32_t)sy2));
         const int x = (int)(g & 255u) + ii, y = (int)((g >> 8) & 255u) + jj;
+        // scaled edge values floor(E / 256) at the tile-local pixel (x, y)
+        const int e0 = (int)bperm(t, rv[6]) + __mul24((int)bperm(t, rv[0]), x) + __mul24((int)bperm(t, rv[3]), y);
+        const int e1 = (int)bperm(t, rv[7]) + __mul24((int)bperm(t, rv[1]), x) + __mul24((int)bperm(t, rv[4]), y);
+        const int e2 = (int)bperm(t, rv[8]) + __mul24((int)bperm(t, rv[2]), x) + __mul24((int)bperm(t, rv[5]), y);
         const float pxf = ((float)(T.x0 + x) + 0.5f) - P.cx;
         const float pyf = ((float)(T.y0 + y) + 0.5f) - P.cy;
         const float tpa = __uint_as_float(bperm(t, __float_as_uint(pa)));
@@ -680,18 +672,19 @@ __device__ __forceinline__ void exact_pass(const RenderParams& P, Shared& S, Wav
         if (!ok) np = 0;
     }
     const int nfan = __ballot(np == 4) != 0 ? 2 : 1;
-    bool have_plane = false, plane_bad = false;
+    // R3 depth plane of the unclipped triangle (shared by its fan pieces)
     float pa = 0.0f, pb = 0.0f, pc = 0.0f;
+    if (np != 0 && !depth_plane(P, cam, tri, pa, pb, pc)) np = 0;
     const int px0 = 256 * T.x0 + 128, py0 = 256 * T.y0 + 128;
     // fan triangles (p0, p1, p2) and (p0, p2, p3)
 #pragma unroll 1
     for (int f = 0; f < nfan; ++f) {
-        bool big = false, packed = false;
+        bool valid = false;
         const int ax = X0, ay = Y0;
         int bx = f == 0 ? X1 : X2, by = f == 0 ? Y1 : Y2;
         int cx = f == 0 ? X2 : X3, cy = f == 0 ? Y2 : Y3;
         int i0 = 0, i1 = -1, j0 = 0, j1 = -1;
-        if (live && f + 2 < np && !plane_bad) {
+        if (f + 2 < np) {
             const int minX = min(ax, min(bx, cx)), maxX = max(ax, max(bx, cx));
             const int minY = min(ay, min(by, cy)), maxY = max(ay, max(by, cy));
             i0 = max((minX - 128 + 255) >> 8, T.x0); i1 = min((maxX - 128) >> 8, T.x0 + T.w - 1);
@@ -707,36 +700,15 @@ __device__ __forceinline__ void exact_pass(const RenderParams& P, Shared& S, Wav
                         const int tx = bx, ty = by;
                         bx = cx; by = cy; cx = tx; cy = ty;
                     }
-                    if (!have_plane) {
-                        have_plane = depth_plane(P, cam, tri, pa, pb, pc);
-                        plane_bad = !have_plane;
-                    }
-                    if (have_plane) {
-                        const int npx = (i1 - i0 + 1) * (j1 - j0 + 1);
-                        if (npx > kSmallPx) {
-                            big = true;
-                        } else {
-                            STAT(kStLaneTris, 1);
-                            STAT(kStLanePx, npx);
-                            if (small_span)
-                                packed = true;
-                            else
-                                raster_lane<long long, false>(P, S, T, ax, ay, bx, by, cx, cy, i0, i1, j0, j1, pa,
-                                                              pb, pc, cls);
-                        }
-                    }
+                    valid = true;
                 }
             }
         }
-        if (__ballot(packed) != 0)
-            raster_packed(P, S, L, T, packed, ax, ay, bx, by, cx, cy, i0, i1, j0, j1, pa, pb, pc, cls);
-        uint64_t m = __ballot(big);
-        if (m == 0) continue;
-        // record of this lane's triangle: edges v1->v2, v2->v0, v0->v1 at the tile's pixel (0, 0)
+        // edge setup: edges v1->v2, v2->v0, v0->v1 at the tile's pixel (0, 0),
+        // in the int32 form (floor(c / 256), -dy, dx) when every value fits
         uint32_t rv[12] = {0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
-        uint32_t rbox = 0, rj1 = 0;
-        if (big) {
-            bool e32 = true;
+        bool e32 = true;
+        if (valid) {
             const int ex[3] = {bx, cx, ax}, ey[3] = {by, cy, ay};
             const int fx[3] = {cx, ax, bx}, fy[3] = {cy, ay, by};
             long long cv[3];
@@ -767,6 +739,21 @@ __device__ __forceinline__ void exact_pass(const RenderParams& P, Shared& S, Wav
                     rv[9 + k] = (uint32_t)dys[k];
                 }
             }
+        }
+        const int npx = (i1 - i0 + 1) * (j1 - j0 + 1);
+        const bool big = valid && npx > kSmallPx;
+        const bool packed = valid && npx <= kSmallPx && e32;
+        if (valid && npx <= kSmallPx) {
+            STAT(kStLaneTris, 1);
+            STAT(kStLanePx, npx);
+            if (!e32)
+                raster_lane<long long, false>(P, S, T, ax, ay, bx, by, cx, cy, i0, i1, j0, j1, pa, pb, pc, cls);
+        }
+        if (__ballot(packed) != 0) raster_packed(P, S, L, T, packed, rv, i0, i1, j0, j1, pa, pb, pc, cls);
+        uint64_t m = __ballot(big);
+        if (m == 0) continue;
+        uint32_t rbox = 0, rj1 = 0;
+        if (big) {
             rbox = cls | (uint32_t)(i0 - T.x0) << 8 | (uint32_t)(i1 - T.x0) << 16 | (uint32_t)(j0 - T.y0) << 24;
             rj1 = (uint32_t)(j1 - T.y0) | (e32 ? 256u : 0u);
             STAT(kStRecTris, 1);
