@@ -48,7 +48,7 @@
 #define PICTURA_VIEW_WAVES 2
 #endif
 #ifndef PICTURA_SMALL_PX
-#define PICTURA_SMALL_PX 64
+#define PICTURA_SMALL_PX 128
 #endif
 
 namespace pictura {
