@@ -211,13 +211,7 @@ __device__ __forceinline__ uint32_t wave_incl_sum(uint32_t x)
 // Exclusive prefix sum over the wave; `total` receives the sum of all lanes.
 __device__ __forceinline__ uint32_t wave_excl_scan(uint32_t v, uint32_t& total)
 {
-    const int lane = lane_id();
-    uint32_t x = v;
-#pragma unroll
-    for (int o = 1; o < 64; o <<= 1) {
-        const uint32_t y = __shfl_up(x, o);
-        if (lane >= o) x += y;
-    }
+    const uint32_t x = wave_incl_sum(v);
     total = readlane(x, 63);
     return x - v;
 }
