@@ -11,6 +11,8 @@ write roofline fraction (HIP events on the launch stream) and the CPU
 oracle timed on a bounded sample of the same workload.
 
     python bench.py [--steps 100] [--warmup 10] [--config 4] [--no-cpu-baseline]
+
+(--config 6 times the paper's own rig: 2,048 egos x 4 views at 96x54.)
 """
 import argparse
 import json

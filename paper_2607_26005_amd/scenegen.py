@@ -406,7 +406,38 @@ CONFIGS = {
     3: dict(name="dense_traffic", seed=2, worlds=256, size=1000.0, agents=128, cams=4, res=64, far=100.0, cell=16.0),
     4: dict(name="throughput_headline", seed=3, worlds=1024, size=1000.0, agents=64, cams=4, res=64, far=150.0, cell=24.0),
     5: dict(name="highres_large_scene", seed=4, worlds=128, size=4000.0, agents=64, cams=4, res=128, far=200.0, cell=32.0),
+    # the paper's own rig and batch: 2048 egos x 4 views at 96x54 (App. A.2, Tab. camera_rig; Tab. render_mem)
+    6: dict(name="paper_rig", seed=5, worlds=64, size=1000.0, agents=32, cams="paper", res=(96, 54), far=100.0, cell=16.0),
 }
+
+
+# The paper's four-camera rig (App. A.2, Tab. camera_rig): a 1920x1080 sensor
+# with a 1545 px focal length rendered at 96x54, so the focal length scales by
+# 96 / 1920 to 77.25 px; per-camera extrinsics in the ego frame (x forward,
+# y left, z up, metres; yaw about z, degrees).
+PAPER_SENSOR = (1920, 1080, 1545.0)
+PAPER_RENDER = (96, 54)
+PAPER_MOUNTS = ((1.66, -0.01, 1.49, 0.0),     # front
+                (1.63, 0.12, 1.48, 55.0),     # front-left
+                (1.62, -0.16, 1.49, -55.0),   # front-right
+                (-0.47, 0.02, 1.43, 180.0))   # back
+
+
+def make_paper_rig(far: float = 100.0, near: float = 0.5) -> Rig:
+    sw, sh, f = PAPER_SENSOR
+    w, h = PAPER_RENDER
+    fs = f * w / sw
+    mounts = []
+    for x, y, z, yaw in PAPER_MOUNTS:
+        if yaw == 0.0:
+            c, s = 1.0, 0.0
+        elif yaw == 180.0:
+            c, s = -1.0, 0.0
+        else:
+            c, s = float(np.cos(np.radians(yaw))), float(np.sin(np.radians(yaw)))
+        mounts.append([x, y, z, c, s])
+    return Rig(width=w, height=h, fx=fs, fy=fs, cx=w / 2.0, cy=h / 2.0, near=near, far=far,
+               mount=np.asarray(mounts, np.float32))
 
 
 def make_rig(num_cams: int, res: int, far: float, near: float = 0.5, cam_height: float = 1.5) -> Rig:
@@ -426,7 +457,7 @@ def _build_world(cfg_id: int, cfg: dict, w: int):
     if cfg_id == 1:
         return _grid_world(rng, size, 10.0, 2, [2], 2.0, False, cfg["agents"], 8.0, 0.0, 0.0,
                            fixed_centres=[-50.0, 50.0])
-    if cfg_id in (2, 4):
+    if cfg_id in (2, 4, 6):
         return _grid_world(rng, size, 25.0, 6, [2, 3, 4], 2.5, True, cfg["agents"], 8.0, 0.1, 0.0)
     if cfg_id == 3:
         return _grid_world(rng, size, 25.0, 6, [2, 3, 4], 2.5, True, cfg["agents"], 0.0, 0.1, 0.2)
@@ -436,7 +467,7 @@ def _build_world(cfg_id: int, cfg: dict, w: int):
 
 
 def make_config(cfg_id: int, num_worlds: Optional[int] = None, init_speed_seed: bool = True) -> Workload:
-    """Build workload `cfg_id` (1..5), optionally only its first `num_worlds` worlds."""
+    """Build workload `cfg_id` (1..6), optionally only its first `num_worlds` worlds."""
     cfg = CONFIGS[cfg_id]
     nw = cfg["worlds"] if num_worlds is None else int(num_worlds)
     A = cfg["agents"]
@@ -466,7 +497,7 @@ def make_config(cfg_id: int, num_worlds: Optional[int] = None, init_speed_seed: 
                     length=cat("L"), width=cat("W"), height=cat("H"),
                     cls=np.ascontiguousarray(np.concatenate([a.cls for a in ag_parts])),
                     psi=cat("psi"), speed=speed)
-    rig = make_rig(cfg["cams"], cfg["res"], cfg["far"])
+    rig = make_paper_rig(cfg["far"]) if cfg["cams"] == "paper" else make_rig(cfg["cams"], cfg["res"], cfg["far"])
     return Workload(name=cfg["name"], config=cfg_id, seed=cfg["seed"], scene=scene, agents=agents,
                     rig=rig, cell_size=cfg["cell"], world_size=size)
 

@@ -103,6 +103,12 @@ def test_highres_tiled_sampled(lib):
     check_views(lib, wl, sample_views(wl.num_views, 48, 24), "highres")
 
 
+def test_paper_rig_sampled(lib):
+    # the paper's rig (96x54, f = 77.25 px, yaws 0 / +-55 / 180): two tiles per view
+    wl = workload(6, 8)
+    check_views(lib, wl, sample_views(wl.num_views, 160, 26), "paper-rig")
+
+
 # ---- invariances: culling, tiling, cell size, permutation, duplication -------
 
 def _small():
