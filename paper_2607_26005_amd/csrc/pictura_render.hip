@@ -62,7 +62,7 @@ constexpr int kViewWaves = PICTURA_VIEW_WAVES;   // waves per view tile
 constexpr int kThreads = 64 * kViewWaves;
 constexpr int kWavesPerSimd = 4;  // register budget: four waves per SIMD (as many as the LDS admits)
 constexpr int kSmallPx = PICTURA_SMALL_PX;   // bounding boxes of at most this many pixels are rasterized by one lane
-constexpr int kQueue = 128;       // per-wave queue of first-pass survivors
+constexpr int kQueue = 192;       // per-wave queue of first-pass survivors
 // Framebuffer rows are padded to a pitch of 4 mod 32 words, so the 64 lanes
 // of an 8x8 block hit every LDS bank exactly twice.
 constexpr int kFbCap = 64 * 68;
@@ -495,9 +495,12 @@ __device__ __forceinline__ void raster_packed(const RenderParams& P, Shared& S, 
         const float iz = fmaf(tpa, pxf, fmaf(tpb, pyf, tpc));
         const uint32_t bits = min(__float_as_uint(iz), __float_as_uint(P.izcap));
         const uint32_t key = ((P.qbase - (bits >> 3)) << 8) | (g >> 24);
-        // (p in range keeps the address inside the tile whatever the owner search found)
-        if ((slot < n) & (p >= 0) & (p < tn) & ((e0 | e1 | e2) >= 0) & (iz >= P.izfar))
-            atomicMin(&S.fb[y * T.pitch + x], key);
+        // p in range keeps the address inside the tile whatever the owner
+        // search found; other lanes take word 0 and the key 0xFFFFFFFF, which
+        // changes nothing, so the LDS minimum needs no branch
+        const bool inr = (slot < n) & (p >= 0) & (p < tn);
+        const bool hit = inr & ((e0 | e1 | e2) >= 0) & (iz >= P.izfar);
+        atomicMin(&S.fb[inr ? y * T.pitch + x : 0], hit ? key : 0xFFFFFFFFu);
         __builtin_amdgcn_wave_barrier();
     }
 }
@@ -566,14 +569,29 @@ __device__ __forceinline__ void raster_blocks(const RenderParams& P, Shared& S, 
     }
     const float pxu = (float)(T.x0 + X), pyu = (float)(T.y0 + Y);
     const uint32_t xy = (uint32_t)X | ((uint32_t)Y << 8);
+    const uint32_t boff = (uint32_t)((Y * T.pitch + X) * 4);   // byte offset of the block in the framebuffer
     uint64_t m = __ballot(pass);
     if (P.stats && lane == 0) {
         atomicAdd(&S.stat[kStBlocksTested], (uint32_t)nb);
         atomicAdd(&S.stat[kStBlocksPassed], (uint32_t)__popcll(m));
     }
-    while (m) {
-        const int b = __builtin_ctzll(m);
-        m &= m - 1;
+    // Lanes that miss the piece take the key 0xFFFFFFFF, which changes
+    // nothing, so the LDS minimum needs no branch (every address lies inside
+    // the framebuffer: rows below 64, columns below the pitch).
+    auto key_at = [&](int b, uint32_t& addr) -> uint32_t {
+        if constexpr (I32 && Fast) {
+            // the block's offsets, as the lane that tested it computed them
+            const int e0 = Eb[0] + (int)readlane((uint32_t)off[0], b);
+            const int e1 = Eb[1] + (int)readlane((uint32_t)off[1], b);
+            const int e2 = Eb[2] + (int)readlane((uint32_t)off[2], b);
+            const float pxf = pxl + readlane_f(pxu, b);
+            const float pyf = pyl + readlane_f(pyu, b);
+            const float iz = fmaf(pa, pxf, fmaf(pb, pyf, pc));
+            const uint32_t bits = min(__float_as_uint(iz), __float_as_uint(P.izcap));
+            const uint32_t key = ((P.qbase - (bits >> 3)) << 8) | cls;
+            addr = readlane(boff, b) + (uint32_t)loff4;
+            return (((e0 | e1 | e2) >= 0) && iz >= P.izfar) ? key : 0xFFFFFFFFu;
+        }
         const uint32_t q = readlane(xy, b);
         const int bX = (int)(q & 255u), bY = (int)(q >> 8);
         bool cov;
@@ -600,7 +618,15 @@ __device__ __forceinline__ void raster_blocks(const RenderParams& P, Shared& S, 
         const float iz = fmaf(pa, pxf, fmaf(pb, pyf, pc));
         const uint32_t bits = min(__float_as_uint(iz), __float_as_uint(P.izcap));
         const uint32_t key = ((P.qbase - (bits >> 3)) << 8) | cls;
-        if (cov && iz >= P.izfar) atomicMin((uint32_t*)((char*)S.fb + ((bY * T.pitch + bX) * 4 + loff4)), key);
+        addr = (uint32_t)((bY * T.pitch + bX) * 4 + loff4);
+        return (cov && iz >= P.izfar) ? key : 0xFFFFFFFFu;
+    };
+    while (m) {
+        const int b0 = __builtin_ctzll(m);
+        m &= m - 1;
+        uint32_t a0;
+        const uint32_t k0 = key_at(b0, a0);
+        atomicMin((uint32_t*)((char*)S.fb + a0), k0);
     }
 }
 
@@ -1053,35 +1079,53 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd) void render_views_kernel(c
             __builtin_amdgcn_wave_barrier();
         }
         TACC(kCycSource, t_src);
-        if (phase != kDone) {
-            // first pass over candidate slots s0 .. s0 + 63
+        if (phase == kStatic) {
+            // first pass over candidate slots s0 .. s0 + 127: both halves' triangles
+            // are loaded before either is tested (one memory round trip)
             TSTART(t_first);
             const uint32_t slot = s0 + (uint32_t)lane;
-            uint32_t entry = 0;
+            // cells overlapping the slots (every visible cell holds a triangle)
+            uint32_t bs0 = 0, bp0 = 0, bs1 = 0, bp1 = 0;
+            int c = cfirst;
+            for (; c < nvis; ++c) {
+                const uint32_t pc = readlane(my_pre, c);
+                if (pc >= s0 + 128u) break;
+                const uint32_t sc = readlane(my_start, c);
+                if (slot >= pc) { bs0 = sc; bp0 = pc; }
+                if (slot + 64u >= pc) { bs1 = sc; bp1 = pc; }
+            }
+            // the cell holding slot s0 + 128: the one that ended the loop if it starts there, else the last visited
+            cfirst = (c < nvis && readlane(my_pre, c) == s0 + 128u) ? c : max(c - 1, 0);
+            const uint32_t e0 = bs0 + (slot - bp0), e1 = bs1 + (slot + 64u - bp1);
+            float t0[9] = {}, t1[9] = {};
+            uint32_t c0 = 0, c1 = 0;
+            if (slot < total) load_static(P, e0, t0, c0);
+            if (slot + 64u < total) load_static(P, e1, t1, c1);
+#pragma unroll 1
+            for (int h = 0; h < 2; ++h) {
+                float tri[9];
+#pragma unroll
+                for (int q = 0; q < 9; ++q) tri[q] = h ? t1[q] : t0[q];
+                const uint32_t sl = slot + 64u * (uint32_t)h;
+                const bool surv = sl < total && first_pass(P, T, cam, tri, cull);
+                if (surv) STAT(kStSurv, 1);
+                STAT1(kStChunks, 1);
+                nq = queue_push(L, nq, surv, h ? e1 : e0);
+            }
+            s0 += 128;
+            TACC(kCycFirst, t_first);
+        } else if (phase == kBoxes) {
+            // first pass over box slots s0 .. s0 + 63
+            TSTART(t_first);
+            const uint32_t slot = s0 + (uint32_t)lane;
             float tri[9] = {};
             uint32_t cls = 0;
-            if (phase == kStatic) {
-                // cells overlapping the slots (every visible cell holds a triangle)
-                uint32_t bstart = 0, bpre = 0;
-                int c = cfirst;
-                for (; c < nvis; ++c) {
-                    const uint32_t pc = readlane(my_pre, c);
-                    if (pc >= s0 + 64u) break;
-                    const uint32_t sc = readlane(my_start, c);
-                    if (slot >= pc) { bstart = sc; bpre = pc; }
-                }
-                // the cell holding slot s0 + 64: the one that ended the loop if it starts there, else the last visited
-                cfirst = (c < nvis && readlane(my_pre, c) == s0 + 64u) ? c : max(c - 1, 0);
-                entry = bstart + (slot - bpre);
-                if (slot < total) load_static(P, entry, tri, cls);
-            } else {
-                // slot = 12 * (visible agent) + face; the multiply-shift divides exactly for slot < 831
-                const uint32_t vi = (slot * 43691u) >> 19;
-                const uint32_t face = slot - 12u * vi;
-                const uint32_t ai = (uint32_t)__shfl((int)my_start, (int)min(vi, 63u));
-                entry = kBoxFlag | (ai << 4) | face;
-                if (slot < total) load_box(P, abase_w + ai, (int)face, tri, cls);
-            }
+            // slot = 12 * (visible agent) + face; the multiply-shift divides exactly for slot < 831
+            const uint32_t vi = (slot * 43691u) >> 19;
+            const uint32_t face = slot - 12u * vi;
+            const uint32_t ai = (uint32_t)__shfl((int)my_start, (int)min(vi, 63u));
+            const uint32_t entry = kBoxFlag | (ai << 4) | face;
+            if (slot < total) load_box(P, abase_w + ai, (int)face, tri, cls);
             const bool surv = slot < total && first_pass(P, T, cam, tri, cull);
             if (surv) STAT(kStSurv, 1);
             STAT1(kStChunks, 1);
@@ -1089,7 +1133,7 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd) void render_views_kernel(c
             s0 += 64;
             TACC(kCycFirst, t_first);
         }
-        if (nq >= 64 || (phase == kDone && nq > 0)) {
+        while (nq >= 64 || (phase == kDone && nq > 0)) {
             // exact pass over the newest 64 survivors (or all that are left)
             const int n = min(nq, 64);
             const bool live = lane < n;
