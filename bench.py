@@ -12,7 +12,8 @@ oracle timed on a bounded sample of the same workload.
 
     python bench.py [--steps 100] [--warmup 10] [--config 4] [--no-cpu-baseline]
 
-(--config 6 times the paper's own rig: 2,048 egos x 4 views at 96x54.)
+(--config 6 times the paper's own rig: 2,048 egos x 4 views at 96x54;
+--config 7 the same rig over towns with walls, parked cars and traffic lights.)
 """
 import argparse
 import json
@@ -89,12 +90,12 @@ def cpu_baseline(wl, target_s):
     rng = np.random.default_rng(1234)
     probe = np.sort(rng.choice(wl.num_views, size=min(32 * threads, wl.num_views), replace=False))
     t0 = time.perf_counter()
-    O.render(wl.scene, wl.agents, wl.rig, view_ids=probe, want_flags=False, num_threads=threads)
+    O.render(wl.scene, wl.agents, wl.rig, view_ids=probe, want_flags=False, num_threads=threads, lights=wl.lights)
     dt = time.perf_counter() - t0
     n = int(min(wl.num_views, max(len(probe), target_s / max(dt / len(probe), 1e-9))))
     ids = np.sort(rng.choice(wl.num_views, size=n, replace=False))
     t0 = time.perf_counter()
-    O.render(wl.scene, wl.agents, wl.rig, view_ids=ids, want_flags=False, num_threads=threads)
+    O.render(wl.scene, wl.agents, wl.rig, view_ids=ids, want_flags=False, num_threads=threads, lights=wl.lights)
     dt = time.perf_counter() - t0
     images_s = n / dt
     C = wl.rig.num_cams
@@ -130,6 +131,8 @@ def main():
     r = pictura.Renderer(0)
     r.upload(wl.scene, wl.cell_size)
     da = pictura.DeviceAgents.from_host(wl.agents)
+    if wl.lights is not None:
+        r.set_lights(pictura.DeviceLights.from_host(wl.lights))
     steer, accel = sg.controls(A, K + Wm, seed=wl.seed)
     steer_d = torch.as_tensor(steer, device="cuda")
     accel_d = torch.as_tensor(accel, device="cuda")
@@ -205,7 +208,8 @@ def main():
         "config": {
             "workload": f"{wl.name}: {wl.scene.num_worlds} worlds x {wl.agents.agents_per_world} agents x "
                         f"{wl.rig.num_cams} cameras, {W}x{H} uint8 class + fp32 depth, "
-                        f"{wl.scene.num_tris // wl.scene.num_worlds} static tris/world, far {wl.rig.far:g} m",
+                        f"{wl.scene.num_tris // wl.scene.num_worlds} static tris/world, far {wl.rig.far:g} m"
+                        + (f", {wl.lights.lights_per_world} traffic lights/world" if wl.lights is not None else ""),
             "views_per_step": V,
             "step": "bicycle update + render" if moving else "render",
         },

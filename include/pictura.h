@@ -99,6 +99,33 @@ typedef struct {
     const float* length; /* wheelbase is 0.6 * length */
 } pictura_agent_state;
 
+/* Traffic lights (paper Sec. 3.2, rendering features: disks visible only
+ * within a limited angular range, drawn for the approach they govern and
+ * culled once the camera faces away).  Device memory, caller-owned, structure
+ * of arrays; light l of world w has index w * lights_per_world + l.  A light
+ * is a disk of radius `radius` centred at (x, y, z) whose normal is the
+ * horizontal unit vector (cos_f, sin_f).  Rule R10: with d = C - centre (C
+ * the camera centre of rule R1), h = cos_f * d.x + sin_f * d.y and
+ * q = (d.x^2 + d.y^2) + d.z^2 (fp32, in this order), a view draws the light
+ * iff h > 0 and h * h >= (cos_max * cos_max) * q.  Rule R11: the disk is 12
+ * triangles (centre, rim k, rim k+1 mod 12), rim k = centre +
+ * radius * (cos 30k deg * u + sin 30k deg * up) with u = (-sin_f, cos_f, 0),
+ * up = (0, 0, 1), the cosines and sines rounded to fp32 and each coordinate
+ * computed as x - (r cos) * sin_f, y + (r cos) * cos_f, z + r sin.  Its
+ * pixels take class cls[l] (e.g. the signal state). */
+typedef struct {
+    int32_t num_worlds;
+    int32_t lights_per_world;
+    const float* x;
+    const float* y;
+    const float* z;
+    const float* cos_f;
+    const float* sin_f;
+    const float* radius;
+    const uint8_t* cls;
+    float cos_max;   /* cosine of the visibility cone's half-angle, in [0, 1] */
+} pictura_lights;
+
 /* Create a context on HIP device `device`.  Returns PICTURA_EDEVICE when no
  * such device exists.  *out is set to NULL on failure. */
 pictura_status pictura_create(int32_t device, pictura_ctx* out);
@@ -126,7 +153,8 @@ pictura_status pictura_scene_upload(pictura_ctx ctx, const pictura_scene* scene,
 pictura_status pictura_bin_scene(pictura_ctx ctx, float cell_size_m, void* stream);
 
 /* Render all V = num_worlds * agents_per_world * num_cams views (paper
- * Sec. 3.2, Eq. obs_pv).  View v = (w * agents_per_world + a) * num_cams + k
+ * Sec. 3.2, Eq. obs_pv), with the traffic lights attached by
+ * pictura_set_lights, if any.  View v = (w * agents_per_world + a) * num_cams + k
  * writes out_cls[v][y][x] (uint8 class; 4 = sky for background) and
  * out_depth[v][y][x] (fp32 view-space depth in metres, +inf for background),
  * row-major, y down.  Both outputs are caller-owned device buffers of
@@ -136,6 +164,17 @@ pictura_status pictura_bin_scene(pictura_ctx ctx, float cell_size_m, void* strea
  * small enough for the 24-bit depth key).  Asynchronous on `stream`. */
 pictura_status pictura_render_views(pictura_ctx ctx, const pictura_agents* agents, const pictura_rig* rig,
                                     uint8_t* out_cls, float* out_depth, void* stream);
+
+/* Attach traffic lights (see pictura_lights) to the context: later
+ * pictura_render_views calls draw them.  The context keeps the pointers, not
+ * a copy: the arrays must stay valid while it renders, and their contents
+ * may change between render calls (a signal changing state is a new cls
+ * value, ordered on the render stream like any other input).  NULL, or
+ * lights_per_world == 0, detaches.  EINVAL: num_worlds < 1, null arrays,
+ * lights_per_world > 2^20, cos_max outside [0, 1]; a render call returns
+ * EINVAL when num_worlds differs from its scene's.  ERANGE: more than
+ * 2^31 - 1 lights.  No device work; synchronous. */
+pictura_status pictura_set_lights(pictura_ctx ctx, const pictura_lights* lights);
 
 /* One kinematic-bicycle step for every agent (the per-step agent motion of
  * the headline workload): v' = clamp(v + accel * dt, 0, vmax);

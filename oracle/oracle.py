@@ -40,6 +40,7 @@ def lib():
         L.oracle_render.restype = ctypes.c_int
         L.oracle_render.argtypes = [ctypes.c_int, p, p, p,
                                     ctypes.c_int, p, p, p, p, p, p, p, p, p,
+                                    ctypes.c_int, p, p, p, p, p, p, p, ctypes.c_float,
                                     ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                     ctypes.c_float, ctypes.c_float, ctypes.c_float, ctypes.c_float,
                                     ctypes.c_float, ctypes.c_float, p,
@@ -63,10 +64,11 @@ def _c(a, dtype):
     return np.ascontiguousarray(a, dtype=dtype)
 
 
-def render(scene, agents, rig, view_ids=None, want_flags=True, want_cover=False, num_threads=0):
+def render(scene, agents, rig, view_ids=None, want_flags=True, want_cover=False, num_threads=0, lights=None):
     """Render the selected views (default: all).  Returns dict with
     cls [n,H,W] u8, depth [n,H,W] f32, flags [n,H,W] u8 (bit0 EDGE, bit1 TIE),
-    and cover [n,H,W] u16 when requested."""
+    and cover [n,H,W] u16 when requested.  lights: object with
+    lights_per_world, x, y, z, cos_f, sin_f, radius, cls, cos_max (or None)."""
     L = lib()
     A = int(agents.agents_per_world)
     C = int(rig.mount.shape[0])
@@ -85,8 +87,16 @@ def render(scene, agents, rig, view_ids=None, want_flags=True, want_cover=False,
           ("x", "y", "z0", "cos_h", "sin_h", "length", "width", "height")]
     acls = _c(agents.cls, np.uint8)
     mount = _c(rig.mount, np.float32)
+    NL = int(lights.lights_per_world) if lights is not None else 0
+    if NL > 0:
+        lf = [_c(getattr(lights, f), np.float32) for f in ("x", "y", "z", "cos_f", "sin_f", "radius")]
+        lc = _c(lights.cls, np.uint8)
+        cmax = float(lights.cos_max)
+    else:
+        lf, lc, cmax = [None] * 6, None, 1.0
     rc = L.oracle_render(int(scene.num_worlds), _ptr(keep[0]), _ptr(keep[1]), _ptr(keep[2]),
                          A, *[_ptr(a) for a in af], _ptr(acls),
+                         NL, *[_ptr(a) for a in lf], _ptr(lc), cmax,
                          C, W, H, float(rig.fx), float(rig.fy), float(rig.cx), float(rig.cy),
                          float(rig.near), float(rig.far), _ptr(mount),
                          n, _ptr(view_ids), _ptr(out_cls), _ptr(out_depth), _ptr(out_flags),

@@ -56,6 +56,15 @@
  *              1 / float_from_bits(((bits(IZCAP) >> 3) - q) << 3 | 4).
  *  R9 boxes    corners (x + (a*c - b*s), y + (a*s + b*c), z0 or z0 + H) with
  *              a = +-L/2, b = +-W/2; 12 triangles (two per face).
+ *  R10 lights  (traffic-light disks visible only within a limited angular
+ *              range, Sec. 3.2 rendering features) a light with centre L,
+ *              horizontal normal (cf, sf) and cone cosine cos_max is drawn
+ *              iff, with d = C - L, h = cf*d.x + sf*d.y and
+ *              q = (d.x*d.x + d.y*d.y) + d.z*d.z:  h > 0 and
+ *              h*h >= (cos_max*cos_max)*q.
+ *  R11 disks   12 triangles (L, rim k, rim k+1 mod 12); rim k =
+ *              (L.x - a*sf, L.y + a*cf, L.z + b) with a = r*cos(30k deg),
+ *              b = r*sin(30k deg), the cosine and sine rounded to fp32.
  *
  * Arithmetic is IEEE fp32 with round-to-nearest and no contraction (this
  * file must be compiled with -ffp-contract=off and without -ffast-math);
@@ -304,6 +313,29 @@ static void box_corners(float x, float y, float z0, float c, float s, float L, f
     }
 }
 
+/* cos and sin of 30k degrees, k = 0..11, rounded to fp32 (R11) */
+static void sector_table(float cs[12], float sn[12])
+{
+    const float h = (float)(sqrt(3.0) / 2.0);
+    const float c[12] = {1.0f, h, 0.5f, 0.0f, -0.5f, -h, -1.0f, -h, -0.5f, 0.0f, 0.5f, h};
+    for (int k = 0; k < 12; ++k) {
+        cs[k] = c[k];
+        sn[k] = c[(k + 9) % 12];   /* sin(30k) = cos(30(k - 3)) */
+    }
+}
+
+/* R10: is the camera centre inside the light's visibility cone? */
+static int light_seen(const Cam* cam, float x, float y, float z, float cf, float sf, float cos_max)
+{
+    float dx = cam->cx_ - x, dy = cam->cy_ - y, dz = cam->cz_ - z;
+    float t1 = cf * dx, t2 = sf * dy;
+    float h = t1 + t2;
+    float xx = dx * dx, yy = dy * dy, zz = dz * dz;
+    float q = (xx + yy) + zz;
+    float m = cos_max * cos_max;
+    return h > 0.0f && h * h >= m * q;
+}
+
 static void init_params(Params* P, int W, int H, float fx, float fy, float cx, float cy, float nearp, float farp)
 {
     P->W = W; P->H = H; P->fx = fx; P->fy = fy; P->cx = cx; P->cy = cy;
@@ -336,6 +368,8 @@ int oracle_render(int num_worlds, const int64_t* tri_offsets, const float* verts
                   int agents_per_world, const float* ax, const float* ay, const float* az0,
                   const float* acos, const float* asin, const float* alen, const float* awid,
                   const float* ahgt, const uint8_t* acls,
+                  int lights_per_world, const float* lx, const float* ly, const float* lz,
+                  const float* lcf, const float* lsf, const float* lrad, const uint8_t* lcls, float cos_max,
                   int num_cams, int W, int H, float fx, float fy, float cx, float cy,
                   float nearp, float farp, const float* mount,
                   int64_t num_sel, const int64_t* view_ids,
@@ -344,6 +378,8 @@ int oracle_render(int num_worlds, const int64_t* tri_offsets, const float* verts
 {
     Params P;
     init_params(&P, W, H, fx, fy, cx, cy, nearp, farp);
+    float sec_c[12], sec_s[12];
+    sector_table(sec_c, sec_s);
     const int64_t npx = (int64_t)W * H;
     const int64_t per_world = (int64_t)agents_per_world * num_cams;
     const int64_t total_views = per_world * num_worlds;
@@ -393,6 +429,24 @@ int oracle_render(int num_worlds, const int64_t* tri_offsets, const float* verts
                         tri[3 * q + 2] = cor[BOX_TRIS[f][q]][2];
                     }
                     draw_triangle(&P, &cam, &F, tri, acls[h]);
+                }
+            }
+            for (int64_t l = 0; l < lights_per_world; ++l) {
+                int64_t h = w * lights_per_world + l;
+                if (!light_seen(&cam, lx[h], ly[h], lz[h], lcf[h], lsf[h], cos_max)) continue;
+                float rim[12][3];
+                for (int k = 0; k < 12; ++k) {
+                    float a = lrad[h] * sec_c[k], b = lrad[h] * sec_s[k];
+                    float as_ = a * lsf[h], ac = a * lcf[h];
+                    rim[k][0] = lx[h] - as_;
+                    rim[k][1] = ly[h] + ac;
+                    rim[k][2] = lz[h] + b;
+                }
+                for (int k = 0; k < 12; ++k) {
+                    int k1 = (k + 1) % 12;
+                    float tri[9] = {lx[h], ly[h], lz[h], rim[k][0], rim[k][1], rim[k][2],
+                                    rim[k1][0], rim[k1][1], rim[k1][2]};
+                    draw_triangle(&P, &cam, &F, tri, lcls[h]);
                 }
             }
             for (int64_t p = 0; p < npx; ++p) {

@@ -47,6 +47,8 @@ struct pictura_ctx_s {
     int tile = 0;
     int stats_on = 0;
     unsigned long long* stats = nullptr;   // [kNumStats] device counters
+    // traffic lights (caller-owned device arrays; lights.lights_per_world == 0: none)
+    pictura_lights lights{};
 };
 
 namespace {
@@ -329,6 +331,15 @@ pictura_status pictura_render_views(pictura_ctx c, const pictura_agents* ag, con
     P.out_cls = out_cls; P.out_depth = out_depth;
     P.cull = c->cull;
     P.vec_out = ((reinterpret_cast<uintptr_t>(out_cls) | reinterpret_cast<uintptr_t>(out_depth)) & 15u) == 0 ? 1 : 0;
+    if (c->lights.lights_per_world > 0) {
+        const pictura_lights& l = c->lights;
+        if (l.num_worlds != c->num_worlds)
+            return fail(c, PICTURA_EINVAL, "render_views: lights.num_worlds %d != scene num_worlds %d", l.num_worlds,
+                        c->num_worlds);
+        P.lx = l.x; P.ly = l.y; P.lz = l.z; P.lcf = l.cos_f; P.lsf = l.sin_f; P.lr = l.radius; P.lcls = l.cls;
+        P.L = l.lights_per_world;
+        P.lcos2 = l.cos_max * l.cos_max;
+    }
     DeviceGuard dg(c->device);
     if (c->stats_on) {
         hipError_t se = hipSuccess;
@@ -400,6 +411,26 @@ pictura_status pictura_bins_copy(pictura_ctx c, uint32_t* cell_start, float* cel
     }
     if (perm && c->T > 0 && (e = hipMemcpy(perm, c->perm, sizeof(uint32_t) * c->T, hipMemcpyDeviceToHost)) != hipSuccess)
         return hip_fail(c, e, "bins_copy");
+    return PICTURA_OK;
+}
+
+pictura_status pictura_set_lights(pictura_ctx c, const pictura_lights* l)
+{
+    if (!c) return PICTURA_EINVAL;
+    c->err.clear();
+    if (!l || l->lights_per_world == 0) {
+        c->lights = pictura_lights{};
+        return PICTURA_OK;
+    }
+    if (l->num_worlds < 1) return fail(c, PICTURA_EINVAL, "set_lights: num_worlds must be >= 1");
+    if (l->lights_per_world < 0 || l->lights_per_world > (1 << 20))
+        return fail(c, PICTURA_EINVAL, "set_lights: lights_per_world must be 0..2^20");
+    if (!l->x || !l->y || !l->z || !l->cos_f || !l->sin_f || !l->radius || !l->cls)
+        return fail(c, PICTURA_EINVAL, "set_lights: null array");
+    if (!(l->cos_max >= 0.0f && l->cos_max <= 1.0f)) return fail(c, PICTURA_EINVAL, "set_lights: cos_max must lie in [0, 1]");
+    if ((int64_t)l->num_worlds * l->lights_per_world > 0x7FFFFFFFll)
+        return fail(c, PICTURA_ERANGE, "set_lights: more than 2^31 - 1 lights");
+    c->lights = *l;
     return PICTURA_OK;
 }
 

@@ -63,6 +63,12 @@ struct RenderParams {
     int32_t vec_out;    // 1: output pointers are 16-byte aligned
     int32_t fast_decode; // 1: every decoded 1/z lies where the fast reciprocal is exact
     unsigned long long* stats;  // optional [kNumStats] work counters (null: off)
+    // traffic lights (R10, R11), SoA [num_worlds * L]; L == 0: none
+    const float* lx; const float* ly; const float* lz;
+    const float* lcf; const float* lsf; const float* lr;
+    const uint8_t* lcls;
+    int32_t L;
+    float lcos2;        // cos_max * cos_max (fp32)
 };
 
 struct AgentStepParams {

@@ -57,7 +57,8 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr uint32_t kClearKey = (0xFFFFFFu << 8) | 4u;
-constexpr uint32_t kBoxFlag = 0x80000000u;
+constexpr uint32_t kBoxFlag = 0x80000000u;     // queue entry: (agent << 4) | face of a box
+constexpr uint32_t kLightFlag = 0x40000000u;   // queue entry: (light << 4) | sector of a traffic light
 constexpr int kViewWaves = PICTURA_VIEW_WAVES;   // waves per view tile
 constexpr int kThreads = 64 * kViewWaves;
 constexpr int kWavesPerSimd = 4;  // register budget: four waves per SIMD (as many as the LDS admits)
@@ -299,6 +300,43 @@ __device__ __forceinline__ void load_box(const RenderParams& P, int64_t h, int f
     cls = (uint32_t)P.acls[h];
 }
 
+// R11: sector k of light h, the triangle (centre, rim k, rim k + 1).  Rim
+// vertex k is centre + r cos(30k deg) u + r sin(30k deg) up, with
+// u = (-sin_f, cos_f, 0) and the cosines and sines rounded to fp32.
+__device__ __forceinline__ void light_rim(float r, float cf, float sf, int k, float x, float y, float z, float* o)
+{
+    constexpr float kS3 = 0.866025403784438646763723f;   // sqrt(3) / 2
+    constexpr float kCos12[12] = {1.0f, kS3, 0.5f, 0.0f, -0.5f, -kS3, -1.0f, -kS3, -0.5f, 0.0f, 0.5f, kS3};
+    constexpr float kSin12[12] = {0.0f, 0.5f, kS3, 1.0f, kS3, 0.5f, 0.0f, -0.5f, -kS3, -1.0f, -kS3, -0.5f};
+    const float a = r * kCos12[k], b = r * kSin12[k];
+    const float as_ = a * sf, ac = a * cf;
+    o[0] = x - as_;
+    o[1] = y + ac;
+    o[2] = z + b;
+}
+
+__device__ __forceinline__ void load_light(const RenderParams& P, int64_t h, int k, float* tri, uint32_t& cls)
+{
+    const float x = P.lx[h], y = P.ly[h], z = P.lz[h], cf = P.lcf[h], sf = P.lsf[h], r = P.lr[h];
+    tri[0] = x;
+    tri[1] = y;
+    tri[2] = z;
+    light_rim(r, cf, sf, k, x, y, z, tri + 3);
+    light_rim(r, cf, sf, k == 11 ? 0 : k + 1, x, y, z, tri + 6);
+    cls = (uint32_t)P.lcls[h];
+}
+
+// R10: does the camera centre lie in light h's visibility cone?
+//   d = C - centre;  h = cf d.x + sf d.y;  visible iff h > 0 and h^2 >= cos_max^2 |d|^2
+__device__ __forceinline__ bool light_visible(const RenderParams& P, const Cam& cam, int64_t h)
+{
+    const float dx = cam.x - P.lx[h], dy = cam.y - P.ly[h], dz = cam.z - P.lz[h];
+    const float t1 = P.lcf[h] * dx, t2 = P.lsf[h] * dy;
+    const float hh = t1 + t2;
+    const float q = (dx * dx + dy * dy) + dz * dz;
+    return hh > 0.0f && hh * hh >= P.lcos2 * q;
+}
+
 __device__ __forceinline__ void load_static(const RenderParams& P, uint32_t t, float* tri, uint32_t& cls)
 {
     const float4 A = P.scene.triA[t];
@@ -309,10 +347,11 @@ __device__ __forceinline__ void load_static(const RenderParams& P, uint32_t t, f
     cls = __float_as_uint(C.y);
 }
 
-__device__ __forceinline__ void load_entry(const RenderParams& P, uint32_t e, int64_t abase_w, float* tri,
-                                           uint32_t& cls)
+__device__ __forceinline__ void load_entry(const RenderParams& P, uint32_t e, int64_t abase_w, int64_t lbase_w,
+                                           float* tri, uint32_t& cls)
 {
     if (e & kBoxFlag) load_box(P, abase_w + ((e & ~kBoxFlag) >> 4), (int)(e & 15u), tri, cls);
+    else if (e & kLightFlag) load_light(P, lbase_w + ((e & ~kLightFlag) >> 4), (int)(e & 15u), tri, cls);
     else load_static(P, e, tri, cls);
 }
 
@@ -635,15 +674,15 @@ __device__ __forceinline__ void raster_blocks(const RenderParams& P, Shared& S, 
 // ---------------------------------------------------------------------------
 
 __device__ __forceinline__ void exact_pass(const RenderParams& P, Shared& S, WaveLds& L, const Tile& T, const Cam& cam,
-                                           bool live, uint32_t entry, int64_t abase_w, float pxl, float pyl,
-                                           int loff4)
+                                           bool live, uint32_t entry, int64_t abase_w, int64_t lbase_w, float pxl,
+                                           float pyl, int loff4)
 {
     float tri[9] = {};
     uint32_t cls = 0;
     int np = 0;
     int X0 = 0, Y0 = 0, X1 = 0, Y1 = 0, X2 = 0, Y2 = 0, X3 = 0, Y3 = 0;
     if (live) {
-        load_entry(P, entry, abase_w, tri, cls);
+        load_entry(P, entry, abase_w, lbase_w, tri, cls);
         float xv[3], yv[3], zv[3];
 #pragma unroll
         for (int k = 0; k < 3; ++k) view_xform(cam, tri[3 * k], tri[3 * k + 1], tri[3 * k + 2], xv[k], yv[k], zv[k]);
@@ -978,6 +1017,7 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd) void render_views_kernel(c
     const float rrw = rw > 0 ? 1.0f / (float)rw : 0.0f;
     const float hc = 0.5f * cs + grid.margin;   // half extent of a cell rectangle widened by the margin
     const int64_t abase_w = (int64_t)w * P.A;
+    const int64_t lbase_w = (int64_t)w * P.L;
     if (tid == 0) { STAT(kStTiles, 1); STAT(kStCellsRect, nrect); }
     __syncthreads();
     TACC(kCycPrologue, t_kernel);
@@ -985,12 +1025,12 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd) void render_views_kernel(c
     // ---- per-wave pipeline: sources -> first pass -> queue -> exact pass ----
     // One loop with one inlined copy of the first and exact passes keeps the
     // whole kernel in the instruction cache.
-    enum { kStatic = 0, kBoxes = 1, kDone = 2 };
+    enum { kStatic = 0, kBoxes = 1, kLights = 2, kDone = 3 };
     int phase = kStatic;
     // wave w of the view takes the cells (and agents) whose index is w mod
     // kViewWaves; each wave exact-passes its own survivors
     int chunk = 0;                   // next 64-cell chunk of this wave
-    int achunk = 0;                  // next 64-agent chunk of this wave
+    int achunk = 0;                  // next 64-agent (then 64-light) chunk of this wave
     uint32_t total = 0, s0 = 0;      // candidate slots of the current chunk, next slot
     uint32_t my_start = 0, my_pre = 0;   // lane i: visible cell i (first triangle, exclusive prefix) or agent i
     int nvis = 0, cfirst = 0;
@@ -1051,7 +1091,7 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd) void render_views_kernel(c
             __builtin_amdgcn_wave_barrier();
         }
         while (phase == kBoxes && s0 >= total) {
-            if (achunk * 64 * kViewWaves >= P.A) { phase = kDone; break; }
+            if (achunk * 64 * kViewWaves >= P.A) { phase = kLights; achunk = 0; break; }
             const int ai = (achunk * 64 + lane) * kViewWaves + wid;
             ++achunk;
             bool vis = false;
@@ -1072,6 +1112,33 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd) void render_views_kernel(c
                 STAT(kStBoxesVis, 1);
                 STAT(kStBoxTris, 12);
             }
+            __builtin_amdgcn_wave_barrier();
+            my_start = lane < nvis ? L.u.agents[lane] : 0u;
+            total = 12u * (uint32_t)nvis;
+            s0 = 0;
+            __builtin_amdgcn_wave_barrier();
+        }
+        while (phase == kLights && s0 >= total) {
+            // traffic lights whose visibility cone holds the camera (R10)
+            if (achunk * 64 * kViewWaves >= P.L) { phase = kDone; break; }
+            const int li = (achunk * 64 + lane) * kViewWaves + wid;
+            ++achunk;
+            bool vis = false;
+            if (li < P.L) {
+                const int64_t h = lbase_w + li;
+                vis = light_visible(P, cam, h);
+                if (vis && cull) {
+                    // the disk lies within r of its centre; the margin covers the rounding of the rim vertices
+                    const float x = P.lx[h], y = P.ly[h], z = P.lz[h];
+                    const float R = P.lr[h] * 1.0009765625f + (fabsf(x) + fabsf(y) + fabsf(z)) * 9.5367431640625e-07f
+                                    + 0.0009765625f;
+                    vis = aabb_visible(P, T, F, cam, x - R, y - R, z - R, x + R, y + R, z + R);
+                }
+            }
+            const uint64_t m = __ballot(vis);
+            nvis = __popcll(m);
+            if (nvis == 0) continue;
+            if (vis) L.u.agents[mbcnt(m)] = (uint32_t)li;
             __builtin_amdgcn_wave_barrier();
             my_start = lane < nvis ? L.u.agents[lane] : 0u;
             total = 12u * (uint32_t)nvis;
@@ -1114,18 +1181,22 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd) void render_views_kernel(c
             }
             s0 += 128;
             TACC(kCycFirst, t_first);
-        } else if (phase == kBoxes) {
-            // first pass over box slots s0 .. s0 + 63
+        } else if (phase != kDone) {
+            // first pass over box (or light) slots s0 .. s0 + 63
             TSTART(t_first);
             const uint32_t slot = s0 + (uint32_t)lane;
             float tri[9] = {};
             uint32_t cls = 0;
-            // slot = 12 * (visible agent) + face; the multiply-shift divides exactly for slot < 831
+            // slot = 12 * (visible box or light) + triangle; the multiply-shift divides exactly for slot < 831
             const uint32_t vi = (slot * 43691u) >> 19;
             const uint32_t face = slot - 12u * vi;
             const uint32_t ai = (uint32_t)__shfl((int)my_start, (int)min(vi, 63u));
-            const uint32_t entry = kBoxFlag | (ai << 4) | face;
-            if (slot < total) load_box(P, abase_w + ai, (int)face, tri, cls);
+            const bool boxes = phase == kBoxes;
+            const uint32_t entry = (boxes ? kBoxFlag : kLightFlag) | (ai << 4) | face;
+            if (slot < total) {
+                if (boxes) load_box(P, abase_w + ai, (int)face, tri, cls);
+                else load_light(P, lbase_w + ai, (int)face, tri, cls);
+            }
             const bool surv = slot < total && first_pass(P, T, cam, tri, cull);
             if (surv) STAT(kStSurv, 1);
             STAT1(kStChunks, 1);
@@ -1142,7 +1213,7 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd) void render_views_kernel(c
             __builtin_amdgcn_wave_barrier();
             STAT1(kStExact, 1);
             TSTART(t_ex);
-            exact_pass(P, S, L, T, cam, live, entry, abase_w, pxl, pyl, loff4);
+            exact_pass(P, S, L, T, cam, live, entry, abase_w, lbase_w, pxl, pyl, loff4);
             TACC(kCycExact, t_ex);
         }
         if (phase == kDone && nq == 0) break;

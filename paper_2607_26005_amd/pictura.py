@@ -51,6 +51,12 @@ class _Rig(ctypes.Structure):
                 ("mount", (ctypes.c_float * 5) * MAX_CAMS)]
 
 
+class _Lights(ctypes.Structure):
+    _fields_ = [("num_worlds", ctypes.c_int32), ("lights_per_world", ctypes.c_int32)] + \
+               [(n, ctypes.c_void_p) for n in ("x", "y", "z", "cos_f", "sin_f", "radius", "cls")] + \
+               [("cos_max", ctypes.c_float)]
+
+
 class _AgentState(ctypes.Structure):
     _fields_ = [("count", ctypes.c_int32)] + \
                [(n, ctypes.c_void_p) for n in ("x", "y", "psi", "speed", "cos_h", "sin_h", "length")]
@@ -79,12 +85,15 @@ _lib.pictura_set_option.argtypes = [_P, ctypes.c_int32, ctypes.c_int32]
 _lib.pictura_set_option.restype = ctypes.c_int32
 _lib.pictura_stats_copy.argtypes = [_P, _P, ctypes.c_int32, ctypes.c_int32]
 _lib.pictura_stats_copy.restype = ctypes.c_int32
+_lib.pictura_set_lights.argtypes = [_P, ctypes.POINTER(_Lights)]
+_lib.pictura_set_lights.restype = ctypes.c_int32
 _lib.pictura_selftest_rcp.argtypes = [_P, ctypes.c_uint32, ctypes.c_uint32, _P]
 _lib.pictura_selftest_rcp.restype = ctypes.c_int32
 
 EXPORTED = ["pictura_create", "pictura_destroy", "pictura_last_error", "pictura_scene_upload",
             "pictura_bin_scene", "pictura_render_views", "pictura_agents_step", "pictura_bins_info",
-            "pictura_bins_copy", "pictura_set_option", "pictura_stats_copy", "pictura_selftest_rcp"]
+            "pictura_bins_copy", "pictura_set_option", "pictura_stats_copy", "pictura_selftest_rcp",
+            "pictura_set_lights"]
 
 STAT_NAMES = ["view_tiles", "cells_in_rect", "cells_prefiltered", "cells_visible", "cand_tris", "boxes_visible",
               "box_tris", "first_pass_survivors", "exact_batches", "clipped", "raster_tris", "lane_tris",
@@ -180,6 +189,18 @@ def pictura_agents_step(ctx, state, steer, accel, dt: float = 0.1, vmax: float =
                                          _stream(stream)))
 
 
+def pictura_set_lights(ctx, lights):
+    """lights: DeviceLights (torch CUDA tensors) or None (detach).  The context
+    keeps the pointers: the tensors must stay alive while it renders."""
+    if lights is None:
+        _check(ctx, _lib.pictura_set_lights(ctx, None))
+        return
+    l = _Lights(int(lights.num_worlds), int(lights.lights_per_world),
+                *[_ptr(getattr(lights, n)) for n in ("x", "y", "z", "cos_f", "sin_f", "radius", "cls")],
+                float(lights.cos_max))
+    _check(ctx, _lib.pictura_set_lights(ctx, ctypes.byref(l)))
+
+
 def pictura_bins_info(ctx, num_worlds: int):
     dims = np.empty((num_worlds, 2), np.int32)
     base = np.empty(num_worlds + 1, np.int64)
@@ -240,6 +261,28 @@ class DeviceAgents:
                             f(agents.cls, torch.uint8), f(agents.psi), f(agents.speed))
 
 
+@dataclasses.dataclass
+class DeviceLights:
+    num_worlds: int
+    lights_per_world: int
+    x: "object"
+    y: "object"
+    z: "object"
+    cos_f: "object"
+    sin_f: "object"
+    radius: "object"
+    cls: "object"
+    cos_max: float
+
+    @staticmethod
+    def from_host(lights, device="cuda"):
+        import torch
+        f = lambda a, dt=torch.float32: torch.as_tensor(np.ascontiguousarray(a), dtype=dt).to(device)
+        return DeviceLights(int(lights.num_worlds), int(lights.lights_per_world),
+                            *[f(getattr(lights, n)) for n in ("x", "y", "z", "cos_f", "sin_f", "radius")],
+                            f(lights.cls, torch.uint8), float(lights.cos_max))
+
+
 class Renderer:
     """Owns a library context, its scene and bins."""
 
@@ -247,6 +290,7 @@ class Renderer:
         self.ctx = pictura_create(device)
         self.num_worlds = 0
         self.num_tris = 0
+        self.lights = None
 
     def close(self):
         if self.ctx:
@@ -281,6 +325,10 @@ class Renderer:
 
     def set_option(self, option, value):
         pictura_set_option(self.ctx, option, value)
+
+    def set_lights(self, lights: Optional[DeviceLights]):
+        pictura_set_lights(self.ctx, lights)
+        self.lights = lights   # the context keeps the pointers: hold the tensors
 
     def bins(self):
         dims, base, total = pictura_bins_info(self.ctx, self.num_worlds)

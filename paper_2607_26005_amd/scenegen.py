@@ -20,6 +20,12 @@ workloads of the same kind stand in for them:
                every step by the kinematic bicycle update     (262,144 views)
   5 large      128 worlds 4x4 km of cubic-Bezier roads tessellated at 0.5 m
                (~500k triangles per world), 128x128 views, far 200 m
+  6 paper rig  64 worlds of the small-batch town seen through the paper's
+               four-camera rig at 96x54 (2,048 egos: one render chunk)
+  7 town       the paper's other rendering features on the small-batch town:
+               building walls along the blocks, parked cars, and traffic
+               lights (disks with a limited visibility cone) at every
+               intersection, one facing each approach; paper rig, 96x54
 
 Coordinates are metres, world-centred, z up.  Vertical layers are lifted so
 that coplanar classes never tie: ground z=0, road top z=0.02, markings
@@ -38,7 +44,9 @@ import numpy as np
 
 # Semantic class IDs.  Sky is never a triangle: it is the background class.
 GROUND, ROAD, MARKING, VEHICLE, SKY, CURB, PEDESTRIAN = 0, 1, 2, 3, 4, 5, 6
-CLASS_NAMES = ["ground", "road", "marking", "vehicle", "sky", "curb", "pedestrian"]
+WALL, LIGHT_RED, LIGHT_AMBER, LIGHT_GREEN = 7, 8, 9, 10
+CLASS_NAMES = ["ground", "road", "marking", "vehicle", "sky", "curb", "pedestrian", "wall", "light_red",
+               "light_amber", "light_green"]
 
 Z_GROUND = 0.0
 Z_ROAD = 0.02
@@ -107,6 +115,23 @@ class Agents:
 
 
 @dataclasses.dataclass
+class Lights:
+    """Traffic lights, index = world * lights_per_world + l: disks of `radius`
+    centred at (x, y, z) with horizontal normal (cos_f, sin_f), seen only from
+    within the cone of half-angle acos(cos_max) around that normal."""
+    num_worlds: int
+    lights_per_world: int
+    x: np.ndarray
+    y: np.ndarray
+    z: np.ndarray
+    cos_f: np.ndarray
+    sin_f: np.ndarray
+    radius: np.ndarray
+    cls: np.ndarray          # uint8: the signal state's class
+    cos_max: float
+
+
+@dataclasses.dataclass
 class Rig:
     """Pinhole cameras mounted on every agent (yaw-only mounts)."""
     width: int
@@ -134,6 +159,7 @@ class Workload:
     rig: Rig
     cell_size: float
     world_size: float
+    lights: Optional[Lights] = None
 
     @property
     def num_views(self) -> int:
@@ -331,7 +357,7 @@ def _place_on_straight_roads(rng, roads: List[StraightRoad], size, n, min_gap, j
 
 
 def _grid_world(rng, size, tile, n_roads_axis, lane_choices, seg, curbs, n_agents,
-                min_gap, jitter, ped_frac, fixed_centres=None):
+                min_gap, jitter, ped_frac, fixed_centres=None, return_roads=False):
     tris, clss = [ground_tiles(size, tile)], []
     clss.append(np.full(len(tris[0]), GROUND, np.uint8))
     roads: List[StraightRoad] = []
@@ -350,7 +376,90 @@ def _grid_world(rng, size, tile, n_roads_axis, lane_choices, seg, curbs, n_agent
         tris += t
         clss += c
     ag = _place_on_straight_roads(rng, roads, size, n_agents, min_gap, jitter, ped_frac)
+    if return_roads:
+        return np.concatenate(tris), np.concatenate(clss), ag, roads
     return np.concatenate(tris), np.concatenate(clss), ag
+
+
+def _aabox_tris(x0, y0, z0, x1, y1, z1):
+    """Axis-aligned boxes [n] -> 12 triangles each (scene input: parked cars)."""
+    c = [_xyz(np.where(n & 1, x1, x0), np.where(n & 2, y1, y0), np.where(n & 4, z1, z0)) for n in range(8)]
+    faces = ((0, 1, 3, 2), (4, 5, 7, 6), (0, 2, 6, 4), (1, 3, 7, 5), (0, 1, 5, 4), (2, 3, 7, 6))
+    return np.concatenate([_quads(c[a], c[b], c[d], c[e]) for a, b, d, e in faces])
+
+
+LIGHT_Z, LIGHT_R, LIGHT_COS_MAX = 5.0, 0.3, 0.5   # head height, disk radius, cone cos(60 deg)
+
+
+def _town_world(rng, size, n_agents):
+    """Small-batch town plus walls, parked cars and traffic lights."""
+    tris, clss, ag, roads = _grid_world(rng, size, 25.0, 6, [2, 3, 4], 2.5, True, n_agents, 8.0, 0.1, 0.0,
+                                        return_roads=True)
+    extra_t, extra_c = [], []
+    lx, ly, lcf, lsf, lcls = [], [], [], [], []
+    for r in roads:
+        others = [o for o in roads if o.axis != r.axis]
+        hw = r.width / 2
+        # blocks between consecutive crossings
+        cuts = sorted([-size / 2] + [o.c for o in others] + [size / 2])
+        for a, b in zip(cuts[:-1], cuts[1:]):
+            wa = a + (0 if a == -size / 2 else max(o.width for o in others if o.c == a) / 2 + 6.0)
+            wb = b - (0 if b == size / 2 else max(o.width for o in others if o.c == b) / 2 + 6.0)
+            if wb - wa < 20.0:
+                continue
+            for side in (-1.0, 1.0):
+                # building walls 4 m behind the curb: facades of 12..40 m, 6..18 m tall, with gaps
+                u = wa
+                while u < wb - 8.0:
+                    ln = min(rng.uniform(12.0, 40.0), wb - u)
+                    h = rng.uniform(6.0, 18.0)
+                    v = side * (hw + 4.0)
+                    q = _quads(_map_uv(r, np.array([u]), v, Z_GROUND), _map_uv(r, np.array([u + ln]), v, Z_GROUND),
+                               _map_uv(r, np.array([u + ln]), v, h), _map_uv(r, np.array([u]), v, h))
+                    extra_t.append(q)
+                    extra_c.append(np.full(len(q), WALL, np.uint8))
+                    u += ln + rng.uniform(2.0, 10.0)
+                # parked cars on the strip between curb and wall, 30 % of 7 m slots
+                slots = wa + 3.0 + 7.0 * np.arange(int((wb - wa - 6.0) // 7.0))
+                slots = slots[rng.random(len(slots)) < 0.3]
+                if len(slots):
+                    v0, v1 = side * (hw + 0.9), side * (hw + 2.8)
+                    p0 = _map_uv(r, slots - 2.25, min(v0, v1), Z_GROUND)
+                    p1 = _map_uv(r, slots + 2.25, max(v0, v1), Z_GROUND + 1.5)
+                    lo, hi = np.minimum(p0, p1), np.maximum(p0, p1)
+                    bx = _aabox_tris(lo[:, 0], lo[:, 1], lo[:, 2], hi[:, 0], hi[:, 1], hi[:, 2])
+                    extra_t.append(bx)
+                    extra_c.append(np.full(len(bx), VEHICLE, np.uint8))
+    # traffic lights: at every crossing one head per approach, on the far side of the
+    # junction, facing the traffic that approaches it; the two axes show opposite states
+    xr = [r for r in roads if r.axis == 0]
+    yr = [r for r in roads if r.axis == 1]
+    for ra in xr:
+        for rb in yr:
+            cx_, cy_ = rb.c, ra.c
+            sx = LIGHT_GREEN if rng.random() < 0.5 else LIGHT_RED
+            sy = LIGHT_RED if sx == LIGHT_GREEN else LIGHT_GREEN
+            if rng.random() < 0.15:
+                sx = LIGHT_AMBER
+            # (approach direction (dx, dy), state): traffic driving +x meets a head beyond the crossing at +x
+            for (dx, dy, st, hw_cross, hw_own) in ((1, 0, sx, rb.width / 2, ra.width / 2),
+                                                   (-1, 0, sx, rb.width / 2, ra.width / 2),
+                                                   (0, 1, sy, ra.width / 2, rb.width / 2),
+                                                   (0, -1, sy, ra.width / 2, rb.width / 2)):
+                far = hw_cross + 1.0
+                lat = -hw_own - 1.0          # right-hand traffic: the head stands on the right-hand side
+                px = cx_ + dx * far + dy * (-lat)
+                py = cy_ + dy * far + dx * lat
+                lx.append(px); ly.append(py)
+                lcf.append(float(-dx)); lsf.append(float(-dy))
+                lcls.append(st)
+    if extra_t:
+        tris = np.concatenate([tris] + extra_t)
+        clss = np.concatenate([clss] + extra_c)
+    n = len(lx)
+    lights = dict(x=np.asarray(lx), y=np.asarray(ly), z=np.full(n, LIGHT_Z), cos_f=np.asarray(lcf),
+                  sin_f=np.asarray(lsf), radius=np.full(n, LIGHT_R), cls=np.asarray(lcls, np.uint8))
+    return tris, clss, ag, lights
 
 
 def _bezier_world(rng, size, tile, target_tris, n_agents, jitter):
@@ -408,6 +517,8 @@ CONFIGS = {
     5: dict(name="highres_large_scene", seed=4, worlds=128, size=4000.0, agents=64, cams=4, res=128, far=200.0, cell=32.0),
     # the paper's own rig and batch: 2048 egos x 4 views at 96x54 (App. A.2, Tab. camera_rig; Tab. render_mem)
     6: dict(name="paper_rig", seed=5, worlds=64, size=1000.0, agents=32, cams="paper", res=(96, 54), far=100.0, cell=16.0),
+    # the paper's other rendering features (Sec. 3.2, Fig. qualitative): walls, parked cars, traffic lights
+    7: dict(name="town_features", seed=6, worlds=64, size=1000.0, agents=32, cams="paper", res=(96, 54), far=100.0, cell=16.0),
 }
 
 
@@ -463,18 +574,23 @@ def _build_world(cfg_id: int, cfg: dict, w: int):
         return _grid_world(rng, size, 25.0, 6, [2, 3, 4], 2.5, True, cfg["agents"], 0.0, 0.1, 0.2)
     if cfg_id == 5:
         return _bezier_world(rng, size, 50.0, 500_000, cfg["agents"], 0.1)
+    if cfg_id == 7:
+        return _town_world(rng, size, cfg["agents"])
     raise ValueError(cfg_id)
 
 
 def make_config(cfg_id: int, num_worlds: Optional[int] = None, init_speed_seed: bool = True) -> Workload:
-    """Build workload `cfg_id` (1..6), optionally only its first `num_worlds` worlds."""
+    """Build workload `cfg_id` (1..7), optionally only its first `num_worlds` worlds."""
     cfg = CONFIGS[cfg_id]
     nw = cfg["worlds"] if num_worlds is None else int(num_worlds)
     A = cfg["agents"]
     verts, clss, offs = [], [], [0]
-    ag_parts = []
+    ag_parts, light_parts = [], []
     for w in range(nw):
-        t, c, ag = _build_world(cfg_id, cfg, w)
+        built = _build_world(cfg_id, cfg, w)
+        t, c, ag = built[:3]
+        if len(built) > 3:
+            light_parts.append(built[3])
         verts.append(t.reshape(-1, 9))
         clss.append(c)
         offs.append(offs[-1] + len(t))
@@ -498,8 +614,16 @@ def make_config(cfg_id: int, num_worlds: Optional[int] = None, init_speed_seed: 
                     cls=np.ascontiguousarray(np.concatenate([a.cls for a in ag_parts])),
                     psi=cat("psi"), speed=speed)
     rig = make_paper_rig(cfg["far"]) if cfg["cams"] == "paper" else make_rig(cfg["cams"], cfg["res"], cfg["far"])
+    lights = None
+    if light_parts:
+        nl = len(light_parts[0]["x"])
+        assert all(len(lp["x"]) == nl for lp in light_parts)
+        lcat = lambda f, dt=np.float32: np.ascontiguousarray(np.concatenate([lp[f] for lp in light_parts]).astype(dt))
+        lights = Lights(num_worlds=nw, lights_per_world=nl, x=lcat("x"), y=lcat("y"), z=lcat("z"),
+                        cos_f=lcat("cos_f"), sin_f=lcat("sin_f"), radius=lcat("radius"),
+                        cls=lcat("cls", np.uint8), cos_max=LIGHT_COS_MAX)
     return Workload(name=cfg["name"], config=cfg_id, seed=cfg["seed"], scene=scene, agents=agents,
-                    rig=rig, cell_size=cfg["cell"], world_size=size)
+                    rig=rig, cell_size=cfg["cell"], world_size=size, lights=lights)
 
 
 def controls(num_agents: int, steps: int, seed: int = 3):
