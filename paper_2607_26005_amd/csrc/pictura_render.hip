@@ -1049,6 +1049,8 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd) void render_views_kernel(c
                 int ix = r - iy * rw;
                 if (ix < 0) { --iy; ix += rw; }
                 if (ix >= rw) { ++iy; ix -= rw; }
+                // an even row width would give each wave whole columns: alternate per row instead
+                if ((rw & 1) == 0) ix ^= (iy & 1);
                 bool pre = true;
                 if (cull) {
                     const float ccx = (grid.ox + ((float)(ix0 + ix) + 0.5f) * cs) - cam.x;
