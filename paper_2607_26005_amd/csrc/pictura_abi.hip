@@ -310,6 +310,9 @@ pictura_status pictura_render_views(pictura_ctx c, const pictura_agents* ag, con
     P.rfx = 1.0f / P.fx; P.rfy = 1.0f / P.fy;
     P.izfar = izfar; P.izcap = izcap; P.qbase = f2u(izcap) >> 3;
     P.cabs = std::fabs(P.cx) > std::fabs(P.cy) ? std::fabs(P.cx) : std::fabs(P.cy);
+    P.near_cull = P.nearp * 1.00390625f;
+    P.near_off = -P.nearp * 0.99609375f;
+    P.far_off = P.farp * 1.015625f;
     // pixel-centre offsets: with c a multiple of 2^-8 below 2^14 in magnitude,
     // 0.5 - c and i + (0.5 - c) (i < 4096) are exact in fp32
     P.hx = 0.5f - P.cx;

@@ -49,6 +49,9 @@ struct RenderParams {
     // derived constants
     float fx256, fy256, cx256, cy256, rfx, rfy, izfar, izcap;
     float cabs;         // max(|cx|, |cy|)
+    float near_cull;    // near * (1 + 2^-8): boxes at least this far in front skip the near-plane case
+    float near_off;     // -near * (1 - 2^-8): offset of the near frustum plane (with margin)
+    float far_off;      // far * (1 + 2^-6): offset of the far frustum plane (with margin)
     float hx, hy;       // 0.5 - cx, 0.5 - cy
     int32_t pix_exact;  // 1: (i + 0.5) - cx equals i + hx exactly for every pixel index (same for y)
     uint32_t qbase;

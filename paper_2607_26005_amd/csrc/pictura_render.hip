@@ -116,7 +116,11 @@ struct alignas(16) Shared {
     uint32_t fb[kFbCap];
     WaveLds wv[kViewWaves];
     uint32_t stat[kNumStats];
+    uint32_t ctl[4];   // record ring: reserved, claimed; wave 0 and wave 1 finished producing
 };
+
+enum { kRecTail = 0, kRecHead = 1, kDone0 = 2 };
+constexpr uint32_t kRecReady = 0x5EC0DE01u;   // differs from the clear key the padding starts with
 
 enum Stat {
     kStTiles = 0, kStCellsRect, kStCellsPre, kStCellsVis, kStCand, kStBoxesVis, kStBoxTris, kStSurv,
@@ -161,6 +165,18 @@ __device__ __forceinline__ float recip_rn(float x)
 __device__ __forceinline__ uint32_t mbcnt(uint64_t m)
 {
     return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32), __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
+}
+
+__device__ __forceinline__ uint32_t readfirst(uint32_t v) { return (uint32_t)__builtin_amdgcn_readfirstlane((int)v); }
+
+__device__ __forceinline__ uint32_t lds_load_acquire(const uint32_t* p)
+{
+    return __hip_atomic_load(p, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_WORKGROUP);
+}
+
+__device__ __forceinline__ void lds_store_release(uint32_t* p, uint32_t v)
+{
+    __hip_atomic_store(p, v, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_WORKGROUP);
 }
 
 __device__ __forceinline__ uint32_t readlane(uint32_t v, int l)
@@ -819,6 +835,29 @@ __device__ __forceinline__ void exact_pass(const RenderParams& P, Shared& S, Wav
             if (!e32) STAT(kStRecWide, 1);
         }
         const bool fast = P.pix_exact && (T.w & 7) == 0 && (T.h & 7) == 0;
+        // hand int32-form records to the view's record ring (both waves drain it at the end)
+        const uint64_t md = __ballot(big && e32);
+        const uint32_t cap = (uint32_t)T.h >> 2;
+        if (md != 0 && cap != 0) {
+            const int l0 = __builtin_ctzll(md);
+            uint32_t base = 0;
+            if (lane_id() == l0) base = atomicAdd(&S.ctl[kRecTail], (uint32_t)__popcll(md));
+            base = readlane(base, l0);
+            const uint32_t slot = base + mbcnt(md);
+            const bool put = big && e32 && slot < cap;
+            if (put) {
+                u32x4* g = (u32x4*)&S.fb[4 * (int)slot * T.pitch + T.pitch - 4];
+                const int rs = T.pitch >> 2;   // 16-byte units per framebuffer row
+                g[0] = u32x4{rv[0], rv[1], rv[2], rv[3]};
+                g[rs] = u32x4{rv[4], rv[5], rv[6], rv[7]};
+                g[2 * rs] = u32x4{rv[8], __float_as_uint(pa), __float_as_uint(pb), __float_as_uint(pc)};
+                uint32_t* w3 = &S.fb[(4 * (int)slot + 3) * T.pitch + T.pitch - 4];
+                w3[0] = rbox;
+                w3[1] = rj1;
+                lds_store_release(&w3[2], kRecReady);
+            }
+            m &= ~__ballot(put);
+        }
         TSTART(t_rec);
         while (m) {
             const int l = __builtin_ctzll(m);
@@ -898,7 +937,7 @@ __device__ __forceinline__ bool aabb_visible(const RenderParams& P, const Tile& 
         xmn = fminf(xmn, px); xmx = fmaxf(xmx, px);
         mag = fmaxf(mag, fabsf(px));
     }
-    if (!(zmn >= P.nearp * 1.00390625f)) return true;   // crosses or nearly touches the near plane
+    if (!(zmn >= P.near_cull)) return true;   // crosses or nearly touches the near plane
     const float r0 = __builtin_amdgcn_rcpf(zmn), r1 = __builtin_amdgcn_rcpf(zmx);
     const float ylo = loz - cam.z, yhi = hiz - cam.z;
     const float y0 = P.cy - P.fy * (yhi * r0), y1 = P.cy - P.fy * (yhi * r1);
@@ -979,6 +1018,7 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd) void render_views_kernel(c
     const float pxl = (float)(lane & 7) + P.hx, pyl = (float)(lane >> 3) + P.hy;
     const int loff4 = ((lane >> 3) * T.pitch + (lane & 7)) * 4;
     if (P.stats && tid < kNumStats) S.stat[tid] = 0;
+    if (tid < 4) S.ctl[tid] = 0;
 
     // world-space frustum planes of the tile: four side planes through the
     // camera centre, near and far with margins
@@ -989,8 +1029,8 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd) void render_views_kernel(c
         F.n[1][0] = T.kr * cc - P.fx * sc; F.n[1][1] = T.kr * sc + P.fx * cc; F.n[1][2] = 0.0f; F.o[1] = 0.0f;
         F.n[2][0] = T.kt * cc; F.n[2][1] = T.kt * sc; F.n[2][2] = -P.fy; F.o[2] = 0.0f;
         F.n[3][0] = -T.kb * cc; F.n[3][1] = -T.kb * sc; F.n[3][2] = P.fy; F.o[3] = 0.0f;
-        F.n[4][0] = cc; F.n[4][1] = sc; F.n[4][2] = 0.0f; F.o[4] = -P.nearp * 0.99609375f;
-        F.n[5][0] = -cc; F.n[5][1] = -sc; F.n[5][2] = 0.0f; F.o[5] = P.farp * 1.015625f;
+        F.n[4][0] = cc; F.n[4][1] = sc; F.n[4][2] = 0.0f; F.o[4] = P.near_off;
+        F.n[5][0] = -cc; F.n[5][1] = -sc; F.n[5][2] = 0.0f; F.o[5] = P.far_off;
     }
 
     const WorldGrid grid = P.scene.grids[w];
@@ -998,7 +1038,7 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd) void render_views_kernel(c
     // rectangle of cells covering the tile frustum's xy footprint up to far
     int ix0 = 0, iy0 = 0, ix1 = grid.nx - 1, iy1 = grid.ny - 1;
     if (cull) {
-        const float fz = P.farp * 1.015625f;
+        const float fz = P.far_off;
         const float tl = T.kl / P.fx, tr = T.kr / P.fx;
         const float ax_ = cam.cc + tl * cam.sc, ay_ = cam.sc - tl * cam.cc;   // f + tl r
         const float bx_ = cam.cc + tr * cam.sc, by_ = cam.sc - tr * cam.cc;   // f + tr r
@@ -1219,6 +1259,55 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd) void render_views_kernel(c
             TACC(kCycExact, t_ex);
         }
         if (phase == kDone && nq == 0) break;
+    }
+
+    // ---- record ring: this wave produces no more records; rasterize the ring's
+    // records, the other wave's too, until both waves are done and it is empty
+    {
+        static_assert(kViewWaves == 2, "two done flags");
+        if (lane == 0) lds_store_release(&S.ctl[kDone0 + wid], 1u);
+        const uint32_t cap = (uint32_t)T.h >> 2;
+        const bool fast = P.pix_exact && (T.w & 7) == 0 && (T.h & 7) == 0;
+        TSTART(t_ring);
+        // Every wait below ends: a claimed slot was reserved by a wave that
+        // publishes it right after reserving it, and each wave sets its done
+        // flag after its last reservation.  The sleep counts are bounded all
+        // the same (about a second), so a broken invariant shows as a wrong
+        // image, never as a hung wave.
+        uint32_t naps = 0;
+        for (; naps < (1u << 22); ) {
+            // the done flags first: once both are set, the reserved count is final
+            const bool fin = readfirst(lds_load_acquire(&S.ctl[kDone0])) != 0 &&
+                             readfirst(lds_load_acquire(&S.ctl[kDone0 + 1])) != 0;
+            const uint32_t t = min(readfirst(lds_load_acquire(&S.ctl[kRecTail])), cap);
+            const uint32_t h = readfirst(lds_load_acquire(&S.ctl[kRecHead]));
+            if (h < t) {
+                uint32_t got = 0;
+                if (lane == 0) got = atomicCAS(&S.ctl[kRecHead], h, h + 1u);
+                if (readlane(got, 0) != h) continue;
+                // slot h is reserved; wait until its producer has published it
+                const uint32_t* w3 = &S.fb[(4 * (int)h + 3) * T.pitch + T.pitch - 4];
+                while (readfirst(lds_load_acquire(&w3[2])) != kRecReady && ++naps < (1u << 22))
+                    __builtin_amdgcn_s_sleep(1);
+                if (naps >= (1u << 22)) break;   // never published (cannot happen): skip, do not read it
+                const u32x4* g = (const u32x4*)&S.fb[4 * (int)h * T.pitch + T.pitch - 4];
+                const int rs = T.pitch >> 2;
+                const u32x4 g0 = g[0], g1 = g[rs], g2 = g[2 * rs];
+                uint32_t uw[9] = {readfirst(g0.x), readfirst(g0.y), readfirst(g0.z), readfirst(g0.w),
+                                  readfirst(g1.x), readfirst(g1.y), readfirst(g1.z), readfirst(g1.w),
+                                  readfirst(g2.x)};
+                const float rpa = __uint_as_float(readfirst(g2.y)), rpb = __uint_as_float(readfirst(g2.z));
+                const float rpc = __uint_as_float(readfirst(g2.w));
+                const uint32_t rb = readfirst(w3[0]), rj = readfirst(w3[1]);
+                if (fast) raster_blocks<true, true>(P, S, T, uw, rpa, rpb, rpc, rb, rj, pxl, pyl, loff4);
+                else raster_blocks<true, false>(P, S, T, uw, rpa, rpb, rpc, rb, rj, pxl, pyl, loff4);
+                continue;
+            }
+            if (fin) break;
+            ++naps;
+            __builtin_amdgcn_s_sleep(2);
+        }
+        TACC(kCycRecords, t_ring);
     }
     __syncthreads();
 
