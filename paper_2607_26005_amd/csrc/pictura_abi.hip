@@ -64,6 +64,15 @@ pictura_status fail(pictura_ctx c, pictura_status st, const char* fmt, ...)
     return st;
 }
 
+Div31 make_div31(uint32_t d)
+{
+    if (d <= 1) return Div31{0u, 0u};
+    uint32_t l = 0;
+    while ((1ull << l) < d) ++l;
+    const uint64_t m = ((1ull << (31 + l)) / d) + 1ull;   // < 2^32 for d >= 2
+    return Div31{(uint32_t)m, l - 1};
+}
+
 pictura_status hip_fail(pictura_ctx c, hipError_t e, const char* what)
 {
     if (e == hipErrorOutOfMemory || e == hipErrorMemoryAllocation)
@@ -331,6 +340,10 @@ pictura_status pictura_render_views(pictura_ctx c, const pictura_agents* ag, con
     P.num_views = V;
     P.num_blocks = V * P.tiles_x * P.tiles_y;
     if (P.num_blocks > 0x7FFFFFFFll) return fail(c, PICTURA_ERANGE, "render_views: too many view tiles in one call");
+    P.div_tiles = make_div31((uint32_t)(P.tiles_x * P.tiles_y));
+    P.div_cams = make_div31((uint32_t)P.C);
+    P.div_agents = make_div31((uint32_t)P.A);
+    P.rcs = 1.0f / c->cell_size;
     P.out_cls = out_cls; P.out_depth = out_depth;
     P.cull = c->cull;
     P.vec_out = ((reinterpret_cast<uintptr_t>(out_cls) | reinterpret_cast<uintptr_t>(out_depth)) & 15u) == 0 ? 1 : 0;

@@ -34,6 +34,15 @@ struct SceneDev {
     int32_t num_worlds;
 };
 
+// n / d for 0 <= n < 2^31 without a division: with l = ceil(log2 d) and
+// m = floor(2^(31 + l) / d) + 1 (which fits 32 bits), n / d equals
+// umulhi(n, m) >> (l - 1) (Granlund and Montgomery, "Division by invariant
+// integers using multiplication", 1994).  m == 0 encodes d == 1.
+struct Div31 {
+    uint32_t m;
+    uint32_t s;
+};
+
 struct RenderParams {
     SceneDev scene;
     // agents (SoA)
@@ -59,6 +68,8 @@ struct RenderParams {
     int32_t tile_w, tile_h, tiles_x, tiles_y;
     int64_t num_views;
     int64_t num_blocks;
+    Div31 div_tiles, div_cams, div_agents;   // by tiles_x * tiles_y, C and A
+    float rcs;          // 1 / cell size (rounded; used only with a one-cell margin)
     // outputs
     uint8_t* out_cls;
     float* out_depth;

@@ -551,11 +551,12 @@ __device__ __forceinline__ void raster_packed(const RenderParams& P, Shared& S, 
         const uint32_t bits = min(__float_as_uint(iz), __float_as_uint(P.izcap));
         const uint32_t key = ((P.qbase - (bits >> 3)) << 8) | (g >> 24);
         // p in range keeps the address inside the tile whatever the owner
-        // search found; other lanes take word 0 and the key 0xFFFFFFFF, which
-        // changes nothing, so the LDS minimum needs no branch
+        // search found; other lanes take word `lane` (distinct banks) and the
+        // key 0xFFFFFFFF, which changes nothing, so the LDS minimum needs no
+        // branch
         const bool inr = (slot < n) & (p >= 0) & (p < tn);
         const bool hit = inr & ((e0 | e1 | e2) >= 0) & (iz >= P.izfar);
-        atomicMin(&S.fb[inr ? y * T.pitch + x : 0], hit ? key : 0xFFFFFFFFu);
+        atomicMin(&S.fb[inr ? y * T.pitch + x : lane], hit ? key : 0xFFFFFFFFu);
         __builtin_amdgcn_wave_barrier();
     }
 }
@@ -949,13 +950,16 @@ __device__ __forceinline__ bool aabb_visible(const RenderParams& P, const Tile& 
     return box_has_centre(P, T, xmn - sx, xmx + sx, ymn - sy, ymx + sy, mag);
 }
 
-__device__ __forceinline__ int64_t xcd_remap(int64_t b, int64_t nb)
+__device__ __forceinline__ uint32_t xcd_remap(uint32_t b, uint32_t nb)
 {
     // Workgroups are dispatched round-robin over the 8 XCDs; give each XCD a
     // contiguous range of views so that one world's views share an L2.
-    const int64_t q = nb >> 3, r = nb & 7, x = b & 7, k = b >> 3;
+    const uint32_t q = nb >> 3, r = nb & 7u, x = b & 7u, k = b >> 3;
     return x * q + (x < r ? x : r) + k;
 }
+
+// n / d for n < 2^31 (see Div31)
+__device__ __forceinline__ uint32_t div31(uint32_t n, Div31 d) { return d.m ? (__umulhi(n, d.m) >> d.s) : n; }
 
 __device__ __forceinline__ float decode_depth(const RenderParams& P, uint32_t key)
 {
@@ -969,17 +973,16 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd) void render_views_kernel(c
     const int tid = threadIdx.x, lane = lane_id(), wid = tid >> 6;
     WaveLds& L = S.wv[wid];
     TSTART(t_kernel);
-    const int64_t blk = xcd_remap((int64_t)blockIdx.x, P.num_blocks);
-    const int tiles = P.tiles_x * P.tiles_y;
-    const int64_t v = blk / tiles;
-    const int tile = (int)(blk % tiles);
-
-    // R1: camera of view v
-    const int64_t per_world = (int64_t)P.A * P.C;
-    const int w = (int)(v / per_world);
-    const int a = (int)((v / P.C) % P.A);
-    const int k = (int)(v % P.C);
-    const int64_t g = (int64_t)w * P.A + a;
+    // block -> (view, tile) -> (agent g = w * A + a, camera k), in 32 bits
+    // (fewer than 2^31 view tiles per launch)
+    const uint32_t blk = xcd_remap(blockIdx.x, (uint32_t)P.num_blocks);
+    const uint32_t v32 = div31(blk, P.div_tiles);
+    const int tile = (int)(blk - v32 * (uint32_t)(P.tiles_x * P.tiles_y));
+    const uint32_t g32 = div31(v32, P.div_cams);
+    const int k = (int)(v32 - g32 * (uint32_t)P.C);
+    const int w = (int)div31(g32, P.div_agents);
+    const int a = (int)(g32 - (uint32_t)w * (uint32_t)P.A);
+    const int64_t v = (int64_t)v32, g = (int64_t)g32;
     Cam cam;
     {
         const float c = P.ac[g], s = P.as[g];
@@ -1039,7 +1042,7 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd) void render_views_kernel(c
     int ix0 = 0, iy0 = 0, ix1 = grid.nx - 1, iy1 = grid.ny - 1;
     if (cull) {
         const float fz = P.far_off;
-        const float tl = T.kl / P.fx, tr = T.kr / P.fx;
+        const float tl = T.kl * P.rfx, tr = T.kr * P.rfx;
         const float ax_ = cam.cc + tl * cam.sc, ay_ = cam.sc - tl * cam.cc;   // f + tl r
         const float bx_ = cam.cc + tr * cam.sc, by_ = cam.sc - tr * cam.cc;   // f + tr r
         const float p1x = cam.x + fz * ax_, p1y = cam.y + fz * ay_;
@@ -1047,14 +1050,16 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd) void render_views_kernel(c
         const float mg = grid.margin + 1.0f;
         const float xlo = fminf(cam.x, fminf(p1x, p2x)) - mg, xhi = fmaxf(cam.x, fmaxf(p1x, p2x)) + mg;
         const float ylo = fminf(cam.y, fminf(p1y, p2y)) - mg, yhi = fmaxf(cam.y, fmaxf(p1y, p2y)) + mg;
-        const float fx0 = floorf((xlo - grid.ox) / cs) - 1.0f, fx1 = floorf((xhi - grid.ox) / cs) + 1.0f;
-        const float fy0 = floorf((ylo - grid.oy) / cs) - 1.0f, fy1 = floorf((yhi - grid.oy) / cs) + 1.0f;
+        // (a product by the rounded reciprocal may floor one cell off: the margin cell covers it)
+        const float fx0 = floorf((xlo - grid.ox) * P.rcs) - 1.0f, fx1 = floorf((xhi - grid.ox) * P.rcs) + 1.0f;
+        const float fy0 = floorf((ylo - grid.oy) * P.rcs) - 1.0f, fy1 = floorf((yhi - grid.oy) * P.rcs) + 1.0f;
         ix0 = (int)fmaxf(fx0, 0.0f); iy0 = (int)fmaxf(fy0, 0.0f);
         ix1 = (int)fminf(fx1, (float)(grid.nx - 1)); iy1 = (int)fminf(fy1, (float)(grid.ny - 1));
     }
     const int rw = ix1 - ix0 + 1, rh = iy1 - iy0 + 1;
     const int nrect = (rw > 0 && rh > 0) ? rw * rh : 0;
-    const float rrw = rw > 0 ? 1.0f / (float)rw : 0.0f;
+    // (approximate: the cell index below corrects a row off by one)
+    const float rrw = rw > 0 ? __builtin_amdgcn_rcpf((float)rw) : 0.0f;
     const float hc = 0.5f * cs + grid.margin;   // half extent of a cell rectangle widened by the margin
     const int64_t abase_w = (int64_t)w * P.A;
     const int64_t lbase_w = (int64_t)w * P.L;
