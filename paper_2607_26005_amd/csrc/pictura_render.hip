@@ -1322,9 +1322,14 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd) void render_views_kernel(c
     uint8_t* ocls = P.out_cls + v * view_px;
     float* odep = P.out_depth + v * view_px;
     if (P.vec_out && (P.W % 16) == 0 && (T.w % 16) == 0) {
-        const int u16 = T.w / 16, n16 = u16 * T.h;
+        // tile origin in the view's images; the offsets below stay 32-bit
+        uint8_t* const cbase = ocls + ((int64_t)T.y0 * P.W + T.x0);
+        float* const dbase = odep + ((int64_t)T.y0 * P.W + T.x0);
+        // u / n = (u * ceil(2^16 / n)) >> 16 exactly for u * n < 2^16 (here u < 1024, n <= 16)
+        const int u16 = T.w >> 4, n16 = u16 * T.h;
+        const uint32_t r16 = (65535u + (uint32_t)u16) / (uint32_t)u16;
         for (int u = tid; u < n16; u += kThreads) {
-            const int row = u / u16, c16 = u % u16;
+            const int row = (int)(((uint32_t)u * r16) >> 16), c16 = u - row * u16;
             const u32x4* src = (const u32x4*)&S.fb[row * T.pitch + 16 * c16];
             uint32_t wd[4];
 #pragma unroll
@@ -1333,21 +1338,29 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd) void render_views_kernel(c
                 wd[q] = (kq.x & 255u) | ((kq.y & 255u) << 8) | ((kq.z & 255u) << 16) | ((kq.w & 255u) << 24);
             }
             const u32x4 pk = {wd[0], wd[1], wd[2], wd[3]};
-            __builtin_nontemporal_store(pk, (u32x4*)(ocls + (int64_t)(T.y0 + row) * P.W + T.x0 + 16 * c16));
+            __builtin_nontemporal_store(pk, (u32x4*)(cbase + (uint32_t)(row * P.W + 16 * c16)));
         }
-        const int u4 = T.w / 4, n4 = u4 * T.h;
+        const int u4 = T.w >> 2, n4 = u4 * T.h;
+        const uint32_t r4 = (65535u + (uint32_t)u4) / (uint32_t)u4;
         const float inf = __uint_as_float(0x7F800000u);
-        for (int u = tid; u < n4; u += kThreads) {
-            const int row = u / u4, c4 = u % u4;
+        auto depth_quad = [&](int u, auto decode) {
+            const int row = (int)(((uint32_t)u * r4) >> 16), c4 = u - row * u4;
             const u32x4 kq = *(const u32x4*)&S.fb[row * T.pitch + 4 * c4];
             f32x4 d = {inf, inf, inf, inf};
             if ((kq.x & kq.y & kq.z & kq.w) >> 8 != 0xFFFFFFu) {   // not all background
-                d.x = (kq.x >> 8) == 0xFFFFFFu ? inf : decode_depth(P, kq.x);
-                d.y = (kq.y >> 8) == 0xFFFFFFu ? inf : decode_depth(P, kq.y);
-                d.z = (kq.z >> 8) == 0xFFFFFFu ? inf : decode_depth(P, kq.z);
-                d.w = (kq.w >> 8) == 0xFFFFFFu ? inf : decode_depth(P, kq.w);
+                d.x = (kq.x >> 8) == 0xFFFFFFu ? inf : decode(kq.x);
+                d.y = (kq.y >> 8) == 0xFFFFFFu ? inf : decode(kq.y);
+                d.z = (kq.z >> 8) == 0xFFFFFFu ? inf : decode(kq.z);
+                d.w = (kq.w >> 8) == 0xFFFFFFu ? inf : decode(kq.w);
             }
-            __builtin_nontemporal_store(d, (f32x4*)(odep + (int64_t)(T.y0 + row) * P.W + T.x0 + 4 * c4));
+            __builtin_nontemporal_store(d, (f32x4*)((char*)dbase + (uint32_t)((row * P.W + 4 * c4) * 4)));
+        };
+        if (P.fast_decode) {
+            const auto dec = [&](uint32_t key) { return rcp_rn(__uint_as_float(((P.qbase - (key >> 8)) << 3) | 4u)); };
+            for (int u = tid; u < n4; u += kThreads) depth_quad(u, dec);
+        } else {
+            const auto dec = [&](uint32_t key) { return 1.0f / __uint_as_float(((P.qbase - (key >> 8)) << 3) | 4u); };
+            for (int u = tid; u < n4; u += kThreads) depth_quad(u, dec);
         }
     } else {
         for (int p = tid; p < npx; p += kThreads) {
