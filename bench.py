@@ -35,8 +35,8 @@ HBM_PEAK_GBS = 8000.0   # MI355X HBM3E peak
 # measured on; when the fingerprint differs, `traffic` is reported as null.
 TRAFFIC = {
     "config": 4,
-    "sources_sha256": "9a3c08944a592791b1b85e929085ab2935f58ed5d00f49a302625d98e66123fe",
-    "fetch_bytes": 1.4666e9,
+    "sources_sha256": "ee09d9aa0575a8f0a3b3d4865e15053afb6ab07af21ab8b3de91c7fa0d524c7f",
+    "fetch_bytes": 1.4667e9,
     "write_bytes": 5368709120,
 }
 TRAFFIC_SOURCES = ["paper_2607_26005_amd/csrc/pictura_render.hip",
