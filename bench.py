@@ -13,7 +13,9 @@ oracle timed on a bounded sample of the same workload.
     python bench.py [--steps 100] [--warmup 10] [--config 4] [--no-cpu-baseline]
 
 (--config 6 times the paper's own rig: 2,048 egos x 4 views at 96x54;
---config 7 the same rig over towns with walls, parked cars and traffic lights.)
+--config 7 the same rig over towns with walls, parked cars and traffic lights;
+--encoder adds the policy's image encoder on the rendered tensors to every step:
+render and encode on one stream, no host round trip.)
 """
 import argparse
 import json
@@ -62,6 +64,8 @@ def parse():
     ap.add_argument("--config", type=int, default=4)
     ap.add_argument("--worlds", type=int, default=None, help="use only the first N worlds (testing)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--encoder", action="store_true",
+                    help="also run the image encoder on each step's views (in-loop coupling)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain device copy of known size (counter calibration)")
@@ -139,12 +143,24 @@ def main():
     out_cls = torch.empty((V, H, W), dtype=torch.uint8, device="cuda")
     out_depth = torch.empty((V, H, W), dtype=torch.float32, device="cuda")
     moving = args.config == 4
+    enc = None
+    if args.encoder:
+        from paper_2607_26005_amd.encoder import ViewEncoder
+        torch.manual_seed(0)
+        enc = ViewEncoder(cams=wl.rig.num_cams).cuda().eval()
+    emb = [None]
     torch.cuda.synchronize()
+
+    def encode():
+        if enc is not None:
+            with torch.no_grad():
+                emb[0] = enc(out_cls, out_depth)
 
     def step(s):
         if moving:
             r.agents_step(da, steer_d[s], accel_d[s], dt=0.1, vmax=20.0)
         r.render(da, wl.rig, out_cls, out_depth)
+        encode()
 
     for s in range(Wm):
         step(s)
@@ -165,6 +181,7 @@ def main():
         ev_r0[s].record(stream)
         r.render(da, wl.rig, out_cls, out_depth)
         ev_r1[s].record(stream)
+        encode()
     t_end.record(stream)
     torch.cuda.synchronize()
     wall = time.perf_counter() - wall0
@@ -225,6 +242,9 @@ def main():
         },
         "cpu_baseline": cpu,
     }
+    if enc is not None:
+        line["config"]["step"] += " + image encoder (5 conv layers, 16 queries x 1 cross-attention per camera, fp32)"
+        line["encoder_ms"] = ms_step - avg_render_ms
     print(json.dumps(line), flush=True)
 
 
