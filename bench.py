@@ -15,7 +15,9 @@ oracle timed on a bounded sample of the same workload.
 (--config 6 times the paper's own rig: 2,048 egos x 4 views at 96x54;
 --config 7 the same rig over towns with walls, parked cars and traffic lights;
 --encoder adds the policy's image encoder on the rendered tensors to every step:
-render and encode on one stream, no host round trip.)
+render and encode on one stream, no host round trip;
+--instances times pictura_render_instances instead: the owning agent of every
+pixel and each agent's footprint and visible pixels, besides class and depth.)
 """
 import argparse
 import json
@@ -64,6 +66,8 @@ def parse():
     ap.add_argument("--config", type=int, default=4)
     ap.add_argument("--worlds", type=int, default=None, help="use only the first N worlds (testing)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--instances", action="store_true",
+                    help="render with instance visibility (pictura_render_instances)")
     ap.add_argument("--encoder", action="store_true",
                     help="also run the image encoder on each step's views (in-loop coupling)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
@@ -142,6 +146,16 @@ def main():
     accel_d = torch.as_tensor(accel, device="cuda")
     out_cls = torch.empty((V, H, W), dtype=torch.uint8, device="cuda")
     out_depth = torch.empty((V, H, W), dtype=torch.float32, device="cuda")
+    out_inst = out_counts = None
+    if args.instances:
+        out_inst = torch.empty((V, H, W), dtype=torch.int32, device="cuda")
+        out_counts = torch.empty((V, wl.agents.agents_per_world, 2), dtype=torch.int32, device="cuda")
+
+    def render():
+        if out_inst is None:
+            r.render(da, wl.rig, out_cls, out_depth)
+        else:
+            pictura.pictura_render_instances(r.ctx, da, wl.rig, out_cls, out_depth, out_inst, out_counts)
     moving = args.config == 4
     enc = None
     if args.encoder:
@@ -159,7 +173,7 @@ def main():
     def step(s):
         if moving:
             r.agents_step(da, steer_d[s], accel_d[s], dt=0.1, vmax=20.0)
-        r.render(da, wl.rig, out_cls, out_depth)
+        render()
         encode()
 
     for s in range(Wm):
@@ -179,7 +193,7 @@ def main():
         if moving:
             r.agents_step(da, steer_d[Wm + s], accel_d[Wm + s], dt=0.1, vmax=20.0)
         ev_r0[s].record(stream)
-        r.render(da, wl.rig, out_cls, out_depth)
+        render()
         ev_r1[s].record(stream)
         encode()
     t_end.record(stream)
@@ -193,6 +207,8 @@ def main():
           f"min {min(render_ms):.4f} max {max(render_ms):.4f}", file=sys.stderr, flush=True)
 
     out_bytes = V * H * W * 5
+    if out_inst is not None:   # + int32 owner per pixel and 2 x uint32 counts per (view, agent)
+        out_bytes += V * H * W * 4 + V * wl.agents.agents_per_world * 8
     achieved = out_bytes / (avg_render_ms * 1e-3) / 1e9
     agent_steps_s = A * K / (total_ms * 1e-3)
     images_s = V * K / (total_ms * 1e-3)
@@ -242,6 +258,9 @@ def main():
         },
         "cpu_baseline": cpu,
     }
+    if out_inst is not None:
+        line["config"]["step"] += " with instance visibility (owner per pixel, footprint and visible pixels per agent)"
+        line["roofline"]["traffic"] = None
     if enc is not None:
         line["config"]["step"] += " + image encoder (5 conv layers, 16 queries x 1 cross-attention per camera, fp32)"
         line["encoder_ms"] = ms_step - avg_render_ms

@@ -165,6 +165,28 @@ pictura_status pictura_bin_scene(pictura_ctx ctx, float cell_size_m, void* strea
 pictura_status pictura_render_views(pictura_ctx ctx, const pictura_agents* agents, const pictura_rig* rig,
                                     uint8_t* out_cls, float* out_depth, void* stream);
 
+/* Render like pictura_render_views (same out_cls, out_depth) and also the
+ * instance visibility the paper's analysis reads from its renderer, each road
+ * user's occlusion percentage (Sec. 4.3, probes of the trained policy):
+ *  - out_inst[v][y][x] (int32): the agent index a (0 .. agents_per_world - 1,
+ *    within the view's world) whose box owns the pixel's visible surface: among
+ *    the boxes with a fragment whose visibility key (rule R7) equals the pixel's
+ *    final key, the lowest index; -1 where no box does (map geometry, traffic
+ *    lights, sky).
+ *  - out_counts[v][a][2] (uint32): footprint, the pixels agent a's box covers in
+ *    view v when drawn alone (rules R2-R7, far plane included), and visible, the
+ *    pixels of out_inst equal to a.  The ego's own entry is 0.  Occlusion
+ *    fraction = 1 - visible / footprint.
+ * Device buffers, caller-owned: out_inst V*H*W int32, out_counts
+ * V*agents_per_world*2 uint32 (the library clears it on `stream` first).
+ * The instance variant of the kernel keeps two extra 64x64 buffers in LDS and
+ * runs at half the occupancy of pictura_render_views.  Errors as
+ * pictura_render_views, and EINVAL for a null out_inst or out_counts.
+ * Asynchronous on `stream`. */
+pictura_status pictura_render_instances(pictura_ctx ctx, const pictura_agents* agents, const pictura_rig* rig,
+                                        uint8_t* out_cls, float* out_depth, int32_t* out_inst,
+                                        uint32_t* out_counts, void* stream);
+
 /* Attach traffic lights (see pictura_lights) to the context: later
  * pictura_render_views calls draw them.  The context keeps the pointers, not
  * a copy: the arrays must stay valid while it renders, and their contents

@@ -66,6 +66,13 @@
  *              (L.x - a*sf, L.y + a*cf, L.z + b) with a = r*cos(30k deg),
  *              b = r*sin(30k deg), the cosine and sine rounded to fp32.
  *
+ * Instances (optional outputs; the road users' occlusion percentages the
+ * paper's analysis reads from its renderer, Sec. 4.3): every other agent's box
+ * is also drawn alone, with the same rules, into a frame of its own.  Its
+ * footprint is the number of pixels that frame covers; a pixel belongs to
+ * the lowest-index agent whose own frame holds the pixel's final key there
+ * (-1: none); an agent's visible count is the number of pixels it owns.
+ *
  * Arithmetic is IEEE fp32 with round-to-nearest and no contraction (this
  * file must be compiled with -ffp-contract=off and without -ffast-math);
  * fmaf() appears only where the rules name fma.  Integer edge functions are
@@ -374,6 +381,7 @@ int oracle_render(int num_worlds, const int64_t* tri_offsets, const float* verts
                   float nearp, float farp, const float* mount,
                   int64_t num_sel, const int64_t* view_ids,
                   uint8_t* out_cls, float* out_depth, uint8_t* out_flags, uint16_t* out_cover,
+                  int32_t* out_inst, uint32_t* out_counts,
                   int num_threads)
 {
     Params P;
@@ -396,6 +404,15 @@ int oracle_render(int num_worlds, const int64_t* tri_offsets, const float* verts
         F.k1 = (uint32_t*)malloc(sizeof(uint32_t) * npx);
         F.k2 = (uint32_t*)malloc(sizeof(uint32_t) * npx);
         F.cover = out_cover ? (uint16_t*)malloc(sizeof(uint16_t) * npx) : NULL;
+        /* a box drawn alone (instances) */
+        Frame G;
+        const int want_inst = out_inst != NULL || out_counts != NULL;
+        G.key = (uint32_t*)malloc(sizeof(uint32_t) * npx);
+        G.edge_key = (uint32_t*)malloc(sizeof(uint32_t) * npx);
+        G.k1 = (uint32_t*)malloc(sizeof(uint32_t) * npx);
+        G.k2 = (uint32_t*)malloc(sizeof(uint32_t) * npx);
+        G.cover = NULL;
+        int32_t* inst = (int32_t*)malloc(sizeof(int32_t) * npx);
 #ifdef _OPENMP
 #pragma omp for schedule(dynamic, 1)
 #endif
@@ -449,6 +466,45 @@ int oracle_render(int num_worlds, const int64_t* tri_offsets, const float* verts
                     draw_triangle(&P, &cam, &F, tri, lcls[h]);
                 }
             }
+            if (want_inst) {
+                for (int64_t p = 0; p < npx; ++p) inst[p] = -1;
+                for (int64_t b = 0; b < agents_per_world; ++b) {
+                    int64_t h = w * agents_per_world + b;
+                    uint32_t footprint = 0;
+                    if (h != g) {
+                        for (int64_t p = 0; p < npx; ++p) {
+                            G.key[p] = CLEAR_KEY;
+                            G.edge_key[p] = 0xFFFFFFFFu;
+                            G.k1[p] = CLEAR_KEY;
+                            G.k2[p] = 0xFFFFFFFFu;
+                        }
+                        float cor[8][3];
+                        box_corners(ax[h], ay[h], az0[h], acos[h], asin[h], alen[h], awid[h], ahgt[h], cor);
+                        for (int f = 0; f < 12; ++f) {
+                            float tri[9];
+                            for (int q = 0; q < 3; ++q) {
+                                tri[3 * q] = cor[BOX_TRIS[f][q]][0];
+                                tri[3 * q + 1] = cor[BOX_TRIS[f][q]][1];
+                                tri[3 * q + 2] = cor[BOX_TRIS[f][q]][2];
+                            }
+                            draw_triangle(&P, &cam, &G, tri, acls[h]);
+                        }
+                        for (int64_t p = 0; p < npx; ++p) {
+                            if (G.key[p] == CLEAR_KEY) continue;
+                            ++footprint;
+                            if (G.key[p] == F.key[p] && inst[p] < 0) inst[p] = (int32_t)b;
+                        }
+                    }
+                    if (out_counts) out_counts[(n * agents_per_world + b) * 2] = footprint;
+                }
+                if (out_counts) {
+                    for (int64_t b = 0; b < agents_per_world; ++b) out_counts[(n * agents_per_world + b) * 2 + 1] = 0;
+                    for (int64_t p = 0; p < npx; ++p)
+                        if (inst[p] >= 0) out_counts[(n * agents_per_world + inst[p]) * 2 + 1]++;
+                }
+                if (out_inst)
+                    for (int64_t p = 0; p < npx; ++p) out_inst[n * npx + p] = inst[p];
+            }
             for (int64_t p = 0; p < npx; ++p) {
                 uint32_t key = F.key[p];
                 uint32_t q = key >> 8;
@@ -474,6 +530,7 @@ int oracle_render(int num_worlds, const int64_t* tri_offsets, const float* verts
             }
         }
         free(F.key); free(F.edge_key); free(F.k1); free(F.k2); free(F.cover);
+        free(G.key); free(G.edge_key); free(G.k1); free(G.k2); free(inst);
     }
     return 0;
 }

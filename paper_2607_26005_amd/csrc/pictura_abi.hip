@@ -273,11 +273,12 @@ pictura_status pictura_bin_scene(pictura_ctx c, float cell, void* stream)
     return PICTURA_OK;
 }
 
-pictura_status pictura_render_views(pictura_ctx c, const pictura_agents* ag, const pictura_rig* rig,
-                                    uint8_t* out_cls, float* out_depth, void* stream)
+// Argument checks and the parameter block of one render call; the launch is the caller's.
+// Returns PICTURA_OK with *empty set when there is nothing to render.
+static pictura_status render_setup(pictura_ctx c, const pictura_agents* ag, const pictura_rig* rig,
+                                   uint8_t* out_cls, float* out_depth, RenderParams& P, bool* empty)
 {
-    if (!c) return PICTURA_EINVAL;
-    c->err.clear();
+    *empty = false;
     if (!ag || !rig || !out_cls || !out_depth) return fail(c, PICTURA_EINVAL, "render_views: null argument");
     if (!c->binned) return fail(c, PICTURA_ESTATE, "render_views: scene not binned");
     if (ag->num_worlds != c->num_worlds)
@@ -302,9 +303,9 @@ pictura_status pictura_render_views(pictura_ctx c, const pictura_agents* ag, con
     if (!(izfar > 0.0f) || !std::isfinite(izcap) || ((f2u(izcap) >> 3) - (f2u(izfar) >> 3)) >= 0xFFFFFFu)
         return fail(c, PICTURA_EINVAL, "render_views: far/near ratio too large for the 24-bit depth key");
     const int64_t V = (int64_t)c->num_worlds * ag->agents_per_world * rig->num_cams;
-    if (V == 0) return PICTURA_OK;
+    if (V == 0) { *empty = true; return PICTURA_OK; }
 
-    RenderParams P{};
+    P = RenderParams{};
     P.scene.triA = c->triA; P.scene.triB = c->triB; P.scene.triC = c->triC;
     P.scene.cell_start = c->cell_start; P.scene.cell_lo = c->cell_lo; P.scene.cell_hi = c->cell_hi;
     P.scene.grids = c->grids; P.scene.cell_size = c->cell_size; P.scene.num_worlds = c->num_worlds;
@@ -356,7 +357,6 @@ pictura_status pictura_render_views(pictura_ctx c, const pictura_agents* ag, con
         P.L = l.lights_per_world;
         P.lcos2 = l.cos_max * l.cos_max;
     }
-    DeviceGuard dg(c->device);
     if (c->stats_on) {
         hipError_t se = hipSuccess;
         if (!c->stats) {
@@ -366,8 +366,43 @@ pictura_status pictura_render_views(pictura_ctx c, const pictura_agents* ag, con
         }
         P.stats = c->stats;
     }
+    return PICTURA_OK;
+}
+
+pictura_status pictura_render_views(pictura_ctx c, const pictura_agents* ag, const pictura_rig* rig,
+                                    uint8_t* out_cls, float* out_depth, void* stream)
+{
+    if (!c) return PICTURA_EINVAL;
+    c->err.clear();
+    DeviceGuard dg(c->device);
+    RenderParams P;
+    bool empty = false;
+    const pictura_status st = render_setup(c, ag, rig, out_cls, out_depth, P, &empty);
+    if (st != PICTURA_OK || empty) return st;
     hipError_t e = launch_render(P, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(c, e, "render_views launch");
+    return PICTURA_OK;
+}
+
+pictura_status pictura_render_instances(pictura_ctx c, const pictura_agents* ag, const pictura_rig* rig,
+                                        uint8_t* out_cls, float* out_depth, int32_t* out_inst,
+                                        uint32_t* out_counts, void* stream)
+{
+    if (!c) return PICTURA_EINVAL;
+    c->err.clear();
+    if (!out_inst || !out_counts) return fail(c, PICTURA_EINVAL, "render_instances: null argument");
+    DeviceGuard dg(c->device);
+    RenderParams P;
+    bool empty = false;
+    const pictura_status st = render_setup(c, ag, rig, out_cls, out_depth, P, &empty);
+    if (st != PICTURA_OK || empty) return st;
+    P.out_inst = out_inst;
+    P.out_counts = out_counts;
+    const size_t nbytes = (size_t)P.num_views * (size_t)P.A * 2u * sizeof(uint32_t);
+    hipError_t e = hipMemsetAsync(out_counts, 0, nbytes, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(c, e, "render_instances clear");
+    e = launch_render(P, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(c, e, "render_instances launch");
     return PICTURA_OK;
 }
 

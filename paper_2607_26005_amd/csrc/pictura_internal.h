@@ -77,6 +77,10 @@ struct RenderParams {
     int32_t vec_out;    // 1: output pointers are 16-byte aligned
     int32_t fast_decode; // 1: every decoded 1/z lies where the fast reciprocal is exact
     unsigned long long* stats;  // optional [kNumStats] work counters (null: off)
+    // instance outputs (both null: off): [V][H][W] agent index within the world
+    // of the visible surface or -1, and [V][A][2] footprint / visible pixels (zeroed before the launch)
+    int32_t* out_inst;
+    uint32_t* out_counts;
     // traffic lights (R10, R11), SoA [num_worlds * L]; L == 0: none
     const float* lx; const float* ly; const float* lz;
     const float* lcf; const float* lsf; const float* lr;

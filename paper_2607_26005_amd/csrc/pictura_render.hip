@@ -690,6 +690,62 @@ __device__ __forceinline__ void raster_blocks(const RenderParams& P, Shared& S, 
 // exact pass: one queued survivor per live lane
 // ---------------------------------------------------------------------------
 
+// R2, R4 and R5 for one world-space triangle: view transform, near clip
+// (Sutherland-Hodgman, explicit cases), snap.  Returns 0 (not drawn), 3, or 4
+// (a quad drawn as the fan pieces (p0, p1, p2) and (p0, p2, p3)).
+__device__ __forceinline__ int setup_triangle(const RenderParams& P, Shared& S, const Cam& cam, const float* tri,
+                                              int& X0, int& Y0, int& X1, int& Y1, int& X2, int& Y2, int& X3,
+                                              int& Y3)
+{
+    int np = 0;
+    float xv[3], yv[3], zv[3];
+#pragma unroll
+    for (int k = 0; k < 3; ++k) view_xform(cam, tri[3 * k], tri[3 * k + 1], tri[3 * k + 2], xv[k], yv[k], zv[k]);
+    const bool in0 = zv[0] >= P.nearp, in1 = zv[1] >= P.nearp, in2 = zv[2] >= P.nearp;
+    bool ok = true;
+    if (in0 && in1 && in2) {
+        ok = snap_vertex(P, xv[0], yv[0], zv[0], X0, Y0) && snap_vertex(P, xv[1], yv[1], zv[1], X1, Y1) &&
+             snap_vertex(P, xv[2], yv[2], zv[2], X2, Y2);
+        np = 3;
+    } else {
+        // R4: Sutherland-Hodgman output of the six straddling cases, in
+        // the order in which v0v1, v1v2, v2v0 visit the edges.
+        STAT(kStClipped, 1);
+        float x01 = 0, y01 = 0, x12 = 0, y12 = 0, x20 = 0, y20 = 0;
+        if (in0 != in1) {
+            if (in0) near_cross(P, xv[0], yv[0], zv[0], xv[1], yv[1], zv[1], x01, y01);
+            else near_cross(P, xv[1], yv[1], zv[1], xv[0], yv[0], zv[0], x01, y01);
+        }
+        if (in1 != in2) {
+            if (in1) near_cross(P, xv[1], yv[1], zv[1], xv[2], yv[2], zv[2], x12, y12);
+            else near_cross(P, xv[2], yv[2], zv[2], xv[1], yv[1], zv[1], x12, y12);
+        }
+        if (in2 != in0) {
+            if (in2) near_cross(P, xv[2], yv[2], zv[2], xv[0], yv[0], zv[0], x20, y20);
+            else near_cross(P, xv[0], yv[0], zv[0], xv[2], yv[2], zv[2], x20, y20);
+        }
+        const float nz = P.nearp;
+        float px[4], py[4], pz[4];
+        const int mcase = (in0 ? 1 : 0) | (in1 ? 2 : 0) | (in2 ? 4 : 0);
+        auto setp = [&](int k, float x, float y, float z) { px[k] = x; py[k] = y; pz[k] = z; };
+        switch (mcase) {
+        case 1: setp(0, xv[0], yv[0], zv[0]); setp(1, x01, y01, nz); setp(2, x20, y20, nz); np = 3; break;
+        case 2: setp(0, x01, y01, nz); setp(1, xv[1], yv[1], zv[1]); setp(2, x12, y12, nz); np = 3; break;
+        case 4: setp(0, x12, y12, nz); setp(1, xv[2], yv[2], zv[2]); setp(2, x20, y20, nz); np = 3; break;
+        case 3: setp(0, xv[0], yv[0], zv[0]); setp(1, xv[1], yv[1], zv[1]); setp(2, x12, y12, nz);
+                setp(3, x20, y20, nz); np = 4; break;
+        case 5: setp(0, xv[0], yv[0], zv[0]); setp(1, x01, y01, nz); setp(2, x12, y12, nz);
+                setp(3, xv[2], yv[2], zv[2]); np = 4; break;
+        default: setp(0, x01, y01, nz); setp(1, xv[1], yv[1], zv[1]); setp(2, xv[2], yv[2], zv[2]);
+                 setp(3, x20, y20, nz); np = 4; break;   // case 6
+        }
+        if (np == 3) { px[3] = px[2]; py[3] = py[2]; pz[3] = pz[2]; }
+        ok = snap_vertex(P, px[0], py[0], pz[0], X0, Y0) && snap_vertex(P, px[1], py[1], pz[1], X1, Y1) &&
+             snap_vertex(P, px[2], py[2], pz[2], X2, Y2) && snap_vertex(P, px[3], py[3], pz[3], X3, Y3);
+    }
+    return ok ? np : 0;
+}
+
 __device__ __forceinline__ void exact_pass(const RenderParams& P, Shared& S, WaveLds& L, const Tile& T, const Cam& cam,
                                            bool live, uint32_t entry, int64_t abase_w, int64_t lbase_w, float pxl,
                                            float pyl, int loff4)
@@ -967,9 +1023,127 @@ __device__ __forceinline__ float decode_depth(const RenderParams& P, uint32_t ke
     return P.fast_decode ? rcp_rn(d) : 1.0f / d;
 }
 
-__global__ __launch_bounds__(kThreads, kWavesPerSimd) void render_views_kernel(const RenderParams P)
+// ---------------------------------------------------------------------------
+// instance pass (render_instances): which agent's box owns each pixel's
+// visible surface, and how many pixels each box covers when drawn alone
+// ---------------------------------------------------------------------------
+
+struct alignas(16) InstLds {
+    uint32_t inst[64 * 64];            // tile pixel (i, j) at j * 64 + i: lowest owning agent, 0xFFFFFFFF none
+    uint32_t bits[kViewWaves][128];    // per wave: coverage of the box being drawn, 2 words per tile row
+};
+
+// Draw agent `agent`'s box (world index h) alone with the rules R2-R7 and the
+// same arithmetic as the raster: every covered pixel sets its coverage bit, and
+// a pixel whose key equals the final key of the view keeps the lowest such
+// agent.  Adds the number of covered pixels to the agent's footprint.  One
+// wave; simple lane-per-pixel sweeps with exact int64 edge values.
+__device__ void draw_box_instances(const RenderParams& P, Shared& S, InstLds& I, const Tile& T, const Cam& cam,
+                                   int64_t h, uint32_t agent, int64_t v)
+{
+    const int lane = lane_id(), wid = threadIdx.x >> 6;
+    uint32_t* bits = I.bits[wid];
+    bits[lane] = 0u;
+    bits[lane + 64] = 0u;
+    __builtin_amdgcn_wave_barrier();
+    const bool live = lane < 12;
+    float tri[9] = {};
+    uint32_t cls = 0;
+    int X0 = 0, Y0 = 0, X1 = 0, Y1 = 0, X2 = 0, Y2 = 0, X3 = 0, Y3 = 0;
+    int np = 0;
+    if (live) {
+        load_box(P, h, lane, tri, cls);
+        np = setup_triangle(P, S, cam, tri, X0, Y0, X1, Y1, X2, Y2, X3, Y3);
+    }
+    float pa = 0.0f, pb = 0.0f, pc = 0.0f;
+    if (np != 0 && !depth_plane(P, cam, tri, pa, pb, pc)) np = 0;
+    const int px0 = 256 * T.x0 + 128, py0 = 256 * T.y0 + 128;
+#pragma unroll 1
+    for (int f = 0; f < 2; ++f) {
+        // fan piece f, oriented, with its edge values at the tile's pixel (0, 0) (R6)
+        int ax = X0, ay = Y0, bx = f == 0 ? X1 : X2, by = f == 0 ? Y1 : Y2, cx = f == 0 ? X2 : X3,
+            cy = f == 0 ? Y2 : Y3;
+        bool valid = f + 2 < np;
+        int i0 = 0, i1 = -1, j0 = 0, j1 = -1;
+        long long cv[3] = {0, 0, 0};
+        int dxs[3] = {0, 0, 0}, dys[3] = {0, 0, 0};
+        if (valid) {
+            const int minX = min(ax, min(bx, cx)), maxX = max(ax, max(bx, cx));
+            const int minY = min(ay, min(by, cy)), maxY = max(ay, max(by, cy));
+            i0 = max((minX - 128 + 255) >> 8, T.x0) - T.x0; i1 = min((maxX - 128) >> 8, T.x0 + T.w - 1) - T.x0;
+            j0 = max((minY - 128 + 255) >> 8, T.y0) - T.y0; j1 = min((maxY - 128) >> 8, T.y0 + T.h - 1) - T.y0;
+            const long long area2 = (long long)(bx - ax) * (long long)(cy - ay) - (long long)(by - ay) * (long long)(cx - ax);
+            valid = i0 <= i1 && j0 <= j1 && area2 != 0;
+            if (area2 < 0) {
+                const int tx = bx, ty = by;
+                bx = cx; by = cy; cx = tx; cy = ty;
+            }
+            const int ex[3] = {bx, cx, ax}, ey[3] = {by, cy, ay};
+            const int fx[3] = {cx, ax, bx}, fy[3] = {cy, ay, by};
+#pragma unroll
+            for (int k = 0; k < 3; ++k) {
+                const int dx = fx[k] - ex[k], dy = fy[k] - ey[k];
+                const int tl = (dy < 0) || (dy == 0 && dx > 0);
+                cv[k] = (long long)dx * (long long)(py0 - ey[k]) - (long long)dy * (long long)(px0 - ex[k]) +
+                        (long long)(tl - 1);
+                dxs[k] = dx;
+                dys[k] = dy;
+            }
+        }
+        uint64_t m = __ballot(valid);
+        while (m) {
+            const int l = __builtin_ctzll(m);
+            m &= m - 1;
+            const int ri0 = (int)readlane((uint32_t)i0, l), ri1 = (int)readlane((uint32_t)i1, l);
+            const int rj0 = (int)readlane((uint32_t)j0, l), rj1 = (int)readlane((uint32_t)j1, l);
+            long long rc[3];
+            int rdx[3], rdy[3];
+#pragma unroll
+            for (int k = 0; k < 3; ++k) {
+                const unsigned long long u = (unsigned long long)cv[k];
+                rc[k] = (long long)(((unsigned long long)readlane((uint32_t)(u >> 32), l) << 32) |
+                                    readlane((uint32_t)u, l));
+                rdx[k] = (int)readlane((uint32_t)dxs[k], l);
+                rdy[k] = (int)readlane((uint32_t)dys[k], l);
+            }
+            const float rpa = readlane_f(pa, l), rpb = readlane_f(pb, l), rpc = readlane_f(pc, l);
+            const uint32_t rcls = readlane(cls, l);
+            const int bw = ri1 - ri0 + 1, n = bw * (rj1 - rj0 + 1);
+            for (int s0 = 0; s0 < n; s0 += 64) {
+                const int p = s0 + lane;
+                if (p < n) {
+                    const int jj = p / bw, i = ri0 + (p - jj * bw), j = rj0 + jj;   // tile pixel
+                    bool cov = true;
+#pragma unroll
+                    for (int k = 0; k < 3; ++k)
+                        cov = cov && rc[k] - 256ll * rdy[k] * i + 256ll * rdx[k] * j >= 0;
+                    const float pxf = ((float)(T.x0 + i) + 0.5f) - P.cx;
+                    const float pyf = ((float)(T.y0 + j) + 0.5f) - P.cy;
+                    const uint32_t key = pixel_key(P, pxf, pyf, rpa, rpb, rpc, rcls);
+                    if (cov && key != 0xFFFFFFFFu) {
+                        atomicOr(&bits[2 * j + (i >> 5)], 1u << (i & 31));
+                        if (key == S.fb[j * T.pitch + i]) atomicMin(&I.inst[j * 64 + i], agent);
+                    }
+                }
+            }
+        }
+    }
+    __builtin_amdgcn_wave_barrier();
+    const uint32_t cnt = (uint32_t)(__popc(bits[lane]) + __popc(bits[lane + 64]));
+    const uint32_t tot = readlane(wave_incl_sum(cnt), 63);
+    if (lane == 0 && tot != 0) atomicAdd(&P.out_counts[2 * (v * P.A + agent)], tot);
+    __builtin_amdgcn_wave_barrier();
+}
+
+struct NoInstLds {};
+
+// kInst: the instance variant (its LDS admits two waves per SIMD, so it may use
+// twice the registers)
+template <bool kInst>
+__global__ __launch_bounds__(kThreads, kInst ? 2 : kWavesPerSimd) void render_views_kernel(const RenderParams P)
 {
     __shared__ Shared S;
+    __shared__ typename std::conditional<kInst, InstLds, NoInstLds>::type I;
     const int tid = threadIdx.x, lane = lane_id(), wid = tid >> 6;
     WaveLds& L = S.wv[wid];
     TSTART(t_kernel);
@@ -1022,6 +1196,9 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd) void render_views_kernel(c
     const int loff4 = ((lane >> 3) * T.pitch + (lane & 7)) * 4;
     if (P.stats && tid < kNumStats) S.stat[tid] = 0;
     if (tid < 4) S.ctl[tid] = 0;
+    if constexpr (kInst) {
+        for (int p = tid; p < 64 * 64; p += kThreads) I.inst[p] = 0xFFFFFFFFu;
+    }
 
     // world-space frustum planes of the tile: four side planes through the
     // camera centre, near and far with margins
@@ -1316,6 +1493,36 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd) void render_views_kernel(c
     }
     __syncthreads();
 
+    if constexpr (kInst) {
+        // every non-ego box that can reach the tile, the waves taking alternate agents
+        for (int ac = 0; ac * 64 * kViewWaves < P.A; ++ac) {
+            const int ai = (ac * 64 + lane) * kViewWaves + wid;
+            bool vis = ai < P.A && ai != a;
+            if (vis && cull) {
+                const int64_t h = abase_w + ai;
+                const float x = P.ax[h], y = P.ay[h], z0 = P.az0[h];
+                const float R = 0.5f * (P.al[h] + P.aw[h]) * 1.0009765625f + 0.0009765625f;
+                vis = aabb_visible(P, T, F, cam, x - R, y - R, z0, x + R, y + R, z0 + P.ah[h]);
+            }
+            uint64_t m = __ballot(vis);
+            while (m) {
+                const int l = __builtin_ctzll(m);
+                m &= m - 1;
+                const uint32_t agent = readlane((uint32_t)ai, l);
+                draw_box_instances(P, S, I, T, cam, abase_w + agent, agent, v);
+            }
+        }
+        __syncthreads();
+        // the instance image and each agent's visible pixels
+        const int64_t view_px = (int64_t)P.W * P.H;
+        for (int p = tid; p < npx; p += kThreads) {
+            const int row = p / T.w, col = p % T.w;
+            const uint32_t id = I.inst[row * 64 + col];
+            P.out_inst[v * view_px + (int64_t)(T.y0 + row) * P.W + T.x0 + col] = (int32_t)id;
+            if (id != 0xFFFFFFFFu) atomicAdd(&P.out_counts[2 * (v * P.A + id) + 1], 1u);
+        }
+    }
+
     // ---- R8 resolve + coalesced write-out of the tile ----
     TSTART(t_out);
     const int64_t view_px = (int64_t)P.W * P.H;
@@ -1381,7 +1588,8 @@ __global__ __launch_bounds__(kThreads, kWavesPerSimd) void render_views_kernel(c
 hipError_t launch_render(const RenderParams& p, hipStream_t s)
 {
     if (p.num_blocks <= 0) return hipSuccess;
-    hipLaunchKernelGGL(render_views_kernel, dim3((unsigned)p.num_blocks), dim3(kThreads), 0, s, p);
+    if (p.out_inst) hipLaunchKernelGGL(render_views_kernel<true>, dim3((unsigned)p.num_blocks), dim3(kThreads), 0, s, p);
+    else hipLaunchKernelGGL(render_views_kernel<false>, dim3((unsigned)p.num_blocks), dim3(kThreads), 0, s, p);
     return hipGetLastError();
 }
 

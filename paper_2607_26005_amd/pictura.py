@@ -85,6 +85,8 @@ _lib.pictura_set_option.argtypes = [_P, ctypes.c_int32, ctypes.c_int32]
 _lib.pictura_set_option.restype = ctypes.c_int32
 _lib.pictura_stats_copy.argtypes = [_P, _P, ctypes.c_int32, ctypes.c_int32]
 _lib.pictura_stats_copy.restype = ctypes.c_int32
+_lib.pictura_render_instances.argtypes = [_P, ctypes.POINTER(_Agents), ctypes.POINTER(_Rig), _P, _P, _P, _P, _P]
+_lib.pictura_render_instances.restype = ctypes.c_int32
 _lib.pictura_set_lights.argtypes = [_P, ctypes.POINTER(_Lights)]
 _lib.pictura_set_lights.restype = ctypes.c_int32
 _lib.pictura_selftest_rcp.argtypes = [_P, ctypes.c_uint32, ctypes.c_uint32, _P]
@@ -93,7 +95,7 @@ _lib.pictura_selftest_rcp.restype = ctypes.c_int32
 EXPORTED = ["pictura_create", "pictura_destroy", "pictura_last_error", "pictura_scene_upload",
             "pictura_bin_scene", "pictura_render_views", "pictura_agents_step", "pictura_bins_info",
             "pictura_bins_copy", "pictura_set_option", "pictura_stats_copy", "pictura_selftest_rcp",
-            "pictura_set_lights"]
+            "pictura_set_lights", "pictura_render_instances"]
 
 STAT_NAMES = ["view_tiles", "cells_in_rect", "cells_prefiltered", "cells_visible", "cand_tris", "boxes_visible",
               "box_tris", "first_pass_survivors", "exact_batches", "clipped", "raster_tris", "lane_tris",
@@ -180,6 +182,17 @@ def pictura_render_views(ctx, agents, rig, out_cls, out_depth, stream=None):
     r = make_rig(rig) if not isinstance(rig, _Rig) else rig
     _check(ctx, _lib.pictura_render_views(ctx, ctypes.byref(a), ctypes.byref(r), _ptr(out_cls), _ptr(out_depth),
                                           _stream(stream)))
+
+
+def pictura_render_instances(ctx, agents, rig, out_cls, out_depth, out_inst, out_counts, stream=None):
+    """As pictura_render_views, plus out_inst (int32, V*H*W) and out_counts
+    (int32 tensor viewed as uint32, V*A*2: footprint, visible)."""
+    a = _Agents(int(agents.num_worlds), int(agents.agents_per_world),
+                *[_ptr(getattr(agents, n)) for n in ("x", "y", "z0", "cos_h", "sin_h", "length", "width", "height",
+                                                     "cls")])
+    r = make_rig(rig) if not isinstance(rig, _Rig) else rig
+    _check(ctx, _lib.pictura_render_instances(ctx, ctypes.byref(a), ctypes.byref(r), _ptr(out_cls), _ptr(out_depth),
+                                              _ptr(out_inst), _ptr(out_counts), _stream(stream)))
 
 
 def pictura_agents_step(ctx, state, steer, accel, dt: float = 0.1, vmax: float = 20.0, stream=None):
@@ -319,6 +332,20 @@ class Renderer:
             out_depth = torch.empty(shape, dtype=torch.float32, device=agents.x.device)
         pictura_render_views(self.ctx, agents, rig, out_cls, out_depth, stream)
         return out_cls, out_depth
+
+    def render_instances(self, agents: DeviceAgents, rig, stream=None):
+        """Returns (cls, depth, inst, counts): counts [V, A, 2] int32 holding
+        (footprint, visible) pixels per agent and view."""
+        import torch
+        V = agents.num_worlds * agents.agents_per_world * int(rig.mount.shape[0])
+        shape = (V, int(rig.height), int(rig.width))
+        dev = agents.x.device
+        out_cls = torch.empty(shape, dtype=torch.uint8, device=dev)
+        out_depth = torch.empty(shape, dtype=torch.float32, device=dev)
+        out_inst = torch.empty(shape, dtype=torch.int32, device=dev)
+        counts = torch.empty((V, agents.agents_per_world, 2), dtype=torch.int32, device=dev)
+        pictura_render_instances(self.ctx, agents, rig, out_cls, out_depth, out_inst, counts, stream)
+        return out_cls, out_depth, out_inst, counts
 
     def agents_step(self, agents: DeviceAgents, steer, accel, dt=0.1, vmax=20.0, stream=None):
         pictura_agents_step(self.ctx, agents, steer, accel, dt, vmax, stream)
