@@ -17,7 +17,8 @@ oracle timed on a bounded sample of the same workload.
 --encoder adds the policy's image encoder on the rendered tensors to every step:
 render and encode on one stream, no host round trip;
 --instances times pictura_render_instances instead: the owning agent of every
-pixel and each agent's footprint and visible pixels, besides class and depth.)
+pixel and each agent's footprint and visible pixels, besides class and depth;
+--rgb times pictura_render_rgb: the shaded colour image besides class and depth.)
 """
 import argparse
 import json
@@ -66,6 +67,7 @@ def parse():
     ap.add_argument("--config", type=int, default=4)
     ap.add_argument("--worlds", type=int, default=None, help="use only the first N worlds (testing)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
+    ap.add_argument("--rgb", action="store_true", help="render the shaded colour image too (pictura_render_rgb)")
     ap.add_argument("--instances", action="store_true",
                     help="render with instance visibility (pictura_render_instances)")
     ap.add_argument("--encoder", action="store_true",
@@ -146,13 +148,17 @@ def main():
     accel_d = torch.as_tensor(accel, device="cuda")
     out_cls = torch.empty((V, H, W), dtype=torch.uint8, device="cuda")
     out_depth = torch.empty((V, H, W), dtype=torch.float32, device="cuda")
-    out_inst = out_counts = None
+    out_inst = out_counts = out_rgb = None
+    if args.rgb:
+        out_rgb = torch.empty((V, 3, H, W), dtype=torch.uint8, device="cuda")
     if args.instances:
         out_inst = torch.empty((V, H, W), dtype=torch.int32, device="cuda")
         out_counts = torch.empty((V, wl.agents.agents_per_world, 2), dtype=torch.int32, device="cuda")
 
     def render():
-        if out_inst is None:
+        if out_rgb is not None:
+            pictura.pictura_render_rgb(r.ctx, da, wl.rig, out_cls, out_depth, out_rgb)
+        elif out_inst is None:
             r.render(da, wl.rig, out_cls, out_depth)
         else:
             pictura.pictura_render_instances(r.ctx, da, wl.rig, out_cls, out_depth, out_inst, out_counts)
@@ -207,6 +213,8 @@ def main():
           f"min {min(render_ms):.4f} max {max(render_ms):.4f}", file=sys.stderr, flush=True)
 
     out_bytes = V * H * W * 5
+    if out_rgb is not None:    # + 3 colour bytes per pixel
+        out_bytes += V * H * W * 3
     if out_inst is not None:   # + int32 owner per pixel and 2 x uint32 counts per (view, agent)
         out_bytes += V * H * W * 4 + V * wl.agents.agents_per_world * 8
     achieved = out_bytes / (avg_render_ms * 1e-3) / 1e9
@@ -258,6 +266,9 @@ def main():
         },
         "cpu_baseline": cpu,
     }
+    if out_rgb is not None:
+        line["config"]["step"] += " with the shaded colour image (planar RGB)"
+        line["roofline"]["traffic"] = None
     if out_inst is not None:
         line["config"]["step"] += " with instance visibility (owner per pixel, footprint and visible pixels per agent)"
         line["roofline"]["traffic"] = None

@@ -165,6 +165,25 @@ pictura_status pictura_bin_scene(pictura_ctx ctx, float cell_size_m, void* strea
 pictura_status pictura_render_views(pictura_ctx ctx, const pictura_agents* agents, const pictura_rig* rig,
                                     uint8_t* out_cls, float* out_depth, void* stream);
 
+/* Render like pictura_render_views and also a shaded colour image (rule R13;
+ * the paper's observations are RGB images, Sec. 3.2, rendering features: agents
+ * are cuboids coloured per face with depth-aware brightness).  In this mode a
+ * box triangle's visibility key carries a shading id, class | (face + 1) << 4
+ * with face 0 bottom, 1 top, 2 back, 3 front, 4 right, 5 left (the order of
+ * rule R9's triangles, two per face), in place of its class; every other
+ * triangle keeps its class.  out_cls receives key & 15.  out_rgb[v][c][y][x]
+ * (uint8, planar, c = red, green, blue): with base = palette[class] / 255 (the
+ * table in the repository's design notes), factor = 0.45, 1, 0.55, 0.85, 0.7,
+ * 0.7 for the faces bottom .. left and 1 for other surfaces, b = 1 - 0.6 *
+ * min(z / far, 1) on box faces (z the output depth) and 1 elsewhere:
+ * rint(255 * min(base * (factor * b), 1)), fp32 in this order.  Antialiasing is
+ * not applied (single sample per pixel).  Device buffers, caller-owned:
+ * out_rgb V*3*H*W bytes.  EINVAL as pictura_render_views, a null out_rgb, or a
+ * scene class ID above 15 (agent and light classes are taken modulo 16).
+ * Asynchronous on `stream`. */
+pictura_status pictura_render_rgb(pictura_ctx ctx, const pictura_agents* agents, const pictura_rig* rig,
+                                  uint8_t* out_cls, float* out_depth, uint8_t* out_rgb, void* stream);
+
 /* Render like pictura_render_views (same out_cls, out_depth) and also the
  * instance visibility the paper's analysis reads from its renderer, each road
  * user's occlusion percentage (Sec. 4.3, probes of the trained policy):

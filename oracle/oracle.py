@@ -44,7 +44,7 @@ def lib():
                                     ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                     ctypes.c_float, ctypes.c_float, ctypes.c_float, ctypes.c_float,
                                     ctypes.c_float, ctypes.c_float, p,
-                                    ctypes.c_int64, p, p, p, p, p, p, p, ctypes.c_int]
+                                    ctypes.c_int64, p, p, p, p, p, p, p, p, ctypes.c_int]
         L.oracle_quantize.restype = None
         L.oracle_quantize.argtypes = [p, ctypes.c_int64, ctypes.c_float, ctypes.c_float, p, p]
         L.oracle_bin.restype = ctypes.c_int
@@ -65,13 +65,14 @@ def _c(a, dtype):
 
 
 def render(scene, agents, rig, view_ids=None, want_flags=True, want_cover=False, num_threads=0, lights=None,
-           want_instances=False):
+           want_instances=False, want_rgb=False):
     """Render the selected views (default: all).  Returns dict with
     cls [n,H,W] u8, depth [n,H,W] f32, flags [n,H,W] u8 (bit0 EDGE, bit1 TIE),
     and cover [n,H,W] u16 when requested.  lights: object with
     lights_per_world, x, y, z, cos_f, sin_f, radius, cls, cos_max (or None).
     want_instances adds inst [n,H,W] int32 (owning agent or -1) and counts
-    [n,A,2] uint32 (footprint, visible pixels per agent)."""
+    [n,A,2] uint32 (footprint, visible pixels per agent); want_rgb switches to
+    colour mode (rule R13) and adds rgb [n,3,H,W] uint8."""
     L = lib()
     A = int(agents.agents_per_world)
     C = int(rig.mount.shape[0])
@@ -87,6 +88,7 @@ def render(scene, agents, rig, view_ids=None, want_flags=True, want_cover=False,
     out_cover = np.empty((n, H, W), np.uint16) if want_cover else None
     out_inst = np.empty((n, H, W), np.int32) if want_instances else None
     out_counts = np.empty((n, A, 2), np.uint32) if want_instances else None
+    out_rgb = np.empty((n, 3, H, W), np.uint8) if want_rgb else None
     keep = [_c(scene.tri_offsets, np.int64), _c(scene.verts, np.float32), _c(scene.cls, np.uint8)]
     af = [_c(getattr(agents, f), np.float32) for f in
           ("x", "y", "z0", "cos_h", "sin_h", "length", "width", "height")]
@@ -105,7 +107,7 @@ def render(scene, agents, rig, view_ids=None, want_flags=True, want_cover=False,
                          C, W, H, float(rig.fx), float(rig.fy), float(rig.cx), float(rig.cy),
                          float(rig.near), float(rig.far), _ptr(mount),
                          n, _ptr(view_ids), _ptr(out_cls), _ptr(out_depth), _ptr(out_flags),
-                         _ptr(out_cover), _ptr(out_inst), _ptr(out_counts), int(num_threads))
+                         _ptr(out_cover), _ptr(out_inst), _ptr(out_counts), _ptr(out_rgb), int(num_threads))
     if rc != 0:
         raise ValueError("oracle_render: view id out of range")
     out = dict(cls=out_cls, depth=out_depth)
@@ -113,6 +115,8 @@ def render(scene, agents, rig, view_ids=None, want_flags=True, want_cover=False,
         out["flags"] = out_flags
     if want_cover:
         out["cover"] = out_cover
+    if want_rgb:
+        out["rgb"] = out_rgb
     if want_instances:
         out["inst"] = out_inst
         out["counts"] = out_counts

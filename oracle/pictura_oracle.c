@@ -66,6 +66,16 @@
  *              (L.x - a*sf, L.y + a*cf, L.z + b) with a = r*cos(30k deg),
  *              b = r*sin(30k deg), the cosine and sine rounded to fp32.
  *
+ * R13 colour (optional output): in colour mode the 12 triangles of a box use
+ *              the shading id (class & 15) | (k/2 + 1) << 4 (k the triangle
+ *              index of R9: faces bottom, top, back, front, right, left) in
+ *              place of the class in the key; the class output is key & 15.
+ *              The pixel colour is rint(255 * min(base * (factor * b), 1))
+ *              per channel, base = palette[class] / 255, factor by face
+ *              (0.45, 1, 0.55, 0.85, 0.7, 0.7; 1 off boxes), b = 1 - 0.6 *
+ *              min(z * (1/far), 1) on box faces (z the output depth), else 1.
+ *              No antialiasing (one sample per pixel).
+ *
  * Instances (optional outputs; the road users' occlusion percentages the
  * paper's analysis reads from its renderer, Sec. 4.3): every other agent's box
  * is also drawn alone, with the same rules, into a frame of its own.  Its
@@ -320,6 +330,33 @@ static void box_corners(float x, float y, float z0, float c, float s, float L, f
     }
 }
 
+/* R13 palette (class -> RGB bytes) and face factors */
+static const uint8_t PALETTE[16][3] = {
+    {96, 112, 72}, {72, 72, 78}, {232, 232, 224}, {52, 96, 220}, {140, 184, 232}, {160, 160, 152},
+    {224, 72, 64}, {168, 144, 120}, {255, 32, 24}, {255, 184, 0}, {32, 224, 96}, {128, 128, 128},
+    {128, 128, 128}, {128, 128, 128}, {128, 128, 128}, {128, 128, 128}};
+static const float FACE_FACTOR[8] = {1.0f, 0.45f, 1.0f, 0.55f, 0.85f, 0.7f, 0.7f, 1.0f};
+
+static void shade(const Params* P, uint32_t key, uint8_t* c3)
+{
+    uint32_t cls = key & 15u, face = (key >> 4) & 7u, q = key >> 8;
+    float f = FACE_FACTOR[face];
+    if (face != 0u && q != 0xFFFFFFu) {
+        float z = 1.0f / u2f(((P->qbase - q) << 3) | 4u);
+        float rfar = 1.0f / P->farp;
+        float t = z * rfar;
+        if (t > 1.0f) t = 1.0f;
+        float b = 1.0f - 0.6f * t;
+        f = f * b;
+    }
+    for (int c = 0; c < 3; ++c) {
+        float base = (float)PALETTE[cls][c] / 255.0f;
+        float v = base * f;
+        if (v > 1.0f) v = 1.0f;
+        c3[c] = (uint8_t)rintf(255.0f * v);
+    }
+}
+
 /* cos and sin of 30k degrees, k = 0..11, rounded to fp32 (R11) */
 static void sector_table(float cs[12], float sn[12])
 {
@@ -381,7 +418,7 @@ int oracle_render(int num_worlds, const int64_t* tri_offsets, const float* verts
                   float nearp, float farp, const float* mount,
                   int64_t num_sel, const int64_t* view_ids,
                   uint8_t* out_cls, float* out_depth, uint8_t* out_flags, uint16_t* out_cover,
-                  int32_t* out_inst, uint32_t* out_counts,
+                  int32_t* out_inst, uint32_t* out_counts, uint8_t* out_rgb,
                   int num_threads)
 {
     Params P;
@@ -445,7 +482,9 @@ int oracle_render(int num_worlds, const int64_t* tri_offsets, const float* verts
                         tri[3 * q + 1] = cor[BOX_TRIS[f][q]][1];
                         tri[3 * q + 2] = cor[BOX_TRIS[f][q]][2];
                     }
-                    draw_triangle(&P, &cam, &F, tri, acls[h]);
+                    uint32_t sid = acls[h];
+                    if (out_rgb) sid = (sid & 15u) | (uint32_t)(f / 2 + 1) << 4;
+                    draw_triangle(&P, &cam, &F, tri, sid);
                 }
             }
             for (int64_t l = 0; l < lights_per_world; ++l) {
@@ -508,7 +547,12 @@ int oracle_render(int num_worlds, const int64_t* tri_offsets, const float* verts
             for (int64_t p = 0; p < npx; ++p) {
                 uint32_t key = F.key[p];
                 uint32_t q = key >> 8;
-                out_cls[n * npx + p] = (uint8_t)(key & 255u);
+                out_cls[n * npx + p] = (uint8_t)(key & (out_rgb ? 15u : 255u));
+                if (out_rgb) {
+                    uint8_t c3[3];
+                    shade(&P, key, c3);
+                    for (int c = 0; c < 3; ++c) out_rgb[(n * 3 + c) * npx + p] = c3[c];
+                }
                 if (q == 0xFFFFFFu) {
                     out_depth[n * npx + p] = INFINITY;
                 } else {

@@ -24,6 +24,7 @@ struct pictura_ctx_s {
     uint8_t* cls = nullptr;
     int64_t* offsets_d = nullptr;
     bool have_scene = false;
+    uint8_t max_cls = 0;   // largest class ID of the static triangles
     // bins
     bool binned = false;
     float cell_size = 0.0f;
@@ -175,8 +176,11 @@ pictura_status pictura_scene_upload(pictura_ctx c, const pictura_scene* s, void*
     const int64_t T = s->tri_offsets[nw];
     if (T > 0x7FFFFFFFll) return fail(c, PICTURA_ERANGE, "scene_upload: more than 2^31-1 triangles");
     if (T > 0 && (!s->verts || !s->cls)) return fail(c, PICTURA_EINVAL, "scene_upload: null verts/cls");
-    for (int64_t t = 0; t < T; ++t)
+    uint8_t max_cls = 0;
+    for (int64_t t = 0; t < T; ++t) {
         if (s->cls[t] == 255) return fail(c, PICTURA_EINVAL, "scene_upload: class ID 255 is reserved");
+        max_cls = s->cls[t] > max_cls ? s->cls[t] : max_cls;
+    }
     for (int w = 0; w < nw; ++w) {
         const float* b = s->bounds + 4 * w;
         if (!(std::isfinite(b[0]) && std::isfinite(b[1]) && std::isfinite(b[2]) && std::isfinite(b[3])) ||
@@ -209,6 +213,7 @@ pictura_status pictura_scene_upload(pictura_ctx c, const pictura_scene* s, void*
     c->num_worlds = nw;
     c->T = T;
     c->have_scene = true;
+    c->max_cls = max_cls;
     return PICTURA_OK;
 }
 
@@ -381,6 +386,25 @@ pictura_status pictura_render_views(pictura_ctx c, const pictura_agents* ag, con
     if (st != PICTURA_OK || empty) return st;
     hipError_t e = launch_render(P, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(c, e, "render_views launch");
+    return PICTURA_OK;
+}
+
+pictura_status pictura_render_rgb(pictura_ctx c, const pictura_agents* ag, const pictura_rig* rig, uint8_t* out_cls,
+                                  float* out_depth, uint8_t* out_rgb, void* stream)
+{
+    if (!c) return PICTURA_EINVAL;
+    c->err.clear();
+    if (!out_rgb) return fail(c, PICTURA_EINVAL, "render_rgb: null argument");
+    if (c->have_scene && c->max_cls > 15) return fail(c, PICTURA_EINVAL, "render_rgb: scene class IDs must be below 16");
+    DeviceGuard dg(c->device);
+    RenderParams P;
+    bool empty = false;
+    const pictura_status st = render_setup(c, ag, rig, out_cls, out_depth, P, &empty);
+    if (st != PICTURA_OK || empty) return st;
+    P.out_rgb = out_rgb;
+    P.rfar = 1.0f / P.farp;
+    hipError_t e = launch_render(P, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(c, e, "render_rgb launch");
     return PICTURA_OK;
 }
 

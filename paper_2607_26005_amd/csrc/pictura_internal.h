@@ -81,6 +81,10 @@ struct RenderParams {
     // of the visible surface or -1, and [V][A][2] footprint / visible pixels (zeroed before the launch)
     int32_t* out_inst;
     uint32_t* out_counts;
+    // shaded RGB output (null: off), planar [V][3][H][W] uint8 (rule R13); when set,
+    // box triangles carry their face in bits 4..6 of the class byte
+    uint8_t* out_rgb;
+    float rfar;         // 1 / far (rounded)
     // traffic lights (R10, R11), SoA [num_worlds * L]; L == 0: none
     const float* lx; const float* ly; const float* lz;
     const float* lcf; const float* lsf; const float* lr;

@@ -314,6 +314,8 @@ __device__ __forceinline__ void load_box(const RenderParams& P, int64_t h, int f
         tri[3 * q + 2] = (n & 4) ? ztop : z0;
     }
     cls = (uint32_t)P.acls[h];
+    // R13: in RGB mode the shading id adds the face (1 bottom, 2 top, 3 back, 4 front, 5 right, 6 left)
+    if (P.out_rgb) cls = (cls & 15u) | ((uint32_t)(face >> 1) + 1u) << 4;
 }
 
 // R11: sector k of light h, the triangle (centre, rim k, rim k + 1).  Rim
@@ -1017,6 +1019,33 @@ __device__ __forceinline__ uint32_t xcd_remap(uint32_t b, uint32_t nb)
 // n / d for n < 2^31 (see Div31)
 __device__ __forceinline__ uint32_t div31(uint32_t n, Div31 d) { return d.m ? (__umulhi(n, d.m) >> d.s) : n; }
 
+// R13: colour of a resolved key.  Shading id sid = key & 255: class = sid & 15,
+// face = sid >> 4 (0: not a box face).  v = base[class] * (face factor * b),
+// b = 1 - 0.6 min(z / far, 1) on box faces (depth-aware brightness, z the
+// decoded depth of R8), 1 elsewhere; byte = rint(255 min(v, 1)).
+__device__ __forceinline__ void shade_rgb(const RenderParams& P, uint32_t key, uint32_t* c3)
+{
+    constexpr uint8_t kPal[16][3] = {{96, 112, 72},   {72, 72, 78},    {232, 232, 224}, {52, 96, 220},
+                                     {140, 184, 232}, {160, 160, 152}, {224, 72, 64},   {168, 144, 120},
+                                     {255, 32, 24},   {255, 184, 0},   {32, 224, 96},   {128, 128, 128},
+                                     {128, 128, 128}, {128, 128, 128}, {128, 128, 128}, {128, 128, 128}};
+    constexpr float kFace[8] = {1.0f, 0.45f, 1.0f, 0.55f, 0.85f, 0.7f, 0.7f, 1.0f};
+    const uint32_t cls = key & 15u, face = (key >> 4) & 7u;
+    float f = kFace[face];
+    if (face != 0u && (key >> 8) != 0xFFFFFFu) {
+        const float z = 1.0f / __uint_as_float(((P.qbase - (key >> 8)) << 3) | 4u);
+        const float t = fminf(z * P.rfar, 1.0f);
+        const float b = 1.0f - 0.6f * t;
+        f = f * b;
+    }
+#pragma unroll
+    for (int c = 0; c < 3; ++c) {
+        const float base = (float)kPal[cls][c] / 255.0f;
+        const float val = fminf(base * f, 1.0f);
+        c3[c] = (uint32_t)rintf(255.0f * val);
+    }
+}
+
 __device__ __forceinline__ float decode_depth(const RenderParams& P, uint32_t key)
 {
     const float d = __uint_as_float(((P.qbase - (key >> 8)) << 3) | 4u);
@@ -1535,6 +1564,7 @@ __global__ __launch_bounds__(kThreads, kInst ? 2 : kWavesPerSimd) void render_vi
         // u / n = (u * ceil(2^16 / n)) >> 16 exactly for u * n < 2^16 (here u < 1024, n <= 16)
         const int u16 = T.w >> 4, n16 = u16 * T.h;
         const uint32_t r16 = (65535u + (uint32_t)u16) / (uint32_t)u16;
+        const uint32_t cm = P.out_rgb ? 15u : 255u;   // class byte (R13: the face bits are not part of the class)
         for (int u = tid; u < n16; u += kThreads) {
             const int row = (int)(((uint32_t)u * r16) >> 16), c16 = u - row * u16;
             const u32x4* src = (const u32x4*)&S.fb[row * T.pitch + 16 * c16];
@@ -1542,7 +1572,7 @@ __global__ __launch_bounds__(kThreads, kInst ? 2 : kWavesPerSimd) void render_vi
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
                 const u32x4 kq = src[q];
-                wd[q] = (kq.x & 255u) | ((kq.y & 255u) << 8) | ((kq.z & 255u) << 16) | ((kq.w & 255u) << 24);
+                wd[q] = (kq.x & cm) | ((kq.y & cm) << 8) | ((kq.z & cm) << 16) | ((kq.w & cm) << 24);
             }
             const u32x4 pk = {wd[0], wd[1], wd[2], wd[3]};
             __builtin_nontemporal_store(pk, (u32x4*)(cbase + (uint32_t)(row * P.W + 16 * c16)));
@@ -1574,8 +1604,22 @@ __global__ __launch_bounds__(kThreads, kInst ? 2 : kWavesPerSimd) void render_vi
             const int row = p / T.w, col = p % T.w;
             const uint32_t key = S.fb[row * T.pitch + col];
             const int64_t o = (int64_t)(T.y0 + row) * P.W + T.x0 + col;
-            ocls[o] = (uint8_t)(key & 255u);
+            ocls[o] = (uint8_t)(key & (P.out_rgb ? 15u : 255u));
             odep[o] = (key >> 8) == 0xFFFFFFu ? __uint_as_float(0x7F800000u) : decode_depth(P, key);
+        }
+    }
+    if (P.out_rgb) {
+        // R13: shaded colour of each pixel, planar [3][H][W] per view
+        uint8_t* const rgb = P.out_rgb + v * 3 * view_px;
+        for (int p = tid; p < npx; p += kThreads) {
+            const int row = p / T.w, col = p % T.w;
+            const uint32_t key = S.fb[row * T.pitch + col];
+            uint32_t c3[3];
+            shade_rgb(P, key, c3);
+            const int64_t o = (int64_t)(T.y0 + row) * P.W + T.x0 + col;
+            rgb[o] = (uint8_t)c3[0];
+            rgb[view_px + o] = (uint8_t)c3[1];
+            rgb[2 * view_px + o] = (uint8_t)c3[2];
         }
     }
     if (P.stats) {

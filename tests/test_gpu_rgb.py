@@ -1,0 +1,77 @@
+"""GPU parity of the shaded colour mode (rule R13) against the oracle: classes
+and depth as in the plain mode, colour bytes bit-exact wherever the oracle does
+not flag the pixel (EDGE / TIE), and at most 1e-4 of the pixels may differ."""
+import functools
+
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from paper_2607_26005_amd import scenegen as sg
+from tests.parity import assert_parity
+
+pytestmark = pytest.mark.gpu
+
+
+def _torch():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no HIP device")
+    return torch
+
+
+@pytest.fixture(scope="module")
+def lib():
+    _torch()
+    from paper_2607_26005_amd import pictura
+    return pictura
+
+
+@functools.lru_cache(maxsize=None)
+def workload(cfg, worlds=None):
+    return sg.make_config(cfg, num_worlds=worlds)
+
+
+def check(lib, wl, views, label, tile=0):
+    torch = _torch()
+    print(f"[{label}] {wl.num_views} views tile={tile}", flush=True)
+    r = lib.Renderer(0)
+    try:
+        r.set_option(lib.OPT_TILE, tile)
+        r.upload(wl.scene, wl.cell_size)
+        if wl.lights is not None:
+            r.set_lights(lib.DeviceLights.from_host(wl.lights))
+        da = lib.DeviceAgents.from_host(wl.agents)
+        c, d, rgb = r.render_rgb(da, wl.rig)
+        torch.cuda.synchronize()
+        idx = torch.as_tensor(np.asarray(views), device="cuda")
+        gc, gd, grgb = c[idx].cpu().numpy(), d[idx].cpu().numpy(), rgb[idx].cpu().numpy()
+    finally:
+        r.close()
+    ora = O.render(wl.scene, wl.agents, wl.rig, view_ids=np.asarray(views), lights=wl.lights, want_rgb=True)
+    s = assert_parity(gc, gd, ora, label)
+    unflag = ora["flags"] == 0
+    diff = (grgb != ora["rgb"]).any(1)
+    assert not (diff & unflag).any(), (label, int((diff & unflag).sum()))
+    assert diff.sum() <= 1e-4 * diff.size, (label, int(diff.sum()))
+    boxes = int(((ora["cls"] == 3) | (ora["cls"] == 6)).sum())
+    print(f"[{label}] {s} colour mismatches {int(diff.sum())}, box pixels {boxes}", flush=True)
+    return boxes
+
+
+def test_rgb_tiny_all_views(lib):
+    wl = workload(1)
+    assert check(lib, wl, np.arange(wl.num_views), "rgb-tiny") > 0
+
+
+def test_rgb_dense_traffic_sampled(lib):
+    wl = workload(3, 4)
+    views = np.sort(np.random.default_rng(51).choice(wl.num_views, size=96, replace=False))
+    assert check(lib, wl, views, "rgb-dense") > 0
+
+
+def test_rgb_town_paper_rig_and_tiles(lib):
+    wl = workload(7, 2)   # two tiles per view, lights
+    views = np.sort(np.random.default_rng(52).choice(wl.num_views, size=64, replace=False))
+    check(lib, wl, views, "rgb-town")
+    check(lib, wl, views, "rgb-town-tile24", tile=24)
