@@ -18,7 +18,8 @@ oracle timed on a bounded sample of the same workload.
 render and encode on one stream, no host round trip;
 --instances times pictura_render_instances instead: the owning agent of every
 pixel and each agent's footprint and visible pixels, besides class and depth;
---rgb times pictura_render_rgb: the shaded colour image besides class and depth.)
+--rgb times pictura_render_rgb: the shaded colour image besides class and depth;
+--aa with --rgb times pictura_render_rgb_aa: the colour image antialiased.)
 """
 import argparse
 import json
@@ -68,6 +69,7 @@ def parse():
     ap.add_argument("--worlds", type=int, default=None, help="use only the first N worlds (testing)")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--rgb", action="store_true", help="render the shaded colour image too (pictura_render_rgb)")
+    ap.add_argument("--aa", action="store_true", help="with --rgb: antialiased colour (pictura_render_rgb_aa)")
     ap.add_argument("--instances", action="store_true",
                     help="render with instance visibility (pictura_render_instances)")
     ap.add_argument("--encoder", action="store_true",
@@ -75,7 +77,10 @@ def parse():
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain device copy of known size (counter calibration)")
-    return ap.parse_args()
+    args = ap.parse_args()
+    if args.aa and not args.rgb:
+        ap.error("--aa needs --rgb")
+    return args
 
 
 def copy_calibration():
@@ -157,7 +162,8 @@ def main():
 
     def render():
         if out_rgb is not None:
-            pictura.pictura_render_rgb(r.ctx, da, wl.rig, out_cls, out_depth, out_rgb)
+            fn = pictura.pictura_render_rgb_aa if args.aa else pictura.pictura_render_rgb
+            fn(r.ctx, da, wl.rig, out_cls, out_depth, out_rgb)
         elif out_inst is None:
             r.render(da, wl.rig, out_cls, out_depth)
         else:
@@ -268,6 +274,8 @@ def main():
     }
     if out_rgb is not None:
         line["config"]["step"] += " with the shaded colour image (planar RGB)"
+        if args.aa:
+            line["config"]["step"] += ", antialiased (analytic coverage, one sample per pixel)"
         line["roofline"]["traffic"] = None
     if out_inst is not None:
         line["config"]["step"] += " with instance visibility (owner per pixel, footprint and visible pixels per agent)"

@@ -176,13 +176,37 @@ pictura_status pictura_render_views(pictura_ctx ctx, const pictura_agents* agent
  * table in the repository's design notes), factor = 0.45, 1, 0.55, 0.85, 0.7,
  * 0.7 for the faces bottom .. left and 1 for other surfaces, b = 1 - 0.6 *
  * min(z / far, 1) on box faces (z the output depth) and 1 elsewhere:
- * rint(255 * min(base * (factor * b), 1)), fp32 in this order.  Antialiasing is
- * not applied (single sample per pixel).  Device buffers, caller-owned:
+ * rint(255 * min(base * (factor * b), 1)), fp32 in this order.  One sample
+ * per pixel (pictura_render_rgb_aa antialiases).  Device buffers, caller-owned:
  * out_rgb V*3*H*W bytes.  EINVAL as pictura_render_views, a null out_rgb, or a
  * scene class ID above 15 (agent and light classes are taken modulo 16).
  * Asynchronous on `stream`. */
 pictura_status pictura_render_rgb(pictura_ctx ctx, const pictura_agents* agents, const pictura_rig* rig,
                                   uint8_t* out_cls, float* out_depth, uint8_t* out_rgb, void* stream);
+
+/* pictura_render_rgb with analytic-coverage antialiasing at one sample per
+ * pixel (rule R14; the paper's production renders smooth edges this way so
+ * that thin structures such as lane lines stay visible at low resolution,
+ * Sec. 3.2, rendering features, and App. on render quality).  out_cls and
+ * out_depth are those of pictura_render_views (the pixel centre's surface).
+ * Each fan piece of rule R6 leaves a fragment on every pixel whose centre is
+ * within one pixel of its snapped bounding box and that it covers in part:
+ * with E_k the edge function of R6 at the centre (no top-left bias) and L_k
+ * the edge's length, both in subpixels, c_k = min(max(fma(fl(E_k),
+ * fl(1 / (256 L_k)), 0.5), 0), 1), coverage a = min(max(((c_0 + c_1) + c_2) -
+ * 2, 0), 1), a8 = rint(255 a), fp32; the fragment exists when 0 < a8 < 255
+ * and the piece's depth plane passes R7's test at the centre.  A pixel keeps
+ * its nearest fragment, ordered by o = (key >> 16) << 16 | (key & 255) << 8 |
+ * (255 - a8) with key the fragment's R7 key.  With key_c the pixel's final
+ * key, when o >> 16 <= key_c >> 16 (the fragment is not behind the centre's
+ * surface) and (o >> 8) & 255 != key_c & 255 (another shading id), the
+ * pixel's colour is (C_o * a8 + C_c * (255 - a8) + 127) /
+ * 255 per channel in integers, C_o the R13 colour of the key ((o >> 16) << 16)
+ * | ((o >> 8) & 255) and C_c that of key_c; otherwise C_c.  Runs a kernel
+ * variant with an extra 16 KiB LDS edge buffer per tile at half the
+ * occupancy.  Buffers, errors and ordering as pictura_render_rgb. */
+pictura_status pictura_render_rgb_aa(pictura_ctx ctx, const pictura_agents* agents, const pictura_rig* rig,
+                                     uint8_t* out_cls, float* out_depth, uint8_t* out_rgb, void* stream);
 
 /* Render like pictura_render_views (same out_cls, out_depth) and also the
  * instance visibility the paper's analysis reads from its renderer, each road

@@ -44,7 +44,7 @@ def lib():
                                     ctypes.c_int, ctypes.c_int, ctypes.c_int,
                                     ctypes.c_float, ctypes.c_float, ctypes.c_float, ctypes.c_float,
                                     ctypes.c_float, ctypes.c_float, p,
-                                    ctypes.c_int64, p, p, p, p, p, p, p, p, ctypes.c_int]
+                                    ctypes.c_int64, p, p, p, p, p, p, p, p, ctypes.c_int, ctypes.c_int]
         L.oracle_quantize.restype = None
         L.oracle_quantize.argtypes = [p, ctypes.c_int64, ctypes.c_float, ctypes.c_float, p, p]
         L.oracle_bin.restype = ctypes.c_int
@@ -65,14 +65,15 @@ def _c(a, dtype):
 
 
 def render(scene, agents, rig, view_ids=None, want_flags=True, want_cover=False, num_threads=0, lights=None,
-           want_instances=False, want_rgb=False):
+           want_instances=False, want_rgb=False, antialias=False):
     """Render the selected views (default: all).  Returns dict with
     cls [n,H,W] u8, depth [n,H,W] f32, flags [n,H,W] u8 (bit0 EDGE, bit1 TIE),
     and cover [n,H,W] u16 when requested.  lights: object with
     lights_per_world, x, y, z, cos_f, sin_f, radius, cls, cos_max (or None).
     want_instances adds inst [n,H,W] int32 (owning agent or -1) and counts
     [n,A,2] uint32 (footprint, visible pixels per agent); want_rgb switches to
-    colour mode (rule R13) and adds rgb [n,3,H,W] uint8."""
+    colour mode (rule R13) and adds rgb [n,3,H,W] uint8; antialias (with
+    want_rgb) blends partial-coverage fragments into it (rule R14)."""
     L = lib()
     A = int(agents.agents_per_world)
     C = int(rig.mount.shape[0])
@@ -107,7 +108,8 @@ def render(scene, agents, rig, view_ids=None, want_flags=True, want_cover=False,
                          C, W, H, float(rig.fx), float(rig.fy), float(rig.cx), float(rig.cy),
                          float(rig.near), float(rig.far), _ptr(mount),
                          n, _ptr(view_ids), _ptr(out_cls), _ptr(out_depth), _ptr(out_flags),
-                         _ptr(out_cover), _ptr(out_inst), _ptr(out_counts), _ptr(out_rgb), int(num_threads))
+                         _ptr(out_cover), _ptr(out_inst), _ptr(out_counts), _ptr(out_rgb), int(bool(antialias)),
+                         int(num_threads))
     if rc != 0:
         raise ValueError("oracle_render: view id out of range")
     out = dict(cls=out_cls, depth=out_depth)

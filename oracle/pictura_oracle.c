@@ -74,7 +74,18 @@
  *              per channel, base = palette[class] / 255, factor by face
  *              (0.45, 1, 0.55, 0.85, 0.7, 0.7; 1 off boxes), b = 1 - 0.6 *
  *              min(z * (1/far), 1) on box faces (z the output depth), else 1.
- *              No antialiasing (one sample per pixel).
+ * R14 antialiasing (optional, colour mode; the paper smooths edges with
+ *              analytic coverage at one sample per pixel, Sec. 3.2 and its
+ *              appendix on render quality): every snapped fan piece leaves,
+ *              on each pixel whose centre is within one pixel of its box, a
+ *              fragment with coverage a8 = rint(255 a), a = clamp(sum of
+ *              the edges' clamp(0.5 + signed centre distance in px) - 2),
+ *              when 0 < a8 < 255 and its R7 key at the centre exists.  The
+ *              pixel keeps the least o = (key >> 16) << 16 | (key & 255) << 8
+ *              | (255 - a8); a kept fragment not behind the centre's key
+ *              (16-bit depth prefix) with another shading id blends over the
+ *              centre's colour: (C_o a8 + C (255 - a8) + 127) / 255, C_o the
+ *              colour of key ((o >> 16) << 16) | ((o >> 8) & 255).
  *
  * Instances (optional outputs; the road users' occlusion percentages the
  * paper's analysis reads from its renderer, Sec. 4.3): every other agent's box
@@ -173,6 +184,7 @@ typedef struct {
     uint32_t* k1;       /* best key */
     uint32_t* k2;       /* best key of a class different from k1's */
     uint16_t* cover;    /* optional coverage count */
+    uint32_t* frag;     /* R14: [H*W] nearest partial-coverage fragment, or NULL */
 } Frame;
 
 static void frame_update_tie(Frame* F, int p, uint32_t k)
@@ -206,6 +218,68 @@ static int snap(const Params* P, V3 v, int32_t* X, int32_t* Y)
 
 static int64_t floor_div256(int64_t a) { return a >= 0 ? a / 256 : -((-a + 255) / 256); }
 
+/* R14: analytic coverage of pixel centres near one snapped, positively
+ * oriented triangle.  The coverage of a pixel by one edge's half-plane is
+ * approximated by 0.5 plus the centre's signed distance to the edge in
+ * pixels, clamped to [0, 1]; the triangle's coverage is the sum of its three
+ * edges' coverages minus 2, clamped.  Pixels whose centre lies within one
+ * pixel of the snapped bounding box are considered. */
+static void coverage_fragments(const Params* P, Frame* F, const int32_t* vx, const int32_t* vy, float pa, float pb,
+                               float pc, uint32_t cls)
+{
+    int32_t lo_x = vx[0], hi_x = vx[0], lo_y = vy[0], hi_y = vy[0];
+    for (int k = 1; k < 3; ++k) {
+        if (vx[k] < lo_x) lo_x = vx[k];
+        if (vx[k] > hi_x) hi_x = vx[k];
+        if (vy[k] < lo_y) lo_y = vy[k];
+        if (vy[k] > hi_y) hi_y = vy[k];
+    }
+    /* pixel i's centre 256 i + 128 within [lo - 256, hi + 256] */
+    int64_t i0 = floor_div256((int64_t)lo_x - 384 + 255), i1 = floor_div256((int64_t)hi_x + 128);
+    int64_t j0 = floor_div256((int64_t)lo_y - 384 + 255), j1 = floor_div256((int64_t)hi_y + 128);
+    if (i0 < 0) i0 = 0;
+    if (j0 < 0) j0 = 0;
+    if (i1 > P->W - 1) i1 = P->W - 1;
+    if (j1 > P->H - 1) j1 = P->H - 1;
+    float inv_len[3];
+    for (int e = 0; e < 3; ++e) {
+        /* edge e runs from vertex e + 1 to vertex e + 2 (mod 3), as in R6 */
+        int64_t dx = (int64_t)vx[(e + 2) % 3] - vx[(e + 1) % 3];
+        int64_t dy = (int64_t)vy[(e + 2) % 3] - vy[(e + 1) % 3];
+        float len = sqrtf((float)(dx * dx + dy * dy));
+        inv_len[e] = 1.0f / (256.0f * len);
+    }
+    for (int64_t j = j0; j <= j1; ++j) {
+        for (int64_t i = i0; i <= i1; ++i) {
+            int64_t px = 256 * i + 128, py = 256 * j + 128;
+            float sum = 0.0f;
+            for (int e = 0; e < 3; ++e) {
+                int64_t ax = vx[(e + 1) % 3], ay = vy[(e + 1) % 3];
+                int64_t dx = (int64_t)vx[(e + 2) % 3] - ax, dy = (int64_t)vy[(e + 2) % 3] - ay;
+                int64_t E = dx * (py - ay) - dy * (px - ax);
+                float c = fmaf((float)E, inv_len[e], 0.5f);
+                if (c < 0.0f) c = 0.0f;
+                if (c > 1.0f) c = 1.0f;
+                sum = sum + c;
+            }
+            float a = sum - 2.0f;
+            if (a < 0.0f) a = 0.0f;
+            if (a > 1.0f) a = 1.0f;
+            uint32_t a8 = (uint32_t)rintf(255.0f * a);
+            if (a8 == 0u || a8 == 255u) continue;
+            float pxf = ((float)i + 0.5f) - P->cx;
+            float pyf = ((float)j + 0.5f) - P->cy;
+            float iz = fmaf(pa, pxf, fmaf(pb, pyf, pc));
+            if (!(iz >= P->izfar)) continue;
+            if (iz > P->izcap) iz = P->izcap;
+            uint32_t key = ((P->qbase - (f2u(iz) >> 3)) << 8) | cls;
+            uint32_t o = ((key >> 16) << 16) | ((key & 255u) << 8) | (255u - a8);
+            int p = (int)(j * P->W + i);
+            if (o < F->frag[p]) F->frag[p] = o;
+        }
+    }
+}
+
 /* Rasterize one snapped triangle (R6, R7) into the frame. */
 static void raster_tri(const Params* P, Frame* F, int32_t X0, int32_t Y0, int32_t X1, int32_t Y1,
                        int32_t X2, int32_t Y2, float pa, float pb, float pc, uint32_t cls)
@@ -215,6 +289,10 @@ static void raster_tri(const Params* P, Frame* F, int32_t X0, int32_t Y0, int32_
     if (area2 < 0) {
         int32_t tx = X1, ty = Y1;
         X1 = X2; Y1 = Y2; X2 = tx; Y2 = ty;
+    }
+    if (F->frag) {
+        const int32_t vx[3] = {X0, X1, X2}, vy[3] = {Y0, Y1, Y2};
+        coverage_fragments(P, F, vx, vy, pa, pb, pc, cls);
     }
     int32_t ax[3] = {X1, X2, X0}, ay[3] = {Y1, Y2, Y0};
     int32_t bx[3] = {X2, X0, X1}, by[3] = {Y2, Y0, Y1};
@@ -418,7 +496,7 @@ int oracle_render(int num_worlds, const int64_t* tri_offsets, const float* verts
                   float nearp, float farp, const float* mount,
                   int64_t num_sel, const int64_t* view_ids,
                   uint8_t* out_cls, float* out_depth, uint8_t* out_flags, uint16_t* out_cover,
-                  int32_t* out_inst, uint32_t* out_counts, uint8_t* out_rgb,
+                  int32_t* out_inst, uint32_t* out_counts, uint8_t* out_rgb, int aa,
                   int num_threads)
 {
     Params P;
@@ -441,6 +519,7 @@ int oracle_render(int num_worlds, const int64_t* tri_offsets, const float* verts
         F.k1 = (uint32_t*)malloc(sizeof(uint32_t) * npx);
         F.k2 = (uint32_t*)malloc(sizeof(uint32_t) * npx);
         F.cover = out_cover ? (uint16_t*)malloc(sizeof(uint16_t) * npx) : NULL;
+        F.frag = (out_rgb && aa) ? (uint32_t*)malloc(sizeof(uint32_t) * npx) : NULL;
         /* a box drawn alone (instances) */
         Frame G;
         const int want_inst = out_inst != NULL || out_counts != NULL;
@@ -449,6 +528,7 @@ int oracle_render(int num_worlds, const int64_t* tri_offsets, const float* verts
         G.k1 = (uint32_t*)malloc(sizeof(uint32_t) * npx);
         G.k2 = (uint32_t*)malloc(sizeof(uint32_t) * npx);
         G.cover = NULL;
+        G.frag = NULL;
         int32_t* inst = (int32_t*)malloc(sizeof(int32_t) * npx);
 #ifdef _OPENMP
 #pragma omp for schedule(dynamic, 1)
@@ -467,6 +547,7 @@ int oracle_render(int num_worlds, const int64_t* tri_offsets, const float* verts
                 F.k1[p] = CLEAR_KEY;
                 F.k2[p] = 0xFFFFFFFFu;
                 if (F.cover) F.cover[p] = 0;
+                if (F.frag) F.frag[p] = 0xFFFFFFFFu;
             }
             for (int64_t t = tri_offsets[w]; t < tri_offsets[w + 1]; ++t)
                 draw_triangle(&P, &cam, &F, verts + 9 * t, tcls[t]);
@@ -551,6 +632,16 @@ int oracle_render(int num_worlds, const int64_t* tri_offsets, const float* verts
                 if (out_rgb) {
                     uint8_t c3[3];
                     shade(&P, key, c3);
+                    uint32_t o = F.frag ? F.frag[p] : 0xFFFFFFFFu;
+                    /* R14: a fragment not behind the centre's surface, of another
+                     * shading id, is blended over it with its coverage */
+                    if (o != 0xFFFFFFFFu && (o >> 16) <= (key >> 16) && ((o >> 8) & 255u) != (key & 255u)) {
+                        uint8_t f3[3];
+                        shade(&P, ((o >> 16) << 16) | ((o >> 8) & 255u), f3);
+                        uint32_t a8 = 255u - (o & 255u);
+                        for (int c = 0; c < 3; ++c)
+                            c3[c] = (uint8_t)(((uint32_t)f3[c] * a8 + (uint32_t)c3[c] * (255u - a8) + 127u) / 255u);
+                    }
                     for (int c = 0; c < 3; ++c) out_rgb[(n * 3 + c) * npx + p] = c3[c];
                 }
                 if (q == 0xFFFFFFu) {
@@ -573,7 +664,7 @@ int oracle_render(int num_worlds, const int64_t* tri_offsets, const float* verts
                 if (out_cover) out_cover[n * npx + p] = F.cover[p];
             }
         }
-        free(F.key); free(F.edge_key); free(F.k1); free(F.k2); free(F.cover);
+        free(F.key); free(F.edge_key); free(F.k1); free(F.k2); free(F.cover); free(F.frag);
         free(G.key); free(G.edge_key); free(G.k1); free(G.k2); free(inst);
     }
     return 0;

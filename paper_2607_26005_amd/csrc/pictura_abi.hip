@@ -389,8 +389,8 @@ pictura_status pictura_render_views(pictura_ctx c, const pictura_agents* ag, con
     return PICTURA_OK;
 }
 
-pictura_status pictura_render_rgb(pictura_ctx c, const pictura_agents* ag, const pictura_rig* rig, uint8_t* out_cls,
-                                  float* out_depth, uint8_t* out_rgb, void* stream)
+static pictura_status render_rgb(pictura_ctx c, const pictura_agents* ag, const pictura_rig* rig, uint8_t* out_cls,
+                                 float* out_depth, uint8_t* out_rgb, void* stream, bool aa)
 {
     if (!c) return PICTURA_EINVAL;
     c->err.clear();
@@ -403,9 +403,22 @@ pictura_status pictura_render_rgb(pictura_ctx c, const pictura_agents* ag, const
     if (st != PICTURA_OK || empty) return st;
     P.out_rgb = out_rgb;
     P.rfar = 1.0f / P.farp;
+    P.aa = aa ? 1 : 0;
     hipError_t e = launch_render(P, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(c, e, "render_rgb launch");
     return PICTURA_OK;
+}
+
+pictura_status pictura_render_rgb(pictura_ctx c, const pictura_agents* ag, const pictura_rig* rig, uint8_t* out_cls,
+                                  float* out_depth, uint8_t* out_rgb, void* stream)
+{
+    return render_rgb(c, ag, rig, out_cls, out_depth, out_rgb, stream, false);
+}
+
+pictura_status pictura_render_rgb_aa(pictura_ctx c, const pictura_agents* ag, const pictura_rig* rig, uint8_t* out_cls,
+                                     float* out_depth, uint8_t* out_rgb, void* stream)
+{
+    return render_rgb(c, ag, rig, out_cls, out_depth, out_rgb, stream, true);
 }
 
 pictura_status pictura_render_instances(pictura_ctx c, const pictura_agents* ag, const pictura_rig* rig,

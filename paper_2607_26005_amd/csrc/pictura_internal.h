@@ -85,6 +85,7 @@ struct RenderParams {
     // box triangles carry their face in bits 4..6 of the class byte
     uint8_t* out_rgb;
     float rfar;         // 1 / far (rounded)
+    int32_t aa;         // 1: colour antialiasing (R14; with out_rgb)
     // traffic lights (R10, R11), SoA [num_worlds * L]; L == 0: none
     const float* lx; const float* ly; const float* lz;
     const float* lcf; const float* lsf; const float* lr;

@@ -82,6 +82,7 @@ struct Tile {
     int x0, y0, w, h;
     int pitch;         // framebuffer words per row
     float kl, kr, kt, kb;
+    float cm;          // base margin (px) of the projected-box centre test
 };
 
 // Raster record of a snapped, oriented triangle with more than kSmallPx
@@ -390,12 +391,13 @@ __device__ __forceinline__ bool outside_tile(const RenderParams& P, const Tile& 
 
 // Can a box of projected x in [xmn, xmx], y in [ymn, ymx] (approximate
 // projections whose magnitude is at most mag) hold a pixel centre of the
-// tile?  The margin covers half a subpixel of snapping plus the error of the
-// hardware reciprocal and of the fp32 arithmetic.
+// tile (with antialiasing: within one pixel of the tile)?  The margin covers
+// half a subpixel of snapping plus the error of the hardware reciprocal and of
+// the fp32 arithmetic.
 __device__ __forceinline__ bool box_has_centre(const RenderParams& P, const Tile& T, float xmn, float xmx, float ymn,
                                                float ymx, float mag)
 {
-    const float m = 0.00390625f + (mag + P.cabs) * 3.814697265625e-06f;   // 1/256 + 2^-18 (|p| + |c|)
+    const float m = T.cm + (mag + P.cabs) * 3.814697265625e-06f;   // base + 2^-18 (|p| + |c|)
     const float ilo = fmaxf(ceilf(xmn - m - 0.5f), (float)T.x0);
     const float ihi = fminf(floorf(xmx + m - 0.5f), (float)(T.x0 + T.w - 1));
     const float jlo = fmaxf(ceilf(ymn - m - 0.5f), (float)T.y0);
@@ -748,9 +750,206 @@ __device__ __forceinline__ int setup_triangle(const RenderParams& P, Shared& S, 
     return ok ? np : 0;
 }
 
+// R14 (colour antialiasing): the fragments a fan piece leaves on the pixels
+// its edges cross.  For every tile pixel whose centre lies within one pixel
+// of the piece's snapped bounding box: with E_k the exact edge function of R6
+// at the centre (no top-left bias) and L_k the edge's length in subpixels,
+// E_k / (256 L_k) is the centre's distance to the edge in pixels (positive
+// inside); c_k = min(max(fma(fl(E_k), fl(1 / (256 L_k)), 0.5), 0), 1),
+// coverage a = min(max(((c_0 + c_1) + c_2) - 2, 0), 1), a8 = rint(255 a).  A
+// pixel with 0 < a8 < 255 whose key (R7, the piece's plane at the centre)
+// exists takes the minimum of (key >> 16) << 16 | (key & 255) << 8 |
+// (255 - a8) in the edge buffer.  fl(E_k) is the same value whichever exact
+// integer type carries E_k.
+__device__ __forceinline__ float aa_cover(double e, float r)
+{
+    return fminf(fmaxf(fmaf((float)e, r, 0.5f), 0.0f), 1.0f);
+}
+
+__device__ __forceinline__ float aa_cover(int e, float r)
+{
+    return fminf(fmaxf(fmaf((float)e, r, 0.5f), 0.0f), 1.0f);
+}
+
+// Coverage fragment of one pixel (c the three edge coverages): the edge
+// buffer word, or 0xFFFFFFFF when the pixel takes none.
+__device__ __forceinline__ uint32_t aa_fragment(const RenderParams& P, float c0, float c1, float c2, float pxf,
+                                                float pyf, float pa, float pb, float pc, uint32_t cls)
+{
+    const float a = fminf(fmaxf(((c0 + c1) + c2) - 2.0f, 0.0f), 1.0f);
+    const uint32_t a8 = (uint32_t)rintf(255.0f * a);
+    const uint32_t key = pixel_key(P, pxf, pyf, pa, pb, pc, cls);
+    const bool frag = a8 != 0u && a8 != 255u && key != 0xFFFFFFFFu;
+    return frag ? ((key >> 16) << 16) | ((key & 255u) << 8) | (255u - a8) : 0xFFFFFFFFu;
+}
+
+// Pieces with small windows, all lanes together: the window pixels are
+// numbered consecutively over the lanes and every step hands 64 of them to the
+// 64 lanes (as the packed raster does).  With spans below 2^14 subpixels the
+// edge function at any window pixel is below 2^30 in magnitude, so it is an
+// int32 value plus int32 steps from the window's first pixel.
+constexpr int kAaSmall = 64;   // most window pixels of a packed piece
+
+__device__ __forceinline__ void aa_packed(const RenderParams& P, WaveLds& L, uint32_t* fbo, const Tile& T, bool on,
+                                          int i0, int j0, int w, int npx_, const int* e, const int* sa,
+                                          const int* sb, const float* r, float pa, float pb, float pc, uint32_t cls)
+{
+    const int lane = lane_id();
+    const uint32_t npx = on ? (uint32_t)npx_ : 0u;
+    const uint32_t incl = wave_incl_sum(npx);
+    const uint32_t n = readlane(incl, 63), pre = incl - npx;
+    const uint32_t geo = (uint32_t)i0 | (uint32_t)j0 << 8 | (uint32_t)w << 16 | cls << 24;
+    const float rw = __builtin_amdgcn_rcpf((float)w);   // row = floor((p + 0.5) / w) for p < 2^12
+    uint32_t carry = 0;
+    uint32_t* mark = L.u.cells.start;
+    for (uint32_t s0 = 0; s0 < n; s0 += 64) {
+        mark[lane] = 0u;
+        __builtin_amdgcn_wave_barrier();
+        if (npx != 0 && pre >= s0 && pre < s0 + 64u) mark[pre - s0] = (uint32_t)lane + 1u;
+        __builtin_amdgcn_wave_barrier();
+        const uint32_t o = wave_incl_max(max(mark[lane], carry));
+        carry = readlane(o, 63);
+        const int t = (int)o - 1;
+        const uint32_t slot = s0 + (uint32_t)lane;
+        const int p = (int)(slot - bperm(t, pre));
+        const uint32_t g = bperm(t, geo);
+        const int tw = (int)((g >> 16) & 255u);
+        const int tn = (int)bperm(t, npx);
+        const int jj = (int)(((float)p + 0.5f) * __uint_as_float(bperm(t, __float_as_uint(rw))));
+        const int ii = p - jj * tw;
+        const int x = (int)(g & 255u) + ii, y = (int)((g >> 8) & 255u) + jj;   // tile pixel
+        float c[3];
+#pragma unroll
+        for (int k = 0; k < 3; ++k) {
+            const int ek = (int)bperm(t, (uint32_t)e[k]) + __mul24((int)bperm(t, (uint32_t)sa[k]), ii) +
+                           __mul24((int)bperm(t, (uint32_t)sb[k]), jj);
+            c[k] = aa_cover(ek, __uint_as_float(bperm(t, __float_as_uint(r[k]))));
+        }
+        const float pxf = ((float)(T.x0 + x) + 0.5f) - P.cx;
+        const float pyf = ((float)(T.y0 + y) + 0.5f) - P.cy;
+        const uint32_t f = aa_fragment(P, c[0], c[1], c[2], pxf, pyf, __uint_as_float(bperm(t, __float_as_uint(pa))),
+                                       __uint_as_float(bperm(t, __float_as_uint(pb))),
+                                       __uint_as_float(bperm(t, __float_as_uint(pc))), g >> 24);
+        // p in range keeps the address inside the window, hence the tile
+        const bool inr = (slot < n) & (p >= 0) & (p < tn);
+        atomicMin(&fbo[inr ? y * 64 + x : lane], inr ? f : 0xFFFFFFFFu);
+        __builtin_amdgcn_wave_barrier();
+    }
+}
+
+// Window of a piece: the tile pixels whose centre lies within one pixel of
+// its snapped bounding box, 256 i + 128 in [minX - 256, maxX + 256].  Pieces
+// whose window has at most kAaSmall pixels and whose box spans below 2^14
+// subpixels take the packed path; the others are swept by the whole wave one
+// at a time in 8x8 blocks (lane = pixel), E_k evaluated in fp64 from its exact
+// integer value at the tile origin plus exact integer steps: exact while
+// |E_k| < 2^53, and beyond that c_k is 0 or 1 whatever the rounding
+// (|E_k| / (256 L_k) > 2^14 with L_k < 2^31).  c_k grows with E_k, so a block
+// whose largest E_k gives c_k = 0 for some edge, or whose smallest E_k give
+// c_k = 1 for every edge, has no fragment and is skipped.
+__device__ void aa_pieces(const RenderParams& P, WaveLds& L, uint32_t* fbo, const Tile& T, bool ok, int ax, int ay,
+                          int bx, int by, int cx, int cy, float pa, float pb, float pc, uint32_t cls)
+{
+    const int lane = lane_id(), lx = lane & 7, ly = lane >> 3;
+    int i0 = 0, i1 = -1, j0 = 0, j1 = -1;
+    int dxs[3] = {0, 0, 0}, dys[3] = {0, 0, 0};
+    long long e0[3] = {0, 0, 0};
+    float rden[3] = {0.0f, 0.0f, 0.0f};
+    bool small = false;
+    if (ok) {
+        const long long area2 = (long long)(bx - ax) * (long long)(cy - ay) - (long long)(by - ay) * (long long)(cx - ax);
+        if (area2 < 0) {
+            const int tx = bx, ty = by;
+            bx = cx; by = cy; cx = tx; cy = ty;
+        }
+        const int minX = min(ax, min(bx, cx)), maxX = max(ax, max(bx, cx));
+        const int minY = min(ay, min(by, cy)), maxY = max(ay, max(by, cy));
+        i0 = max((minX - 384 + 255) >> 8, T.x0) - T.x0; i1 = min((maxX + 128) >> 8, T.x0 + T.w - 1) - T.x0;
+        j0 = max((minY - 384 + 255) >> 8, T.y0) - T.y0; j1 = min((maxY + 128) >> 8, T.y0 + T.h - 1) - T.y0;
+        ok = area2 != 0 && i0 <= i1 && j0 <= j1;
+        small = ok && (maxX - minX) < 16384 && (maxY - minY) < 16384 && (i1 - i0 + 1) * (j1 - j0 + 1) <= kAaSmall;
+        // edge functions at the window's first pixel (small) or at the tile's
+        const int px0 = 256 * (T.x0 + (small ? i0 : 0)) + 128, py0 = 256 * (T.y0 + (small ? j0 : 0)) + 128;
+        const int ex[3] = {bx, cx, ax}, ey[3] = {by, cy, ay};
+        const int fx[3] = {cx, ax, bx}, fy[3] = {cy, ay, by};
+#pragma unroll
+        for (int k = 0; k < 3; ++k) {
+            const int dx = fx[k] - ex[k], dy = fy[k] - ey[k];
+            e0[k] = (long long)dx * (long long)(py0 - ey[k]) - (long long)dy * (long long)(px0 - ex[k]);
+            dxs[k] = dx;
+            dys[k] = dy;
+            const float len = sqrtf((float)((long long)dx * dx + (long long)dy * dy));
+            rden[k] = 1.0f / (256.0f * len);
+        }
+    }
+    if (__ballot(small) != 0) {
+        const int e[3] = {(int)e0[0], (int)e0[1], (int)e0[2]};
+        const int sa[3] = {-256 * dys[0], -256 * dys[1], -256 * dys[2]};
+        const int sb[3] = {256 * dxs[0], 256 * dxs[1], 256 * dxs[2]};
+        aa_packed(P, L, fbo, T, small, i0, j0, i1 - i0 + 1, (i1 - i0 + 1) * (j1 - j0 + 1), e, sa, sb, rden, pa, pb, pc,
+                  cls);
+    }
+    uint64_t m = __ballot(ok && !small);
+    while (m) {
+        const int l = __builtin_ctzll(m);
+        m &= m - 1;
+        const int ri0 = (int)readlane((uint32_t)i0, l), ri1 = (int)readlane((uint32_t)i1, l);
+        const int rj0 = (int)readlane((uint32_t)j0, l), rj1 = (int)readlane((uint32_t)j1, l);
+        double re[3], rsx[3], rsy[3];
+        float rr[3];
+#pragma unroll
+        for (int k = 0; k < 3; ++k) {
+            const unsigned long long u = (unsigned long long)e0[k];
+            re[k] = (double)(long long)(((unsigned long long)readlane((uint32_t)(u >> 32), l) << 32) |
+                                        readlane((uint32_t)u, l));
+            rsx[k] = -256.0 * (double)(int)readlane((uint32_t)dys[k], l);
+            rsy[k] = 256.0 * (double)(int)readlane((uint32_t)dxs[k], l);
+            rr[k] = readlane_f(rden[k], l);
+        }
+        const float rpa = readlane_f(pa, l), rpb = readlane_f(pb, l), rpc = readlane_f(pc, l);
+        const uint32_t rcls = readlane(cls, l);
+        const int nbx = (ri1 - ri0 + 8) >> 3, nby = (rj1 - rj0 + 8) >> 3;   // at most 8 x 8 blocks
+        uint64_t bm = 1;
+        if (nbx * nby > 1) {
+            // lane = block (lx, ly) of the window: does it hold a fragment?
+            bool need = false;
+            if (lx < nbx && ly < nby) {
+                const int bi0 = ri0 + 8 * lx, bi1 = min(bi0 + 7, ri1);
+                const int bj0 = rj0 + 8 * ly, bj1 = min(bj0 + 7, rj1);
+                bool out = false, in = true;
+#pragma unroll
+                for (int k = 0; k < 3; ++k) {
+                    const double emax = fma(rsy[k], (double)(rsy[k] > 0.0 ? bj1 : bj0),
+                                            fma(rsx[k], (double)(rsx[k] > 0.0 ? bi1 : bi0), re[k]));
+                    const double emin = fma(rsy[k], (double)(rsy[k] > 0.0 ? bj0 : bj1),
+                                            fma(rsx[k], (double)(rsx[k] > 0.0 ? bi0 : bi1), re[k]));
+                    out = out || aa_cover(emax, rr[k]) == 0.0f;
+                    in = in && aa_cover(emin, rr[k]) == 1.0f;
+                }
+                need = !out && !in;
+            }
+            bm = __ballot(need);
+        }
+        while (bm) {
+            const int b = __builtin_ctzll(bm);
+            bm &= bm - 1;
+            const int i = ri0 + 8 * (b & 7) + lx, j = rj0 + 8 * (b >> 3) + ly;   // tile pixel
+            if (i > ri1 || j > rj1) continue;
+            const double di = (double)i, dj = (double)j;
+            const uint32_t f = aa_fragment(P, aa_cover(fma(rsy[0], dj, fma(rsx[0], di, re[0])), rr[0]),
+                                           aa_cover(fma(rsy[1], dj, fma(rsx[1], di, re[1])), rr[1]),
+                                           aa_cover(fma(rsy[2], dj, fma(rsx[2], di, re[2])), rr[2]),
+                                           ((float)(T.x0 + i) + 0.5f) - P.cx, ((float)(T.y0 + j) + 0.5f) - P.cy, rpa,
+                                           rpb, rpc, rcls);
+            atomicMin(&fbo[j * 64 + i], f);
+        }
+    }
+}
+
+template <bool kAA>
 __device__ __forceinline__ void exact_pass(const RenderParams& P, Shared& S, WaveLds& L, const Tile& T, const Cam& cam,
                                            bool live, uint32_t entry, int64_t abase_w, int64_t lbase_w, float pxl,
-                                           float pyl, int loff4)
+                                           float pyl, int loff4, uint32_t* fbo)
 {
     float tri[9] = {};
     uint32_t cls = 0;
@@ -838,6 +1037,7 @@ __device__ __forceinline__ void exact_pass(const RenderParams& P, Shared& S, Wav
                 }
             }
         }
+        if constexpr (kAA) aa_pieces(P, L, fbo, T, f + 2 < np, ax, ay, bx, by, cx, cy, pa, pb, pc, cls);
         // edge setup: edges v1->v2, v2->v0, v0->v1 at the tile's pixel (0, 0),
         // in the int32 form (floor(c / 256), -dy, dx) when every value fits
         uint32_t rv[12] = {0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
@@ -1166,13 +1366,21 @@ __device__ void draw_box_instances(const RenderParams& P, Shared& S, InstLds& I,
 
 struct NoInstLds {};
 
-// kInst: the instance variant (its LDS admits two waves per SIMD, so it may use
-// twice the registers)
-template <bool kInst>
-__global__ __launch_bounds__(kThreads, kInst ? 2 : kWavesPerSimd) void render_views_kernel(const RenderParams P)
+// Colour antialiasing (R14): the edge buffer, the nearest partial-coverage
+// fragment of every pixel.
+struct alignas(16) AaLds {
+    uint32_t fbo[64 * 64];   // tile pixel (i, j) at j * 64 + i; 0xFFFFFFFF none
+};
+
+// kMode 0: class and depth (and colour without antialiasing); 1: the
+// instance variant; 2: colour with antialiasing.  The variants' LDS admits
+// two waves per SIMD, so they may use twice the registers.
+template <int kMode>
+__global__ __launch_bounds__(kThreads, kMode != 0 ? 2 : kWavesPerSimd) void render_views_kernel(const RenderParams P)
 {
+    constexpr bool kInst = kMode == 1, kAA = kMode == 2;
     __shared__ Shared S;
-    __shared__ typename std::conditional<kInst, InstLds, NoInstLds>::type I;
+    __shared__ typename std::conditional<kInst, InstLds, typename std::conditional<kAA, AaLds, NoInstLds>::type>::type I;
     const int tid = threadIdx.x, lane = lane_id(), wid = tid >> 6;
     WaveLds& L = S.wv[wid];
     TSTART(t_kernel);
@@ -1206,10 +1414,14 @@ __global__ __launch_bounds__(kThreads, kInst ? 2 : kWavesPerSimd) void render_vi
     T.w = min(P.tile_w, P.W - T.x0);
     T.h = min(P.tile_h, P.H - T.y0);
     T.pitch = ((T.w + 31) & ~31) + 4;
-    T.kl = ((float)T.x0 - 0.5f) - P.cx;
-    T.kr = ((float)(T.x0 + T.w) + 0.5f) - P.cx;
-    T.kt = P.cy - ((float)T.y0 - 0.5f);
-    T.kb = P.cy - ((float)(T.y0 + T.h) + 0.5f);
+    // culling reaches the pixel centres of the tile, and with antialiasing the
+    // centres within one more pixel, where a surface's edge fragments land
+    constexpr float tpad = kAA ? 1.5f : 0.5f;
+    T.kl = ((float)T.x0 - tpad) - P.cx;
+    T.kr = ((float)(T.x0 + T.w) + tpad) - P.cx;
+    T.kt = P.cy - ((float)T.y0 - tpad);
+    T.kb = P.cy - ((float)(T.y0 + T.h) + tpad);
+    T.cm = kAA ? 1.00390625f : 0.00390625f;
     const int npx = T.w * T.h;
     static_assert(sizeof(Shared) <= 65536, "LDS");
     const bool cull = P.cull != 0;
@@ -1227,6 +1439,9 @@ __global__ __launch_bounds__(kThreads, kInst ? 2 : kWavesPerSimd) void render_vi
     if (tid < 4) S.ctl[tid] = 0;
     if constexpr (kInst) {
         for (int p = tid; p < 64 * 64; p += kThreads) I.inst[p] = 0xFFFFFFFFu;
+    }
+    if constexpr (kAA) {
+        for (int p = tid; p < 64 * 64; p += kThreads) I.fbo[p] = 0xFFFFFFFFu;
     }
 
     // world-space frustum planes of the tile: four side planes through the
@@ -1466,7 +1681,9 @@ __global__ __launch_bounds__(kThreads, kInst ? 2 : kWavesPerSimd) void render_vi
             __builtin_amdgcn_wave_barrier();
             STAT1(kStExact, 1);
             TSTART(t_ex);
-            exact_pass(P, S, L, T, cam, live, entry, abase_w, lbase_w, pxl, pyl, loff4);
+            uint32_t* fbo = nullptr;
+            if constexpr (kAA) fbo = I.fbo;
+            exact_pass<kAA>(P, S, L, T, cam, live, entry, abase_w, lbase_w, pxl, pyl, loff4, fbo);
             TACC(kCycExact, t_ex);
         }
         if (phase == kDone && nq == 0) break;
@@ -1616,6 +1833,18 @@ __global__ __launch_bounds__(kThreads, kInst ? 2 : kWavesPerSimd) void render_vi
             const uint32_t key = S.fb[row * T.pitch + col];
             uint32_t c3[3];
             shade_rgb(P, key, c3);
+            if constexpr (kAA) {
+                // R14: a partial-coverage fragment not behind the centre's surface and
+                // of another shading id blends over it
+                const uint32_t ko = I.fbo[row * 64 + col];
+                if (ko != 0xFFFFFFFFu && (ko >> 16) <= (key >> 16) && ((ko >> 8) & 255u) != (key & 255u)) {
+                    uint32_t o3[3];
+                    shade_rgb(P, ((ko >> 16) << 16) | ((ko >> 8) & 255u), o3);
+                    const uint32_t a8 = 255u - (ko & 255u);
+#pragma unroll
+                    for (int c = 0; c < 3; ++c) c3[c] = (o3[c] * a8 + c3[c] * (255u - a8) + 127u) / 255u;
+                }
+            }
             const int64_t o = (int64_t)(T.y0 + row) * P.W + T.x0 + col;
             rgb[o] = (uint8_t)c3[0];
             rgb[view_px + o] = (uint8_t)c3[1];
@@ -1632,8 +1861,9 @@ __global__ __launch_bounds__(kThreads, kInst ? 2 : kWavesPerSimd) void render_vi
 hipError_t launch_render(const RenderParams& p, hipStream_t s)
 {
     if (p.num_blocks <= 0) return hipSuccess;
-    if (p.out_inst) hipLaunchKernelGGL(render_views_kernel<true>, dim3((unsigned)p.num_blocks), dim3(kThreads), 0, s, p);
-    else hipLaunchKernelGGL(render_views_kernel<false>, dim3((unsigned)p.num_blocks), dim3(kThreads), 0, s, p);
+    if (p.out_inst) hipLaunchKernelGGL(render_views_kernel<1>, dim3((unsigned)p.num_blocks), dim3(kThreads), 0, s, p);
+    else if (p.out_rgb && p.aa) hipLaunchKernelGGL(render_views_kernel<2>, dim3((unsigned)p.num_blocks), dim3(kThreads), 0, s, p);
+    else hipLaunchKernelGGL(render_views_kernel<0>, dim3((unsigned)p.num_blocks), dim3(kThreads), 0, s, p);
     return hipGetLastError();
 }
 

@@ -87,6 +87,8 @@ _lib.pictura_stats_copy.argtypes = [_P, _P, ctypes.c_int32, ctypes.c_int32]
 _lib.pictura_stats_copy.restype = ctypes.c_int32
 _lib.pictura_render_rgb.argtypes = [_P, ctypes.POINTER(_Agents), ctypes.POINTER(_Rig), _P, _P, _P, _P]
 _lib.pictura_render_rgb.restype = ctypes.c_int32
+_lib.pictura_render_rgb_aa.argtypes = [_P, ctypes.POINTER(_Agents), ctypes.POINTER(_Rig), _P, _P, _P, _P]
+_lib.pictura_render_rgb_aa.restype = ctypes.c_int32
 _lib.pictura_render_instances.argtypes = [_P, ctypes.POINTER(_Agents), ctypes.POINTER(_Rig), _P, _P, _P, _P, _P]
 _lib.pictura_render_instances.restype = ctypes.c_int32
 _lib.pictura_set_lights.argtypes = [_P, ctypes.POINTER(_Lights)]
@@ -97,7 +99,7 @@ _lib.pictura_selftest_rcp.restype = ctypes.c_int32
 EXPORTED = ["pictura_create", "pictura_destroy", "pictura_last_error", "pictura_scene_upload",
             "pictura_bin_scene", "pictura_render_views", "pictura_agents_step", "pictura_bins_info",
             "pictura_bins_copy", "pictura_set_option", "pictura_stats_copy", "pictura_selftest_rcp",
-            "pictura_set_lights", "pictura_render_instances", "pictura_render_rgb"]
+            "pictura_set_lights", "pictura_render_instances", "pictura_render_rgb", "pictura_render_rgb_aa"]
 
 STAT_NAMES = ["view_tiles", "cells_in_rect", "cells_prefiltered", "cells_visible", "cand_tris", "boxes_visible",
               "box_tris", "first_pass_survivors", "exact_batches", "clipped", "raster_tris", "lane_tris",
@@ -194,6 +196,16 @@ def pictura_render_rgb(ctx, agents, rig, out_cls, out_depth, out_rgb, stream=Non
     r = make_rig(rig) if not isinstance(rig, _Rig) else rig
     _check(ctx, _lib.pictura_render_rgb(ctx, ctypes.byref(a), ctypes.byref(r), _ptr(out_cls), _ptr(out_depth),
                                         _ptr(out_rgb), _stream(stream)))
+
+
+def pictura_render_rgb_aa(ctx, agents, rig, out_cls, out_depth, out_rgb, stream=None):
+    """As pictura_render_rgb, with analytic-coverage antialiasing of out_rgb."""
+    a = _Agents(int(agents.num_worlds), int(agents.agents_per_world),
+                *[_ptr(getattr(agents, n)) for n in ("x", "y", "z0", "cos_h", "sin_h", "length", "width", "height",
+                                                     "cls")])
+    r = make_rig(rig) if not isinstance(rig, _Rig) else rig
+    _check(ctx, _lib.pictura_render_rgb_aa(ctx, ctypes.byref(a), ctypes.byref(r), _ptr(out_cls), _ptr(out_depth),
+                                           _ptr(out_rgb), _stream(stream)))
 
 
 def pictura_render_instances(ctx, agents, rig, out_cls, out_depth, out_inst, out_counts, stream=None):
@@ -345,8 +357,8 @@ class Renderer:
         pictura_render_views(self.ctx, agents, rig, out_cls, out_depth, stream)
         return out_cls, out_depth
 
-    def render_rgb(self, agents: DeviceAgents, rig, stream=None):
-        """Returns (cls, depth, rgb) with rgb [V, 3, H, W] uint8."""
+    def render_rgb(self, agents: DeviceAgents, rig, stream=None, antialias=False):
+        """Returns (cls, depth, rgb) with rgb [V, 3, H, W] uint8 (antialiased when asked)."""
         import torch
         V = agents.num_worlds * agents.agents_per_world * int(rig.mount.shape[0])
         H, W = int(rig.height), int(rig.width)
@@ -354,7 +366,8 @@ class Renderer:
         out_cls = torch.empty((V, H, W), dtype=torch.uint8, device=dev)
         out_depth = torch.empty((V, H, W), dtype=torch.float32, device=dev)
         out_rgb = torch.empty((V, 3, H, W), dtype=torch.uint8, device=dev)
-        pictura_render_rgb(self.ctx, agents, rig, out_cls, out_depth, out_rgb, stream)
+        fn = pictura_render_rgb_aa if antialias else pictura_render_rgb
+        fn(self.ctx, agents, rig, out_cls, out_depth, out_rgb, stream)
         return out_cls, out_depth, out_rgb
 
     def render_instances(self, agents: DeviceAgents, rig, stream=None):

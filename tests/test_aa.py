@@ -1,0 +1,171 @@
+"""Oracle pins for the antialiased colour mode (rule R14): analytic coverage of
+the pixels a surface's edges cross, at one sample per pixel (Sec. 3.2,
+rendering features; the appendix on render quality: thin structures such as
+lane lines stay visible at low resolution).
+
+The scenes are vertical walls 16 m in front of a camera with f = 64 px on a
+64x64 image, placed so that every projected vertex is exact in fp32 and on
+the subpixel grid: a world point (16, y, z) lands at x = 32 - 4 y, y_img =
+32 - 4 z.  Expected values come from the geometry (pixel areas, strip
+widths), not from the rule's arithmetic."""
+import numpy as np
+
+from oracle import oracle as O
+from tests.scenes import make_agents, make_rig, make_scene, quad
+
+WALL, LANE, SKY = 7, 2, 4
+PAL = {WALL: (168, 144, 120), LANE: (232, 232, 224), SKY: (140, 184, 232)}
+D = 16.0
+
+
+def _y(px):   # world y of projected column px at depth D
+    return (32.0 - px) / 4.0
+
+
+def _z(py):   # world z of projected row py at depth D
+    return (32.0 - py) / 4.0
+
+
+def _render(tris, cls, antialias=True, want_flags=False):
+    sc = make_scene(np.asarray(tris, np.float32), cls)
+    ag = make_agents([(0.0, 0.0, 0.0, 1.0, 0.0, 4.5, 1.9, 1.5, 3)])
+    rig = make_rig(res=64, f=64.0, mounts=((0.0, 0.0, 0.0, 1.0, 0.0),))
+    return O.render(sc, ag, rig, view_ids=[0], want_rgb=True, antialias=antialias, want_flags=want_flags)
+
+
+def _blend(fg, bg, a8):
+    return tuple((f * a8 + b * (255 - a8) + 127) // 255 for f, b in zip(fg, bg))
+
+
+def _wall(px_left, x=D, px_right=432.0):
+    """A wall whose left edge projects to column px_left (rows far off-screen)."""
+    s = D / x
+    yl, yr = (32.0 - px_left) / 4.0 / s, (32.0 - px_right) / 4.0 / s
+    zt, zb = _z(-200.0) / s, _z(300.0) / s
+    return quad((x, yl, zb), (x, yr, zb), (x, yr, zt), (x, yl, zt))
+
+
+def test_vertical_edge_blends_its_pixel_area():
+    # left edge at x = 10.75: pixel 10 ([10, 11]) is a quarter covered and its
+    # centre (10.5) is not, so it shows sky with a quarter of the wall over it
+    o = _render(_wall(10.75), [WALL, WALL])
+    rgb = o["rgb"][0]
+    assert (o["cls"][0][:, 10] == SKY).all() and (o["cls"][0][:, 11] == WALL).all()
+    want = _blend(PAL[WALL], PAL[SKY], 64)    # rint(255 * 0.25)
+    assert all(tuple(rgb[:, j, 10]) == want for j in range(64)), rgb[:, :, 10].T[:4]
+    assert (rgb[:, :, 11:] == np.asarray(PAL[WALL], np.uint8)[:, None, None]).all()
+    assert (rgb[:, :, :10] == np.asarray(PAL[SKY], np.uint8)[:, None, None]).all()
+    # without antialiasing the column is plain sky
+    p = _render(_wall(10.75), [WALL, WALL], antialias=False)
+    assert (p["rgb"][0][:, :, 10] == np.asarray(PAL[SKY], np.uint8)[:, None]).all()
+
+
+def test_edge_covering_the_centre_keeps_the_surface_colour():
+    # left edge at x = 10.25: pixel 10 is three quarters covered, centre inside;
+    # the wall's own fragment does not blend (one sample decides the surface)
+    o = _render(_wall(10.25), [WALL, WALL])
+    assert (o["rgb"][0][:, :, 10:] == np.asarray(PAL[WALL], np.uint8)[:, None, None]).all()
+    assert (o["rgb"][0][:, :, :10] == np.asarray(PAL[SKY], np.uint8)[:, None, None]).all()
+
+
+def _sliver(xl_top, xr_top, x_bot, x=D):
+    """A tall wedge between rows -200 (top, columns xl_top..xr_top) and 300
+    (apex at column x_bot)."""
+    s = D / x
+    return [[(x, _y(xl_top) / s, _z(-200.0) / s), (x, _y(x_bot) / s, _z(300.0) / s),
+             (x, _y(xr_top) / s, _z(-200.0) / s)]]
+
+
+XL, XR, XB = 5274 / 256, 5350 / 256, 20.75   # 20.6015625, 20.8984375
+
+
+def _sliver_width(j):
+    t = (j + 0.5 + 200.0) / 500.0
+    return (XR + (XB - XR) * t) - (XL + (XB - XL) * t)
+
+
+def test_sub_pixel_sliver_shows_with_its_width():
+    # the wedge covers no pixel centre (its columns stay within (20.5, 21.5)),
+    # yet pixel 20 holds it with coverage equal to its width in that row
+    o = _render(_sliver(XL, XR, XB), [LANE])
+    assert (o["cls"][0] == SKY).all()
+    rgb = o["rgb"][0]
+    for j in range(64):
+        a = int(np.rint(255.0 * _sliver_width(j)))
+        ok = [_blend(PAL[LANE], PAL[SKY], a + d) for d in (-1, 0, 1)]
+        assert tuple(rgb[:, j, 20]) in ok, (j, tuple(rgb[:, j, 20]), ok[1])
+    assert tuple(rgb[:, 0, 20]) != tuple(rgb[:, 63, 20])   # the width changes down the image
+    mask = np.ones((64, 64), bool)
+    mask[:, 20] = False
+    assert (rgb[:, mask] == np.asarray(PAL[SKY], np.uint8)[:, None]).all()
+    # one sample per pixel loses it entirely
+    p = _render(_sliver(XL, XR, XB), [LANE], antialias=False)
+    assert (p["rgb"][0] == np.asarray(PAL[SKY], np.uint8)[:, None, None]).all()
+
+
+def test_sliver_in_front_of_a_wall_blends_over_the_wall():
+    o = _render(_sliver(XL, XR, XB, x=12.0) + _wall(0.0), [LANE, WALL, WALL])
+    rgb = o["rgb"][0]
+    for j in (0, 31, 63):
+        a = int(np.rint(255.0 * _sliver_width(j)))
+        ok = [_blend(PAL[LANE], PAL[WALL], a + d) for d in (-1, 0, 1)]
+        assert tuple(rgb[:, j, 20]) in ok, (j, tuple(rgb[:, j, 20]))
+
+
+def test_sliver_behind_a_wall_is_hidden():
+    # a fragment farther than the centre's surface does not blend
+    o = _render(_sliver(XL, XR, XB, x=24.0) + _wall(0.0), [LANE, WALL, WALL])
+    assert (o["rgb"][0] == np.asarray(PAL[WALL], np.uint8)[:, None, None]).all()
+
+
+def test_nearest_fragment_wins():
+    # two slivers over the same pixel column at 12 m and 14 m, sky behind:
+    # the nearer one (wall class) is the one blended
+    near = _sliver(XL, XR, XB, x=12.0)
+    far_ = _sliver(XL, XR, XB, x=14.0)
+    o = _render(far_ + near, [LANE, WALL])
+    rgb = o["rgb"][0]
+    for j in (0, 63):
+        a = int(np.rint(255.0 * _sliver_width(j)))
+        ok = [_blend(PAL[WALL], PAL[SKY], a + d) for d in (-1, 0, 1)]
+        assert tuple(rgb[:, j, 20]) in ok
+
+
+def test_classes_and_depth_match_one_sample_mode():
+    rng = np.random.default_rng(9)
+    tris = rng.uniform([4.0, -12.0, -4.0], [40.0, 12.0, 6.0], size=(60, 3, 3)).astype(np.float32)
+    cls = rng.integers(0, 11, size=60)
+    sc = make_scene(tris, cls)
+    rows = [(0.0, 0.0, 0.0, 1.0, 0.0, 4.5, 1.9, 1.5, 3)]
+    for k in range(4):
+        rows.append((rng.uniform(6, 30), rng.uniform(-8, 8), 0.0, 1.0, 0.0, 4.5, 1.9, 1.5, 3 if k % 2 else 6))
+    ag = make_agents(rows)
+    rig = make_rig(res=64, mounts=((0.0, 0.0, 1.5, 1.0, 0.0),))
+    a = O.render(sc, ag, rig, view_ids=[0], want_rgb=True, antialias=True)
+    b = O.render(sc, ag, rig, view_ids=[0], want_rgb=True, antialias=False)
+    assert np.array_equal(a["cls"], b["cls"]) and np.array_equal(a["depth"], b["depth"])
+    changed = (a["rgb"][0] != b["rgb"][0]).any(0)
+    assert 0 < changed.sum() < 0.5 * changed.size
+    # a changed pixel lies within one pixel of a change of shading in the one-sample image
+    c = b["rgb"][0].astype(np.int32)
+    edge = np.zeros((64, 64), bool)
+    for dy in (-1, 0, 1):
+        for dx in (-1, 0, 1):
+            sh = np.roll(np.roll(c, dy, 1), dx, 2)
+            edge |= (sh != c).any(0)
+    frac = (changed & edge).sum() / changed.sum()
+    assert frac > 0.9, frac
+
+
+def test_coplanar_neighbours_blend_across_their_shared_edge():
+    # two walls in one plane meeting at x = 10.75: pixel 10 is three quarters
+    # wall (its centre's surface) and one quarter lane marking
+    left = quad((D, _y(-400.0), _z(300.0)), (D, _y(10.75), _z(300.0)), (D, _y(10.75), _z(-200.0)),
+                (D, _y(-400.0), _z(-200.0)))
+    o = _render(left + _wall(10.75), [WALL, WALL, LANE, LANE])
+    rgb = o["rgb"][0]
+    assert (o["cls"][0][:, 10] == WALL).all() and (o["cls"][0][:, 11] == LANE).all()
+    want = _blend(PAL[LANE], PAL[WALL], 64)
+    assert all(tuple(rgb[:, j, 10]) == want for j in range(64))
+    assert (rgb[:, :, 11:] == np.asarray(PAL[LANE], np.uint8)[:, None, None]).all()
+    assert (rgb[:, :, :10] == np.asarray(PAL[WALL], np.uint8)[:, None, None]).all()

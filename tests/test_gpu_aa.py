@@ -1,0 +1,121 @@
+"""GPU parity of the antialiased colour mode (rule R14) against the oracle:
+classes and depth as in the plain mode, colour bytes bit-exact wherever the
+oracle does not flag the pixel (EDGE / TIE), at most 1e-4 of the pixels
+different; the hand-built coverage scenes of the oracle pins bit-exact."""
+import functools
+
+import numpy as np
+import pytest
+
+from oracle import oracle as O
+from paper_2607_26005_amd import scenegen as sg
+from tests.parity import assert_parity
+from tests.scenes import make_agents, make_rig, make_scene, quad
+from tests import test_aa as pins
+
+pytestmark = pytest.mark.gpu
+
+
+def _torch():
+    import torch
+    if not torch.cuda.is_available():
+        pytest.skip("no HIP device")
+    return torch
+
+
+@pytest.fixture(scope="module")
+def lib():
+    _torch()
+    from paper_2607_26005_amd import pictura
+    return pictura
+
+
+@functools.lru_cache(maxsize=None)
+def workload(cfg, worlds=None):
+    return sg.make_config(cfg, num_worlds=worlds)
+
+
+def gpu_render(lib, scene, cell, agents, rig, lights=None, tile=0, cull=1, antialias=True):
+    torch = _torch()
+    r = lib.Renderer(0)
+    try:
+        r.set_option(lib.OPT_TILE, tile)
+        r.set_option(lib.OPT_CULL, cull)
+        r.upload(scene, cell)
+        if lights is not None:
+            r.set_lights(lib.DeviceLights.from_host(lights))
+        da = lib.DeviceAgents.from_host(agents)
+        c, d, rgb = r.render_rgb(da, rig, antialias=antialias)
+        torch.cuda.synchronize()
+        return c, d, rgb
+    finally:
+        r.close()
+
+
+def check(lib, wl, views, label, tile=0, cull=1):
+    torch = _torch()
+    print(f"[{label}] {wl.num_views} views tile={tile} cull={cull}", flush=True)
+    c, d, rgb = gpu_render(lib, wl.scene, wl.cell_size, wl.agents, wl.rig, wl.lights, tile, cull)
+    idx = torch.as_tensor(np.asarray(views), device="cuda")
+    gc, gd, grgb = c[idx].cpu().numpy(), d[idx].cpu().numpy(), rgb[idx].cpu().numpy()
+    ora = O.render(wl.scene, wl.agents, wl.rig, view_ids=np.asarray(views), lights=wl.lights, want_rgb=True,
+                   antialias=True)
+    s = assert_parity(gc, gd, ora, label)
+    unflag = ora["flags"] == 0
+    diff = (grgb != ora["rgb"]).any(1)
+    assert not (diff & unflag).any(), (label, int((diff & unflag).sum()), np.argwhere(diff & unflag)[:5])
+    assert diff.sum() <= 1e-4 * diff.size, (label, int(diff.sum()))
+    plain = O.render(wl.scene, wl.agents, wl.rig, view_ids=np.asarray(views), lights=wl.lights, want_rgb=True,
+                     want_flags=False)
+    blended = int((ora["rgb"] != plain["rgb"]).any(1).sum())
+    print(f"[{label}] {s} colour mismatches {int(diff.sum())}, blended px {blended}", flush=True)
+    return blended
+
+
+def test_aa_pin_scenes_bit_exact(lib):
+    ag = make_agents([(0.0, 0.0, 0.0, 1.0, 0.0, 4.5, 1.9, 1.5, 3)])
+    rig = make_rig(res=64, f=64.0, mounts=((0.0, 0.0, 0.0, 1.0, 0.0),))
+    left = quad((16.0, pins._y(-400.0), pins._z(300.0)), (16.0, pins._y(10.75), pins._z(300.0)),
+                (16.0, pins._y(10.75), pins._z(-200.0)), (16.0, pins._y(-400.0), pins._z(-200.0)))
+    scenes = {
+        "edge": (pins._wall(10.75), [7, 7]),
+        "sliver": (pins._sliver(pins.XL, pins.XR, pins.XB), [2]),
+        "sliver-front": (pins._sliver(pins.XL, pins.XR, pins.XB, x=12.0) + pins._wall(0.0), [2, 7, 7]),
+        "sliver-behind": (pins._sliver(pins.XL, pins.XR, pins.XB, x=24.0) + pins._wall(0.0), [2, 7, 7]),
+        "coplanar": (left + pins._wall(10.75), [7, 7, 2, 2]),
+    }
+    for name, (tris, cls) in scenes.items():
+        sc = make_scene(np.asarray(tris, np.float32), cls)
+        ora = O.render(sc, ag, rig, view_ids=[0], want_rgb=True, antialias=True)
+        for tile in (0, 16):
+            c, d, rgb = gpu_render(lib, sc, 64.0, ag, rig, tile=tile)
+            print(f"[aa-pin {name} tile={tile}]", flush=True)
+            assert np.array_equal(c.cpu().numpy(), ora["cls"]), name
+            assert np.array_equal(rgb.cpu().numpy(), ora["rgb"]), (name, tile)
+
+
+def test_aa_tiny_all_views(lib):
+    wl = workload(1)
+    assert check(lib, wl, np.arange(wl.num_views), "aa-tiny") > 0
+
+
+def test_aa_dense_traffic_sampled(lib):
+    wl = workload(3, 4)
+    views = np.sort(np.random.default_rng(61).choice(wl.num_views, size=96, replace=False))
+    assert check(lib, wl, views, "aa-dense") > 0
+
+
+def test_aa_town_paper_rig_tiles_and_unculled(lib):
+    wl = workload(7, 2)   # two tiles per view, walls, parked cars, lights
+    views = np.sort(np.random.default_rng(62).choice(wl.num_views, size=64, replace=False))
+    assert check(lib, wl, views, "aa-town") > 0
+    check(lib, wl, views, "aa-town-tile24", tile=24)
+    check(lib, wl, views[:16], "aa-town-unculled", cull=0)
+
+
+def test_aa_leaves_classes_and_depth_alone(lib):
+    wl = workload(2, 1)
+    c1, d1, _ = gpu_render(lib, wl.scene, wl.cell_size, wl.agents, wl.rig, antialias=True)
+    c0, d0, _ = gpu_render(lib, wl.scene, wl.cell_size, wl.agents, wl.rig, antialias=False)
+    assert np.array_equal(c1.cpu().numpy(), c0.cpu().numpy())
+    assert np.array_equal(d1.cpu().numpy().view(np.uint32), d0.cpu().numpy().view(np.uint32))
