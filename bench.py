@@ -41,7 +41,7 @@ HBM_PEAK_GBS = 8000.0   # MI355X HBM3E peak
 # measured on; when the fingerprint differs, `traffic` is reported as null.
 TRAFFIC = {
     "config": 4,
-    "sources_sha256": "ee09d9aa0575a8f0a3b3d4865e15053afb6ab07af21ab8b3de91c7fa0d524c7f",
+    "sources_sha256": "c02b4b5c9d54fcaa8b1954f9eceb90b34a665b6578acdab0f7721279c07d1d03",
     "fetch_bytes": 1.4667e9,
     "write_bytes": 5368709120,
 }

@@ -613,7 +613,9 @@ __device__ __forceinline__ void raster_blocks(const RenderParams& P, Shared& S, 
     }
     // lane b: block b of the box
     const int eby = (int)(((uint32_t)lane * rinv) >> 16), ebx = lane - eby * nbx;
-    const int X = (bx0 + ebx) * 8, Y = (by0 + eby) * 8;
+    // (lanes past the box hold no block; the masks keep X and Y below 64, so the
+    // products below stay 24-bit multiplies)
+    const int X = ((bx0 + ebx) & 7) * 8, Y = ((by0 + eby) & 7) * 8;
     bool pass = lane < nb;
 #pragma unroll
     for (int k = 0; k < 3; ++k) {
