@@ -170,6 +170,27 @@ def test_empty_world_and_lone_agent(lib):
     check_views(lib, wl, np.arange(wl.num_views), "empty+lone")
 
 
+@pytest.mark.parametrize("s,lo,hi", [(1.875, 24, 39), (2.0, 24, 40), (1.87451171875, 24, 39), (1.87548828125, 24, 39)])
+def test_fill_rule_and_snap_ties_closed_form(lib, s, lo, hi):
+    # A square of half-size s facing the camera 8 m ahead (fx = 32): its edges
+    # project to 32 -+ 4 s px.  For s = 1.875 they run through pixel centres
+    # (top-left rule: left/top included, right/bottom excluded); the last two
+    # sizes put them half a subpixel off the centres, and the snap's ties to
+    # even move them onto the centres.  Closed-form pixel set and depth 8 m,
+    # and the oracle's images bit for bit.
+    pts = [(8.0, a, b) for (a, b) in ((-s, -s), (s, -s), (s, s), (-s, s))]
+    scene = make_scene(quad(*pts), [7, 7])
+    wl = sg.Workload("pin", 0, 0, scene, make_agents([(0.0, 0.0, 0.0, 1.0, 0.0, 1.0, 1.0, 1.0, 3)]), make_rig(),
+                     16.0, 2000.0)
+    c, d = render_gpu(lib, wl.scene, wl.agents, wl.rig, 16.0)
+    gc, gd = c.cpu().numpy()[0], d.cpu().numpy()[0]
+    want = np.zeros((64, 64), bool)
+    want[lo:hi, lo:hi] = True
+    assert np.array_equal(gc == 7, want)
+    assert np.all(np.isinf(gd[~want])) and np.allclose(gd[want], 8.0, rtol=2 ** -20, atol=0)
+    check_views(lib, wl, np.arange(1), f"pin s={s}")
+
+
 def test_camera_inside_box_and_near_clipped_ground(lib):
     G = 1000.0
     tris = quad((-G, -G, 0.0), (G, -G, 0.0), (G, G, 0.0), (-G, G, 0.0))

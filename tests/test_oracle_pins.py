@@ -36,11 +36,17 @@ def fronto_quad(D, s, h=0.0, cls=7, axis=0, sign=1.0, centre=(0.0, 0.0)):
 # P1: an axis-aligned quad at a known distance covers a known pixel set
 # ---------------------------------------------------------------------------
 
-@pytest.mark.parametrize("s,cols", [(1.875, range(24, 39)), (2.0, range(24, 40)), (1.0, range(28, 36))])
+@pytest.mark.parametrize("s,cols", [(1.875, range(24, 39)), (2.0, range(24, 40)), (1.0, range(28, 36)),
+                                    (1.87451171875, range(24, 39)), (1.87548828125, range(24, 39))])
 def test_fronto_quad_pixel_set_and_depth(s, cols):
     # D = 8, fx = 32: edges project to 32 +- 32*s/8 px.  For s = 1.875 they run
     # exactly through pixel centres 24.5 and 39.5: the left/top edges include
     # them, the right/bottom edges exclude them (top-left rule).
+    # The last two sizes put the edges half a subpixel off those centres (256 x
+    # = 6272.5 and 10111.5, then 6271.5 and 10112.5): the 8-bit snap rounds the
+    # ties to even, onto the centres, which gives the same pixel set; rounding
+    # ties upwards (or away from zero) would drop column and row 24 in the first
+    # case and add column and row 39 in the second.
     scene = make_scene(fronto_quad(8.0, s), [7, 7])
     r = O.render(scene, make_agents([ego()]), make_rig(), want_cover=True)
     cls, depth, cover = r["cls"][0], r["depth"][0], r["cover"][0]
