@@ -33,7 +33,10 @@
  *              each crossing point is computed from the inside vertex I
  *              towards the outside vertex O: t = (near - I.z)/(O.z - I.z),
  *              x = fma(t, O.x - I.x, I.x), y likewise, z = near; the 3- or
- *              4-gon is fanned from its first vertex.
+ *              4-gon is fanned from its first vertex.  (Parity unpinned: which
+ *              end the crossing point is computed from only changes its last
+ *              bits, and either choice is watertight; no closed form fixes it,
+ *              so only the GPU comparison checks that both sides agree.)
  *  R5 snap     rz = 1/zv;  X = rint(256cx + 256fx*(xv*rz)),
  *              Y = rint(256cy - 256fy*(yv*rz))   (8-bit subpixel, ties to
  *              even); a coordinate with |value| > 2^29 (or NaN) drops the
@@ -141,6 +144,23 @@ typedef struct {
     float izfar, izcap;
     uint32_t qbase;
 } Params;
+
+/* R7: 24-bit reverse-depth code of an inverse depth; 0 when the far rule
+ * rejects it (iz < 1/far or NaN), else 1 with *q set.  Depths nearer than the
+ * cap (iz > IZCAP) take the cap's code 0. */
+static int quantize_iz(const Params* P, float iz, uint32_t* q)
+{
+    if (!(iz >= P->izfar)) return 0;
+    if (iz > P->izcap) iz = P->izcap;
+    *q = P->qbase - (f2u(iz) >> 3);
+    return 1;
+}
+
+/* R8: depth of a code (the midpoint of its bucket of eight fp32 inverse depths). */
+static float decode_q(const Params* P, uint32_t q)
+{
+    return 1.0f / u2f(((P->qbase - q) << 3) | 4u);
+}
 
 typedef struct { float x, y, z; } V3;
 
@@ -270,9 +290,9 @@ static void coverage_fragments(const Params* P, Frame* F, const int32_t* vx, con
             float pxf = ((float)i + 0.5f) - P->cx;
             float pyf = ((float)j + 0.5f) - P->cy;
             float iz = fmaf(pa, pxf, fmaf(pb, pyf, pc));
-            if (!(iz >= P->izfar)) continue;
-            if (iz > P->izcap) iz = P->izcap;
-            uint32_t key = ((P->qbase - (f2u(iz) >> 3)) << 8) | cls;
+            uint32_t q;
+            if (!quantize_iz(P, iz, &q)) continue;
+            uint32_t key = (q << 8) | cls;
             uint32_t o = ((key >> 16) << 16) | ((key & 255u) << 8) | (255u - a8);
             int p = (int)(j * P->W + i);
             if (o < F->frag[p]) F->frag[p] = o;
@@ -329,9 +349,8 @@ static void raster_tri(const Params* P, Frame* F, int32_t X0, int32_t Y0, int32_
             if (!covered && !(near_edge && in_band)) continue;
             float pxf = ((float)i + 0.5f) - P->cx;
             float iz = fmaf(pa, pxf, fmaf(pb, pyf, pc));
-            if (!(iz >= P->izfar)) continue;
-            if (iz > P->izcap) iz = P->izcap;
-            uint32_t q = P->qbase - (f2u(iz) >> 3);
+            uint32_t q;
+            if (!quantize_iz(P, iz, &q)) continue;
             uint32_t key = (q << 8) | cls;
             int p = (int)(j * P->W + i);
             if (near_edge && in_band && key < F->edge_key[p] + 0u) {
@@ -420,7 +439,7 @@ static void shade(const Params* P, uint32_t key, uint8_t* c3)
     uint32_t cls = key & 15u, face = (key >> 4) & 7u, q = key >> 8;
     float f = FACE_FACTOR[face];
     if (face != 0u && q != 0xFFFFFFu) {
-        float z = 1.0f / u2f(((P->qbase - q) << 3) | 4u);
+        float z = decode_q(P, q);
         float rfar = 1.0f / P->farp;
         float t = z * rfar;
         if (t > 1.0f) t = 1.0f;
@@ -647,8 +666,7 @@ int oracle_render(int num_worlds, const int64_t* tri_offsets, const float* verts
                 if (q == 0xFFFFFFu) {
                     out_depth[n * npx + p] = INFINITY;
                 } else {
-                    float izd = u2f(((P.qbase - q) << 3) | 4u);
-                    out_depth[n * npx + p] = 1.0f / izd;
+                    out_depth[n * npx + p] = decode_q(&P, q);
                 }
                 if (out_flags) {
                     uint8_t fl = 0;
@@ -670,18 +688,17 @@ int oracle_render(int num_worlds, const int64_t* tri_offsets, const float* verts
     return 0;
 }
 
-/* R7/R8 quantizer exposed for exhaustive checks. */
+/* R7/R8 quantizer exposed for exhaustive checks: the same quantize_iz and
+ * decode_q that the renderer applies to every pixel. */
 void oracle_quantize(const float* iz, int64_t n, float nearp, float farp, uint32_t* q_out, float* depth_out)
 {
     Params P;
     init_params(&P, 1, 1, 1.0f, 1.0f, 0.5f, 0.5f, nearp, farp);
     for (int64_t k = 0; k < n; ++k) {
-        float z = iz[k];
-        if (!(z >= P.izfar)) { q_out[k] = 0xFFFFFFu; depth_out[k] = INFINITY; continue; }
-        if (z > P.izcap) z = P.izcap;
-        uint32_t q = P.qbase - (f2u(z) >> 3);
+        uint32_t q;
+        if (!quantize_iz(&P, iz[k], &q)) { q_out[k] = 0xFFFFFFu; depth_out[k] = INFINITY; continue; }
         q_out[k] = q;
-        depth_out[k] = 1.0f / u2f(((P.qbase - q) << 3) | 4u);
+        depth_out[k] = decode_q(&P, q);
     }
 }
 

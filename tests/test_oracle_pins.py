@@ -72,6 +72,98 @@ def test_fronto_quad_rotated_camera_and_mount():
     assert np.allclose(r["depth"][0][want], 8.0, rtol=2 ** -20)
 
 
+def test_anisotropic_intrinsics():
+    # fx = 32, fy = 16 on a 64x48 image (cx = 32, cy = 24): the square's
+    # edges project to 32 -+ 7.5 px across and 24 -+ 3.75 px down, so it
+    # covers columns 24..38 and rows 20..27 (centres 20.5 .. 27.5).
+    from paper_2607_26005_amd.scenegen import Rig
+    scene = make_scene(fronto_quad(8.0, 1.875), [7, 7])
+    rig = Rig(width=64, height=48, fx=32.0, fy=16.0, cx=32.0, cy=24.0, near=0.5, far=100.0,
+              mount=np.asarray([(0.0, 0.0, 0.0, 1.0, 0.0)], np.float32))
+    r = O.render(scene, make_agents([ego()]), rig)
+    want = np.zeros((48, 64), bool)
+    want[20:28, 24:39] = True
+    assert np.array_equal(r["cls"][0] == 7, want)
+    assert np.allclose(r["depth"][0][want], 8.0, rtol=2 ** -20)
+
+
+@pytest.mark.parametrize("heading,yaw,axis,sign", [((1.0, 0.0), (0.0, 1.0), 1, 1.0),    # 0 + 90 deg: faces +y
+                                                    ((0.0, 1.0), (0.0, 1.0), 0, -1.0),   # 90 + 90 deg: faces -x
+                                                    ((0.0, 1.0), (-1.0, 0.0), 1, -1.0)])  # 90 + 180 deg: faces -y
+def test_mount_yaw_composes_with_heading(heading, yaw, axis, sign):
+    # Camera heading = agent heading + mount yaw (cosines and sines in {0, +-1},
+    # exact in fp32).  The square 8 m along the composed direction, shifted 2 m
+    # to that camera's left, covers columns 16..30; straight behind it nothing.
+    (c, s_), (cm, sm) = heading, yaw
+    fx_, fy_ = c * cm - s_ * sm, s_ * cm + c * sm           # forward of the composed heading
+    lx, ly = -fy_, fx_                                      # its left
+    centre = (2.0 * lx, 2.0 * ly)
+    scene = make_scene(fronto_quad(8.0, 1.875, axis=axis, sign=sign, centre=centre) +
+                       fronto_quad(8.0, 1.875, axis=axis, sign=-sign), [7, 7, 5, 5])
+    ag = make_agents([(0.0, 0.0, 0.0, c, s_, 1.0, 1.0, 1.0, 3)])
+    rig = make_rig(mounts=((0.0, 0.0, 0.0, cm, sm),))
+    r = O.render(scene, ag, rig)
+    want = np.zeros((64, 64), bool)
+    want[24:39, 16:31] = True
+    assert np.array_equal(r["cls"][0] == 7, want)
+    assert np.all(r["cls"][0][~want] == SKY)
+
+
+def test_mount_offset_rotates_with_heading():
+    # Agent at (5, -3) heading +y (cos 0, sin 1) with its camera mounted 1 m
+    # ahead and 2 m to the left: the camera sits at (5 - 2, -3 + 1) and faces
+    # +y; a square 8 m ahead of that point fills columns and rows 24..38.
+    scene = make_scene(fronto_quad(8.0, 1.875, axis=1, centre=(3.0, -2.0)), [7, 7])
+    ag = make_agents([(5.0, -3.0, 0.0, 0.0, 1.0, 1.0, 1.0, 1.0, 3)])
+    rig = make_rig(mounts=((1.0, 2.0, 0.0, 1.0, 0.0),))
+    r = O.render(scene, ag, rig)
+    want = np.zeros((64, 64), bool)
+    want[24:39, 24:39] = True
+    assert np.array_equal(r["cls"][0] == 7, want)
+    assert np.allclose(r["depth"][0][want], 8.0, rtol=2 ** -20)
+
+
+def test_far_plane_is_inclusive():
+    # far = 64: a square exactly 64 m away (half-size 16, so 1/z = 1/64 is
+    # exact at every pixel) is drawn, columns and rows 24..39, depth 64; the
+    # same square a little farther is not.
+    rig = make_rig(far=64.0)
+    r = O.render(make_scene(fronto_quad(64.0, 16.0), [7, 7]), make_agents([ego()]), rig)
+    want = np.zeros((64, 64), bool)
+    want[24:40, 24:40] = True
+    assert np.array_equal(r["cls"][0] == 7, want)
+    assert np.allclose(r["depth"][0][want], 64.0, rtol=2 ** -20)
+    r2 = O.render(make_scene(fronto_quad(64.0625, 16.0), [7, 7]), make_agents([ego()]), rig)
+    assert np.all(r2["cls"][0] == SKY)
+
+
+def test_depth_error_bound_over_distances():
+    # Fronto squares (half-size D/16, 2 px) at 200 seeded distances D in [0.6, 95] m: the decoded depth
+    # at the image centre is within 2^-21 (the bucket midpoint) plus a few
+    # roundings of the plane (6.5 ulps in all) of the true distance.
+    rng = np.random.default_rng(11)
+    D = np.sort(rng.uniform(0.6, 95.0, 200)).astype(np.float32)
+    tris, cls = [], []
+    ags = []
+    for k, d in enumerate(D):
+        tris += fronto_quad(float(d), float(d) / 16.0, centre=(0.0, 1000.0 * k))
+        cls += [7, 7]
+        ags.append((0.0, 1000.0 * k, 0.0, 1.0, 0.0, 1.0, 1.0, 1.0, 3))
+    # one world per square, so no square sees another
+    T = len(tris) // len(D)
+    tv = np.asarray(tris, np.float32).reshape(len(D), T, 9)
+    from paper_2607_26005_amd.scenegen import Scene
+    scene = Scene(num_worlds=len(D), verts=np.ascontiguousarray(tv.reshape(-1, 9)), cls=np.asarray(cls, np.uint8),
+                  tri_offsets=np.arange(len(D) + 1, dtype=np.int64) * T,
+                  bounds=np.asarray([(-1000.0, 1000.0 * k - 500.0, 1000.0, 1000.0 * k + 500.0) for k in range(len(D))],
+                                    np.float32))
+    r = O.render(scene, make_agents(ags, num_worlds=len(D)), make_rig())
+    z = r["depth"][:, 32, 32].astype(np.float64)
+    assert np.all(r["cls"][:, 32, 32] == 7)
+    rel = np.abs(z - D.astype(np.float64)) / D
+    assert rel.max() <= 6.5 * 2.0 ** -23, rel.max()
+
+
 def test_offcentre_quad_columns():
     # Quad shifted 2 m to the left (+y): it moves 8 px left on screen.
     scene = make_scene(fronto_quad(8.0, 1.875, centre=(0.0, 2.0)), [7, 7])
@@ -321,10 +413,23 @@ def test_quantizer_exhaustive():
     assert np.all(q[1:] <= q[:-1])                          # nearer -> smaller key
     z = 1.0 / iz.astype(np.float64)
     rel = np.abs(d.astype(np.float64) - z) / z
-    assert rel.max() <= 2.0 ** -20
+    # a code holds 8 consecutive fp32 inverse depths; decoding at the bucket
+    # midpoint is within 4 of their ulps (2^-21 relative), the final division
+    # adds half an ulp of the depth
+    assert rel.max() <= 2.0 ** -21 + 2.0 ** -23
     # outside the range: beyond far is the clear value, nearer than near clamps
     q2, d2 = O.quantize(np.array([lo * 0.999, 3.0, np.nan], np.float32), near, far)
     assert q2[0] == 0xFFFFFF and np.isinf(d2[0]) and q2[1] == 0 and q2[2] == 0xFFFFFF
+
+
+def test_quantizer_cap_is_the_power_of_two_above_one_over_near():
+    # near = 0.3: 1/near = 3.33 and the cap is 4.  Inverse depths up to the cap
+    # keep their own codes (3.9 decodes to about 1/3.9, not to the near
+    # plane); beyond it they share the cap's code 0, decoded as 1/4.
+    q, d = O.quantize(np.array([3.9, 4.0, 5.0, 80.0], np.float32), 0.3, 100.0)
+    assert q[0] > 0 and abs(d[0] * 3.9 - 1.0) <= 2.0 ** -20
+    assert q[1] == 0 and q[2] == 0 and q[3] == 0
+    assert abs(d[2] - 0.25) <= 0.25 * 2.0 ** -20
 
 
 # ---------------------------------------------------------------------------
