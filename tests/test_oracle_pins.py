@@ -512,3 +512,18 @@ def test_bicycle_constant_turn_is_a_circle():
     R = np.hypot(xs - sol[0], ys - sol[1])
     assert R.std() < 1e-4 * R.mean()
     assert np.isclose(R.mean(), v * dt / (2 * np.sin(omega * dt / 2)), rtol=1e-3)
+
+
+def test_bicycle_turns_with_the_updated_speed():
+    # Semi-implicit update (speed first, then heading and position with the new
+    # speed): from rest with a = 4 m/s^2 and tan(steer) = 1, one 0.1 s step
+    # gives v' = 0.4, heading v' / (0.6 L) dt = 0.4 / 3 * 0.1, and moves v' dt
+    # along that heading; a heading update with the old speed would not turn.
+    L = 5.0
+    ag = _agents_for_bicycle(1, [0.0], [0.0], L)
+    out = O.agents_step(ag, np.array([np.pi / 4]), np.array([4.0]), dt=0.1)
+    psi = 0.4 / (0.6 * L) * 0.1
+    assert np.isclose(out["speed"][0], 0.4)
+    assert np.isclose(out["psi"][0], psi, rtol=1e-12)
+    assert np.isclose(out["x"][0], 0.04 * np.cos(psi), rtol=1e-7)
+    assert np.isclose(out["y"][0], 0.04 * np.sin(psi), rtol=1e-7)
