@@ -191,6 +191,31 @@ def test_fill_rule_and_snap_ties_closed_form(lib, s, lo, hi):
     check_views(lib, wl, np.arange(1), f"pin s={s}")
 
 
+def test_degenerate_and_non_finite_triangles(lib):
+    # Triangles the rules drop or that sit on their boundaries, among ordinary
+    # ones: a NaN and an infinite vertex (dropped by the snap's range rule or
+    # the depth plane's finiteness rule), zero-area and coincident-vertex
+    # triangles (area 0), one lying in the near plane (depth = near, the cap's
+    # code), one whose plane holds the camera (delta = 0), one reaching behind
+    # the camera, and one with a vertex 100 km away (wide edge values).
+    nan, inf = float("nan"), float("inf")
+    tris = quad((8.0, -3.0, -2.0), (8.0, 3.0, -2.0), (8.0, 3.0, 2.0), (8.0, -3.0, 2.0))
+    tris += [[(6.0, -1.0, 0.5), (6.0, 1.0, nan), (6.0, 0.0, 1.5)],
+             [(6.0, -1.0, -0.5), (inf, 1.0, -0.5), (6.0, 0.0, -1.5)],
+             [(5.0, -1.0, 0.0), (5.0, 0.0, 0.5), (5.0, 1.0, 1.0)],
+             [(5.0, 2.0, 1.0), (5.0, 2.0, 1.0), (5.0, 2.5, 1.5)],
+             [(0.5, -0.2, -0.2), (0.5, 0.2, -0.2), (0.5, 0.0, 0.2)],
+             [(2.0, -1.0, 0.0), (4.0, 1.0, 0.0), (6.0, 0.0, 0.0)],
+             [(-3.0, -1.0, -0.7), (7.0, -1.5, -0.7), (7.0, 1.5, -0.7)],
+             [(7.5, -2.0, 1.0), (7.5, -1.0, 1.0), (100000.0, 50000.0, -1.0)]]
+    scene = make_scene(tris, [7, 7, 1, 1, 2, 2, 3, 5, 6, 0])
+    ag = make_agents([(0.0, 0.0, 0.0, 1.0, 0.0, 1.0, 1.0, 1.0, 3)])
+    rig = make_rig(mounts=((0.0, 0.0, 0.0, 1.0, 0.0), (0.0, 0.0, 0.0, 0.0, 1.0)), far=100.0)
+    wl = sg.Workload("degenerate", 0, 0, scene, ag, rig, 16.0, 2000.0)
+    s = check_views(lib, wl, np.arange(wl.num_views), "degenerate")
+    assert s["mismatches"] == 0
+
+
 def test_camera_inside_box_and_near_clipped_ground(lib):
     G = 1000.0
     tris = quad((-G, -G, 0.0), (G, -G, 0.0), (G, G, 0.0), (-G, G, 0.0))
