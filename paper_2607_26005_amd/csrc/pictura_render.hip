@@ -643,15 +643,16 @@ __device__ __forceinline__ void raster_blocks(const RenderParams& P, Shared& S, 
     auto key_at = [&](int b, uint32_t& addr) -> uint32_t {
         if constexpr (I32 && Fast) {
             // the block's offsets, as the lane that tested it computed them
-            const int e0 = Eb[0] + (int)readlane((uint32_t)off[0], b);
-            const int e1 = Eb[1] + (int)readlane((uint32_t)off[1], b);
-            const int e2 = Eb[2] + (int)readlane((uint32_t)off[2], b);
-            const float pxf = pxl + readlane_f(pxu, b);
-            const float pyf = pyl + readlane_f(pyu, b);
+            // (broadcast through the LDS crossbar: no vector ALU instruction)
+            const int e0 = Eb[0] + (int)bperm(b, (uint32_t)off[0]);
+            const int e1 = Eb[1] + (int)bperm(b, (uint32_t)off[1]);
+            const int e2 = Eb[2] + (int)bperm(b, (uint32_t)off[2]);
+            const float pxf = pxl + __uint_as_float(bperm(b, __float_as_uint(pxu)));
+            const float pyf = pyl + __uint_as_float(bperm(b, __float_as_uint(pyu)));
             const float iz = fmaf(pa, pxf, fmaf(pb, pyf, pc));
             const uint32_t bits = min(__float_as_uint(iz), __float_as_uint(P.izcap));
             const uint32_t key = ((P.qbase - (bits >> 3)) << 8) | cls;
-            addr = readlane(boff, b) + (uint32_t)loff4;
+            addr = bperm(b, boff) + (uint32_t)loff4;
             return (((e0 | e1 | e2) >= 0) && iz >= P.izfar) ? key : 0xFFFFFFFFu;
         }
         const uint32_t q = readlane(xy, b);
