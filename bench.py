@@ -41,7 +41,7 @@ HBM_PEAK_GBS = 8000.0   # MI355X HBM3E peak
 # measured on; when the fingerprint differs, `traffic` is reported as null.
 TRAFFIC = {
     "config": 4,
-    "sources_sha256": "c02b4b5c9d54fcaa8b1954f9eceb90b34a665b6578acdab0f7721279c07d1d03",
+    "sources_sha256": "2bc95f875570512264874842b6cec8530a00ace65d98f3ba1aea5867ed402356",
     "fetch_bytes": 1.4667e9,
     "write_bytes": 5368709120,
 }
