@@ -565,10 +565,9 @@ __device__ __forceinline__ void raster_packed(const RenderParams& P, Shared& S, 
     }
 }
 
-// Rasterize one record with the whole wave.  Lane b tests 8x8 block
-// (b & 7, b >> 3) of the tile (a tile has at most 8 x 8 blocks): the block
-// must lie in the bounding box and the edge value at the block corner that
-// maximises it must be >= 0 for all three edges.  The
+// Rasterize one record with the whole wave.  Lane b tests 8x8 block b of
+// the bounding box (a tile has at most 8 x 8 blocks): the edge value at the
+// block corner that maximises it must be >= 0 for all three edges.  The
 // passing blocks are then rasterized one per step, lane l handling pixel
 // (l & 7, l >> 3): its edge values at that pixel of block (0, 0) plus the
 // block's offsets, which the lane that tested the block computed.
@@ -592,7 +591,11 @@ __device__ __forceinline__ void raster_blocks(const RenderParams& P, Shared& S, 
     const uint32_t cls = box & 255u;
     const int i0 = (int)((box >> 8) & 255u), i1 = (int)((box >> 16) & 255u);
     const int j0 = (int)(box >> 24), j1 = (int)(j1w & 255u);
-    const int bx0 = i0 >> 3, by0 = j0 >> 3, bx1 = i1 >> 3, by1 = j1 >> 3;
+    const int bx0 = i0 >> 3, by0 = j0 >> 3;
+    const int nbx = (i1 >> 3) - bx0 + 1, nb = nbx * ((j1 >> 3) - by0 + 1);
+    // b / nbx == (b * rinv) >> 16 for b < 64 and nbx <= 8
+    const uint32_t rinv = nbx == 1 ? 65536u : nbx == 2 ? 32768u : nbx == 3 ? 21846u : nbx == 4 ? 16384u
+                        : nbx == 5 ? 13108u : nbx == 6 ? 10923u : nbx == 7 ? 9363u : 8192u;
     E A[3], B[3], Cc[3], Eb[3], off[3];
 #pragma unroll
     for (int k = 0; k < 3; ++k) {
@@ -608,10 +611,12 @@ __device__ __forceinline__ void raster_blocks(const RenderParams& P, Shared& S, 
             Eb[k] = fma(A[k], (double)lx, fma(B[k], (double)ly, Cc[k]));
         }
     }
-    // lane b: block (b & 7, b >> 3) of the tile, whose origin (X, Y) is its own
-    // pixel offset times 8; only the blocks of the bounding box can pass
-    const int X = lx * 8, Y = ly * 8;
-    bool pass = lx >= bx0 && lx <= bx1 && ly >= by0 && ly <= by1;
+    // lane b: block b of the box
+    const int eby = (int)(((uint32_t)lane * rinv) >> 16), ebx = lane - eby * nbx;
+    // (lanes past the box hold no block; the masks keep X and Y below 64, so the
+    // products below stay 24-bit multiplies)
+    const int X = ((bx0 + ebx) & 7) * 8, Y = ((by0 + eby) & 7) * 8;
+    bool pass = lane < nb;
 #pragma unroll
     for (int k = 0; k < 3; ++k) {
         if constexpr (I32) {
@@ -629,7 +634,7 @@ __device__ __forceinline__ void raster_blocks(const RenderParams& P, Shared& S, 
     const uint32_t boff = (uint32_t)((Y * T.pitch + X) * 4);   // byte offset of the block in the framebuffer
     uint64_t m = __ballot(pass);
     if (P.stats && lane == 0) {
-        atomicAdd(&S.stat[kStBlocksTested], (uint32_t)((bx1 - bx0 + 1) * (by1 - by0 + 1)));
+        atomicAdd(&S.stat[kStBlocksTested], (uint32_t)nb);
         atomicAdd(&S.stat[kStBlocksPassed], (uint32_t)__popcll(m));
     }
     // Lanes that miss the piece take the key 0xFFFFFFFF, which changes
