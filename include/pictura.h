@@ -6,10 +6,17 @@
  * the static map triangles (paper Sec. 3.2, Eq. obs_pv: I_ik = Phi(A_i, W_i,
  * K_ik); "only the surroundings are rendered", so a view never draws its own
  * agent).  Each pixel receives the class ID of the nearest surface (uint8)
- * and its view-space depth in metres (fp32, +inf for background).  The
- * projection, near clipping, 8-bit-subpixel snapping, top-left fill rule and
- * the 24-bit-depth|8-bit-class visibility key follow fixed rules (R1..R9 in
- * the repository's design notes), so results do not depend on triangle order.
+ * and its view-space depth in metres (fp32, +inf for background).  Fixed
+ * rules make the result independent of triangle order and of how the work is
+ * split (all fp32 arithmetic without contraction, correctly rounded
+ * divisions): R1 camera = agent pose composed with the mount (yaw only);
+ * R2 view transform; R3 1/z plane of the unsnapped triangle; R4 Sutherland-
+ * Hodgman clip against z = near, fanned from the first vertex; R5 snap to
+ * 1/256 pixel, ties to even; R6 exact integer edge functions at pixel
+ * centres, top-left fill rule, two-sided; R7 key = (24-bit reverse depth from
+ * the fp32 bits of 1/z, capped at the power of two above 1/near) << 8 | class,
+ * the minimum key wins, 1/z below 1/far is rejected; R8 depth = 1 / the code's
+ * bucket midpoint; R9 agent boxes of 12 triangles, the ego's own box skipped.
  *
  * Conventions
  *  - Plain C99; no HIP/CUDA or C++ types.  A `void* stream` is a hipStream_t
@@ -172,8 +179,11 @@ pictura_status pictura_render_views(pictura_ctx ctx, const pictura_agents* agent
  * with face 0 bottom, 1 top, 2 back, 3 front, 4 right, 5 left (the order of
  * rule R9's triangles, two per face), in place of its class; every other
  * triangle keeps its class.  out_cls receives key & 15.  out_rgb[v][c][y][x]
- * (uint8, planar, c = red, green, blue): with base = palette[class] / 255 (the
- * table in the repository's design notes), factor = 0.45, 1, 0.55, 0.85, 0.7,
+ * (uint8, planar, c = red, green, blue): with base = palette[class] / 255
+ * (class: R G B -- 0 ground 96 112 72, 1 road 72 72 78, 2 marking 232 232 224,
+ * 3 vehicle 52 96 220, 4 sky 140 184 232, 5 curb 160 160 152, 6 pedestrian
+ * 224 72 64, 7 wall 168 144 120, 8 red light 255 32 24, 9 amber 255 184 0,
+ * 10 green 32 224 96, 11..15 128 128 128), factor = 0.45, 1, 0.55, 0.85, 0.7,
  * 0.7 for the faces bottom .. left and 1 for other surfaces, b = 1 - 0.6 *
  * min(z / far, 1) on box faces (z the output depth) and 1 elsewhere:
  * rint(255 * min(base * (factor * b), 1)), fp32 in this order.  One sample
