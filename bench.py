@@ -124,7 +124,7 @@ def cpu_baseline(wl, target_s):
 def main():
     args = parse()
     if args.gpus != 1:
-        print(json.dumps({"error": "this build runs on one GPU only: the render path shards by world, "
+        print(json.dumps({"error": "the benchmark runs on one GPU only: the render path shards by world, "
                                    "but no multi-GPU launch exists; use --gpus 1"}))
         sys.exit(2)
     import torch
