@@ -38,17 +38,19 @@ HBM_PEAK_GBS = 8000.0   # MI355X HBM3E peak
 # rocprofv3 FETCH_SIZE and WRITE_SIZE runs (one counter per run), each scaled
 # by what the counter reads for a plain 1 GiB device copy (FETCH_SIZE x1.99994,
 # WRITE_SIZE x1.0).  The figures hold only for the kernel sources they were
-# measured on; when the fingerprint differs, `traffic` is reported as null.
+# measured on (and the workload generator); when the fingerprint differs,
+# `traffic` is reported as null.
 TRAFFIC = {
     "config": 4,
-    "sources_sha256": "2bc95f875570512264874842b6cec8530a00ace65d98f3ba1aea5867ed402356",
-    "fetch_bytes": 1.4667e9,
+    "sources_sha256": "81ef855193b20be59a2dc57725344519a23a07b13531da757c709438f99ccb7e",
+    "fetch_bytes": 1.4805e9,
     "write_bytes": 5368709120,
 }
 TRAFFIC_SOURCES = ["paper_2607_26005_amd/csrc/pictura_render.hip",
                    "paper_2607_26005_amd/csrc/pictura_internal.h",
                    "paper_2607_26005_amd/csrc/pictura_device.h",
-                   "paper_2607_26005_amd/build.py"]
+                   "paper_2607_26005_amd/build.py",
+                   "paper_2607_26005_amd/scenegen.py"]   # the workload (scene, cell size) too
 
 
 def kernel_fingerprint():

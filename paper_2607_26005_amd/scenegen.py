@@ -511,10 +511,10 @@ def _bezier_world(rng, size, tile, target_tris, n_agents, jitter):
 
 CONFIGS = {
     1: dict(name="tiny", seed=0, worlds=1, size=200.0, agents=8, cams=1, res=64, far=100.0, cell=16.0),
-    2: dict(name="small_batch", seed=1, worlds=64, size=1000.0, agents=32, cams=4, res=64, far=100.0, cell=16.0),
-    3: dict(name="dense_traffic", seed=2, worlds=256, size=1000.0, agents=128, cams=4, res=64, far=100.0, cell=16.0),
-    4: dict(name="throughput_headline", seed=3, worlds=1024, size=1000.0, agents=64, cams=4, res=64, far=150.0, cell=24.0),
-    5: dict(name="highres_large_scene", seed=4, worlds=128, size=4000.0, agents=64, cams=4, res=128, far=200.0, cell=32.0),
+    2: dict(name="small_batch", seed=1, worlds=64, size=1000.0, agents=32, cams=4, res=64, far=100.0, cell=20.0),
+    3: dict(name="dense_traffic", seed=2, worlds=256, size=1000.0, agents=128, cams=4, res=64, far=100.0, cell=20.0),
+    4: dict(name="throughput_headline", seed=3, worlds=1024, size=1000.0, agents=64, cams=4, res=64, far=150.0, cell=30.0),
+    5: dict(name="highres_large_scene", seed=4, worlds=128, size=4000.0, agents=64, cams=4, res=128, far=200.0, cell=16.0),
     # the paper's own rig and batch: 2048 egos x 4 views at 96x54 (App. A.2, Tab. camera_rig; Tab. render_mem)
     6: dict(name="paper_rig", seed=5, worlds=64, size=1000.0, agents=32, cams="paper", res=(96, 54), far=100.0, cell=16.0),
     # the paper's other rendering features (Sec. 3.2, Fig. qualitative): walls, parked cars, traffic lights
