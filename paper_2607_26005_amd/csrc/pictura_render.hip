@@ -1378,10 +1378,14 @@ struct alignas(16) AaLds {
 // kMode 0: class and depth (and colour without antialiasing); 1: the
 // instance variant; 2: colour with antialiasing.  The variants' LDS admits
 // two waves per SIMD, so they may use twice the registers.
-template <int kMode>
-__global__ __launch_bounds__(kThreads, kMode != 0 ? 2 : kWavesPerSimd) void render_views_kernel(const RenderParams P)
+template <int kMode, bool kStats>
+__global__ __launch_bounds__(kThreads, kMode != 0 ? 2 : kWavesPerSimd) void render_views_kernel(const RenderParams P_)
 {
     constexpr bool kInst = kMode == 1, kAA = kMode == 2;
+    // The work counters are compiled into their own instantiation: elsewhere
+    // the counter pointer is a constant null and every counting site folds away.
+    RenderParams P = P_;
+    if constexpr (!kStats) P.stats = nullptr;
     __shared__ Shared S;
     __shared__ typename std::conditional<kInst, InstLds, typename std::conditional<kAA, AaLds, NoInstLds>::type>::type I;
     const int tid = threadIdx.x, lane = lane_id(), wid = tid >> 6;
@@ -1400,8 +1404,8 @@ __global__ __launch_bounds__(kThreads, kMode != 0 ? 2 : kWavesPerSimd) void rend
     Cam cam;
     {
         const float c = P.ac[g], s = P.as[g];
-        const float mx = P.mount[k][0], my = P.mount[k][1], mz = P.mount[k][2];
-        const float cm = P.mount[k][3], sm = P.mount[k][4];
+        const float mx = P_.mount[k][0], my = P_.mount[k][1], mz = P_.mount[k][2];
+        const float cm = P_.mount[k][3], sm = P_.mount[k][4];
         const float t1 = mx * c, t2 = my * s, t3 = mx * s, t4 = my * c;
         const float ox = t1 - t2, oy = t3 + t4;
         cam.x = P.ax[g] + ox;
@@ -1864,9 +1868,16 @@ __global__ __launch_bounds__(kThreads, kMode != 0 ? 2 : kWavesPerSimd) void rend
 hipError_t launch_render(const RenderParams& p, hipStream_t s)
 {
     if (p.num_blocks <= 0) return hipSuccess;
-    if (p.out_inst) hipLaunchKernelGGL(render_views_kernel<1>, dim3((unsigned)p.num_blocks), dim3(kThreads), 0, s, p);
-    else if (p.out_rgb && p.aa) hipLaunchKernelGGL(render_views_kernel<2>, dim3((unsigned)p.num_blocks), dim3(kThreads), 0, s, p);
-    else hipLaunchKernelGGL(render_views_kernel<0>, dim3((unsigned)p.num_blocks), dim3(kThreads), 0, s, p);
+    const dim3 grid((unsigned)p.num_blocks), block(kThreads);
+    if (p.stats) {
+        if (p.out_inst) hipLaunchKernelGGL((render_views_kernel<1, true>), grid, block, 0, s, p);
+        else if (p.out_rgb && p.aa) hipLaunchKernelGGL((render_views_kernel<2, true>), grid, block, 0, s, p);
+        else hipLaunchKernelGGL((render_views_kernel<0, true>), grid, block, 0, s, p);
+    } else {
+        if (p.out_inst) hipLaunchKernelGGL((render_views_kernel<1, false>), grid, block, 0, s, p);
+        else if (p.out_rgb && p.aa) hipLaunchKernelGGL((render_views_kernel<2, false>), grid, block, 0, s, p);
+        else hipLaunchKernelGGL((render_views_kernel<0, false>), grid, block, 0, s, p);
+    }
     return hipGetLastError();
 }
 
