@@ -1378,14 +1378,22 @@ struct alignas(16) AaLds {
 // kMode 0: class and depth (and colour without antialiasing); 1: the
 // instance variant; 2: colour with antialiasing.  The variants' LDS admits
 // two waves per SIMD, so they may use twice the registers.
-template <int kMode, bool kStats>
-__global__ __launch_bounds__(kThreads, kMode != 0 ? 2 : kWavesPerSimd) void render_views_kernel(const RenderParams P_)
+// kMode: 0 class and depth, 1 with instance visibility, 2 with antialiased
+// colour, 3 with colour.  kDebug: the work counters and the option to turn
+// culling off are read at run time; otherwise the counter pointer is a
+// constant null and culling constantly on, so every counting site and the
+// unculled paths fold away (and so does the colour code outside modes 2 and 3).
+template <int kMode, bool kDebug>
+__global__ __launch_bounds__(kThreads, kMode == 1 || kMode == 2 ? 2 : kWavesPerSimd)
+void render_views_kernel(const RenderParams P_)
 {
     constexpr bool kInst = kMode == 1, kAA = kMode == 2;
-    // The work counters are compiled into their own instantiation: elsewhere
-    // the counter pointer is a constant null and every counting site folds away.
     RenderParams P = P_;
-    if constexpr (!kStats) P.stats = nullptr;
+    if constexpr (!kDebug) {
+        P.stats = nullptr;
+        P.cull = 1;
+    }
+    if constexpr (kMode == 0 || kMode == 1) P.out_rgb = nullptr;
     __shared__ Shared S;
     __shared__ typename std::conditional<kInst, InstLds, typename std::conditional<kAA, AaLds, NoInstLds>::type>::type I;
     const int tid = threadIdx.x, lane = lane_id(), wid = tid >> 6;
@@ -1869,13 +1877,16 @@ hipError_t launch_render(const RenderParams& p, hipStream_t s)
 {
     if (p.num_blocks <= 0) return hipSuccess;
     const dim3 grid((unsigned)p.num_blocks), block(kThreads);
-    if (p.stats) {
-        if (p.out_inst) hipLaunchKernelGGL((render_views_kernel<1, true>), grid, block, 0, s, p);
-        else if (p.out_rgb && p.aa) hipLaunchKernelGGL((render_views_kernel<2, true>), grid, block, 0, s, p);
+    const int mode = p.out_inst ? 1 : p.out_rgb ? (p.aa ? 2 : 3) : 0;
+    if (p.stats || !p.cull) {
+        if (mode == 1) hipLaunchKernelGGL((render_views_kernel<1, true>), grid, block, 0, s, p);
+        else if (mode == 2) hipLaunchKernelGGL((render_views_kernel<2, true>), grid, block, 0, s, p);
+        else if (mode == 3) hipLaunchKernelGGL((render_views_kernel<3, true>), grid, block, 0, s, p);
         else hipLaunchKernelGGL((render_views_kernel<0, true>), grid, block, 0, s, p);
     } else {
-        if (p.out_inst) hipLaunchKernelGGL((render_views_kernel<1, false>), grid, block, 0, s, p);
-        else if (p.out_rgb && p.aa) hipLaunchKernelGGL((render_views_kernel<2, false>), grid, block, 0, s, p);
+        if (mode == 1) hipLaunchKernelGGL((render_views_kernel<1, false>), grid, block, 0, s, p);
+        else if (mode == 2) hipLaunchKernelGGL((render_views_kernel<2, false>), grid, block, 0, s, p);
+        else if (mode == 3) hipLaunchKernelGGL((render_views_kernel<3, false>), grid, block, 0, s, p);
         else hipLaunchKernelGGL((render_views_kernel<0, false>), grid, block, 0, s, p);
     }
     return hipGetLastError();
