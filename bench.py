@@ -42,8 +42,8 @@ HBM_PEAK_GBS = 8000.0   # MI355X HBM3E peak
 # `traffic` is reported as null.
 TRAFFIC = {
     "config": 4,
-    "sources_sha256": "81ef855193b20be59a2dc57725344519a23a07b13531da757c709438f99ccb7e",
-    "fetch_bytes": 1.4805e9,
+    "sources_sha256": "43adc82f356cae3c1fff2969a92b09ccbf509c20613432cbcfb25dfa6c91af2f",
+    "fetch_bytes": 1.4811e9,
     "write_bytes": 5368709120,
 }
 TRAFFIC_SOURCES = ["paper_2607_26005_amd/csrc/pictura_render.hip",
