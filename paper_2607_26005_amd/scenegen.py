@@ -389,6 +389,26 @@ def _aabox_tris(x0, y0, z0, x1, y1, z1):
 
 
 LIGHT_Z, LIGHT_R, LIGHT_COS_MAX = 5.0, 0.3, 0.5   # head height, disk radius, cone cos(60 deg)
+STOP_W, STOP_GAP = 0.4, 1.0                       # stop-line bar width, gap to the crossing road's edge
+
+
+def light_and_stop_line(cx, cy, dx, dy, hw_cross, hw_own):
+    """The signal of one approach and the stop line it governs (Sec. 3.2,
+    rendering features: the head is placed apart from its stop line, as at
+    junctions whose signal hangs beyond the crossing).  Traffic moving along the
+    unit axis (dx, dy) drives on the right-hand half of its road (half width
+    hw_own); the crossing road has half width hw_cross.  Returns the head's
+    centre (beyond the junction, on the right, facing the approaching traffic)
+    and the bar's two triangles (before the junction, across the right-hand
+    lanes, at the marking layer)."""
+    far = hw_cross + 1.0
+    rx, ry = dy, -dx                                   # right-hand side of the travel direction
+    head = (cx + dx * far + rx * (hw_own + 1.0), cy + dy * far + ry * (hw_own + 1.0))
+    s0, s1 = -(hw_cross + STOP_GAP + STOP_W), -(hw_cross + STOP_GAP)
+    corner = lambda s, t: np.array([[cx + dx * s + rx * t, cy + dy * s + ry * t, Z_MARK]])
+    # counter-clockwise seen from above: along the travel direction, then across to the left
+    bar = _quads(corner(s0, hw_own), corner(s1, hw_own), corner(s1, 0.0), corner(s0, 0.0))
+    return head, bar
 
 
 def _town_world(rng, size, n_agents):
@@ -431,7 +451,8 @@ def _town_world(rng, size, n_agents):
                     extra_t.append(bx)
                     extra_c.append(np.full(len(bx), VEHICLE, np.uint8))
     # traffic lights: at every crossing one head per approach, on the far side of the
-    # junction, facing the traffic that approaches it; the two axes show opposite states
+    # junction, facing the traffic that approaches it, and the stop line it governs on
+    # the near side; the two axes show opposite states
     xr = [r for r in roads if r.axis == 0]
     yr = [r for r in roads if r.axis == 1]
     for ra in xr:
@@ -446,10 +467,9 @@ def _town_world(rng, size, n_agents):
                                                    (-1, 0, sx, rb.width / 2, ra.width / 2),
                                                    (0, 1, sy, ra.width / 2, rb.width / 2),
                                                    (0, -1, sy, ra.width / 2, rb.width / 2)):
-                far = hw_cross + 1.0
-                lat = -hw_own - 1.0          # right-hand traffic: the head stands on the right-hand side
-                px = cx_ + dx * far + dy * (-lat)
-                py = cy_ + dy * far + dx * lat
+                (px, py), bar = light_and_stop_line(cx_, cy_, dx, dy, hw_cross, hw_own)
+                extra_t.append(bar)
+                extra_c.append(np.full(len(bar), MARKING, np.uint8))
                 lx.append(px); ly.append(py)
                 lcf.append(float(-dx)); lsf.append(float(-dy))
                 lcls.append(st)

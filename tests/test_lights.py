@@ -159,3 +159,41 @@ def test_against_float64_raycast_with_lights(seed):
     assert np.array_equal(out["cls"][0][ok], rc[ok])
     fin = ok & np.isfinite(rd)
     assert np.all(np.abs(out["depth"][0][fin] / rd[fin] - 1.0) <= 4e-6)
+
+
+@pytest.mark.parametrize("dx,dy", [(1, 0), (-1, 0), (0, 1), (0, -1)])
+def test_stop_line_before_the_junction_and_head_beyond_it(dx, dy):
+    # the scene generator's signal layout: the head hangs beyond the crossing on the
+    # right-hand side, the stop line it governs lies across the right-hand lanes before it
+    from paper_2607_26005_amd.scenegen import light_and_stop_line, Z_MARK
+    cx, cy, hwc, hwo = 10.0, -20.0, 5.25, 3.5
+    (hx, hy), bar = light_and_stop_line(cx, cy, dx, dy, hwc, hwo)
+    along = lambda x, y: (x - cx) * dx + (y - cy) * dy
+    right = lambda x, y: (x - cx) * dy - (y - cy) * dx
+    assert along(hx, hy) > hwc and right(hx, hy) > hwo
+    assert bar.shape == (2, 3, 3) and np.all(bar[..., 2] == Z_MARK)
+    pa, pr = along(bar[..., 0], bar[..., 1]), right(bar[..., 0], bar[..., 1])
+    assert np.all(pa < -hwc) and np.all(pa >= -hwc - 1.5)
+    assert pr.min() == pytest.approx(0.0) and pr.max() == pytest.approx(hwo)
+    # the two triangles tile the bar: their areas add up to its width times the half road
+    e1, e2 = bar[:, 1, :2] - bar[:, 0, :2], bar[:, 2, :2] - bar[:, 0, :2]
+    area = 0.5 * np.abs(e1[:, 0] * e2[:, 1] - e1[:, 1] * e2[:, 0])
+    assert area.sum() == pytest.approx(0.4 * hwo)
+
+
+def test_approaching_camera_sees_the_stop_line_near_and_its_signal_far():
+    # a camera 12 m before a crossing, on the right-hand lane, looking along the road:
+    # the stop line is drawn before the crossing road's edge, the red head beyond it
+    from paper_2607_26005_amd.scenegen import light_and_stop_line, LIGHT_Z, LIGHT_R
+    hwc, hwo = 5.25, 3.5
+    (hx, hy), bar = light_and_stop_line(0.0, 0.0, 1, 0, hwc, hwo)
+    L = lights_of([(hx, hy, LIGHT_Z, -1.0, 0.0, LIGHT_R, RED)])
+    rig = make_rig(res=256, f=256.0, mounts=((0.0, 0.0, 1.5, 1.0, 0.0),))    # camera 1.5 m above the road
+    out = O.render(make_scene(bar, [2, 2]), ego(-12.0, -1.75), rig, lights=L)
+    cls, dep = out["cls"][0], out["depth"][0]
+    mark, red = cls == 2, cls == RED
+    assert mark.sum() > 100 and red.sum() > 20
+    assert dep[mark].max() < 12.0 - hwc < 12.0 < 12.0 + hx == pytest.approx(dep[red].min())
+    rows_m, rows_r = np.nonzero(mark)[0], np.nonzero(red)[0]
+    assert rows_r.max() < 128 < rows_m.min()          # the head above the horizon, the bar below it
+    assert np.nonzero(red)[1].min() > 128             # the head on the right-hand side
