@@ -42,7 +42,7 @@ HBM_PEAK_GBS = 8000.0   # MI355X HBM3E peak
 # `traffic` is reported as null.
 TRAFFIC = {
     "config": 4,
-    "sources_sha256": "43adc82f356cae3c1fff2969a92b09ccbf509c20613432cbcfb25dfa6c91af2f",
+    "sources_sha256": "18cfa04c8b617f6de132ed6f378130d5fb7f43cdc50d6814d021bdda7c6d3637",
     "fetch_bytes": 1.4811e9,
     "write_bytes": 5368709120,
 }
