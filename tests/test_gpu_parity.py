@@ -6,6 +6,7 @@ the large ones (the GPU renders every view of the batch in the same launch
 configuration the benchmark times; the oracle computes the sampled views one
 by one).
 """
+import dataclasses
 import functools
 
 import numpy as np
@@ -96,6 +97,32 @@ def test_headline_full_size_sampled(lib):
     # the benchmark's workload and launch: 1024 worlds x 64 agents x 4 cameras
     wl = workload(4)
     check_views(lib, wl, sample_views(wl.num_views, 256, 23), "headline")
+
+
+def test_headline_after_bench_steps_sampled(lib):
+    # the state the benchmark's last timed render sees: the headline agents moved
+    # by 110 bicycle updates on the GPU (10 warm-up + 100 timed steps, the same
+    # controls), read back, then rendered by both sides from that state
+    torch = _torch()
+    wl = workload(4)
+    steps = 110
+    steer, accel = sg.controls(wl.agents.count, steps, seed=wl.seed)
+    da = lib.DeviceAgents.from_host(wl.agents)
+    r = lib.Renderer(0)
+    try:
+        for s in range(steps):
+            r.agents_step(da, torch.as_tensor(steer[s], device="cuda"), torch.as_tensor(accel[s], device="cuda"),
+                          dt=0.1, vmax=20.0)
+        torch.cuda.synchronize()
+    finally:
+        r.close()
+    ag = wl.agents.copy()
+    for f in ("x", "y", "cos_h", "sin_h", "psi", "speed"):
+        setattr(ag, f, getattr(da, f).cpu().numpy().astype(np.float32))
+    moved = float(np.median(np.hypot(ag.x - wl.agents.x, ag.y - wl.agents.y)))
+    print(f"[headline-stepped] median displacement {moved:.1f} m over {steps} steps", flush=True)
+    assert moved > 10.0
+    check_views(lib, dataclasses.replace(wl, agents=ag), sample_views(wl.num_views, 256, 29), "headline-stepped")
 
 
 def test_highres_tiled_sampled(lib):
