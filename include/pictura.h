@@ -11,7 +11,9 @@
  * split (all fp32 arithmetic without contraction, correctly rounded
  * divisions): R1 camera = agent pose composed with the mount (yaw only);
  * R2 view transform; R3 1/z plane of the unsnapped triangle; R4 Sutherland-
- * Hodgman clip against z = near, fanned from the first vertex; R5 snap to
+ * Hodgman clip against z = near, fanned from the first vertex, and a
+ * triangle whose three vertices all lie beyond far (or all nearer than near)
+ * is not drawn, since no point of it lies inside the view volume; R5 snap to
  * 1/256 pixel, ties to even; R6 exact integer edge functions at pixel
  * centres, top-left fill rule, two-sided; R7 key = (24-bit reverse depth from
  * the fp32 bits of 1/z, capped at the power of two above 1/near) << 8 | class,
@@ -220,7 +222,8 @@ pictura_status pictura_render_rgb_aa(pictura_ctx ctx, const pictura_agents* agen
 
 /* Render like pictura_render_views (same out_cls, out_depth) and also the
  * instance visibility the paper's analysis reads from its renderer, each road
- * user's occlusion percentage (Sec. 4.3, probes of the trained policy):
+ * user's occlusion percentage (Sec. 5.2, "Grounding in What the Cameras
+ * See": probes of the trained policy):
  *  - out_inst[v][y][x] (int32): the agent index a (0 .. agents_per_world - 1,
  *    within the view's world) whose box owns the pixel's visible surface: among
  *    the boxes with a fragment whose visibility key (rule R7) equals the pixel's
@@ -252,7 +255,10 @@ pictura_status pictura_render_instances(pictura_ctx ctx, const pictura_agents* a
 pictura_status pictura_set_lights(pictura_ctx ctx, const pictura_lights* lights);
 
 /* One kinematic-bicycle step for every agent (the per-step agent motion of
- * the headline workload): v' = clamp(v + accel * dt, 0, vmax);
+ * the headline workload; the paper's simulation step is dt = 0.1 s, App. A.3,
+ * Tab. hparams, and its agents follow a kinematic model whose exact form it
+ * does not print, so the semi-implicit bicycle below is this library's
+ * reading): v' = clamp(v + accel * dt, 0, vmax);
  * psi' = psi + v' / (0.6 length) * tan(steer) * dt wrapped into (-pi, pi];
  * x += v' cos(psi') dt; y += v' sin(psi') dt; cos_h/sin_h = cos/sin(psi').
  * steer[count] (radians) and accel[count] (m/s^2) are device arrays.
@@ -293,6 +299,15 @@ pictura_status pictura_set_option(pictura_ctx ctx, int32_t option, int32_t value
  * record raster (part of the exact pass), final barrier and write-out.
  * reset != 0 zeroes the counters. */
 pictura_status pictura_stats_copy(pictura_ctx ctx, uint64_t* out, int32_t n, int32_t reset);
+
+#define PICTURA_DEVERR_RING_WAIT 1u /* a raster record reserved in a view's record ring was never published */
+/* Device-side errors the render kernels found (the kernels cannot return a
+ * status): *out receives the OR of the PICTURA_DEVERR_* bits set by every
+ * render call on this context since it was created or last reset; 0 means
+ * none.  A set bit means an image may be incomplete (the kernel skipped the
+ * work it could not do rather than hang).  Synchronous: waits for all work
+ * on the context's device.  reset != 0 clears the word.  EINVAL: null out. */
+pictura_status pictura_device_errors(pictura_ctx ctx, uint32_t* out, int32_t reset);
 
 /* Device self-check of the reciprocal the kernels use in place of IEEE
  * division where |argument| lies in [2^-12, 2^20) (hardware reciprocal plus

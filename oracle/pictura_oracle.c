@@ -91,7 +91,7 @@
  *              colour of key ((o >> 16) << 16) | ((o >> 8) & 255).
  *
  * Instances (optional outputs; the road users' occlusion percentages the
- * paper's analysis reads from its renderer, Sec. 4.3): every other agent's box
+ * paper's analysis reads from its renderer, Sec. 5.2): every other agent's box
  * is also drawn alone, with the same rules, into a frame of its own.  Its
  * footprint is the number of pixels that frame covers; a pixel belongs to
  * the lowest-index agent whose own frame holds the pixel's final key there

@@ -50,6 +50,7 @@ struct pictura_ctx_s {
     unsigned long long* stats = nullptr;   // [kNumStats] device counters
     // traffic lights (caller-owned device arrays; lights.lights_per_world == 0: none)
     pictura_lights lights{};
+    uint32_t* dev_err = nullptr;   // device error word (pictura_device_errors), allocated by pictura_create
 };
 
 namespace {
@@ -145,6 +146,18 @@ pictura_status pictura_create(int32_t device, pictura_ctx* out)
     auto* c = new (std::nothrow) pictura_ctx_s();
     if (!c) return PICTURA_ENOMEM;
     c->device = device;
+    {
+        DeviceGuard g(device);
+        if (hipMalloc((void**)&c->dev_err, sizeof(uint32_t)) != hipSuccess) {
+            delete c;
+            return PICTURA_ENOMEM;
+        }
+        if (hipMemset(c->dev_err, 0, sizeof(uint32_t)) != hipSuccess) {
+            (void)hipFree(c->dev_err);
+            delete c;
+            return PICTURA_EDEVICE;
+        }
+    }
     *out = c;
     return PICTURA_OK;
 }
@@ -156,6 +169,7 @@ void pictura_destroy(pictura_ctx c)
         DeviceGuard g(c->device);
         (void)hipDeviceSynchronize();
         free_scene(c);
+        dfree(c->dev_err);
     }
     delete c;
 }
@@ -351,6 +365,7 @@ static pictura_status render_setup(pictura_ctx c, const pictura_agents* ag, cons
     P.div_agents = make_div31((uint32_t)P.A);
     P.rcs = 1.0f / c->cell_size;
     P.out_cls = out_cls; P.out_depth = out_depth;
+    P.dev_err = c->dev_err;
     P.cull = c->cull;
     P.vec_out = ((reinterpret_cast<uintptr_t>(out_cls) | reinterpret_cast<uintptr_t>(out_depth)) & 15u) == 0 ? 1 : 0;
     if (c->lights.lights_per_world > 0) {
@@ -564,6 +579,23 @@ pictura_status pictura_selftest_rcp(pictura_ctx c, uint32_t lo_bits, uint32_t co
     }
     (void)hipFree(d);
     *mismatches = (uint64_t)h;
+    return PICTURA_OK;
+}
+
+pictura_status pictura_device_errors(pictura_ctx c, uint32_t* out, int32_t reset)
+{
+    if (!c) return PICTURA_EINVAL;
+    c->err.clear();
+    if (!out) return fail(c, PICTURA_EINVAL, "device_errors: null output");
+    DeviceGuard dg(c->device);
+    hipError_t e;
+    if ((e = hipDeviceSynchronize()) != hipSuccess) return hip_fail(c, e, "device_errors sync");
+    uint32_t h = 0;
+    if ((e = hipMemcpy(&h, c->dev_err, sizeof h, hipMemcpyDeviceToHost)) != hipSuccess)
+        return hip_fail(c, e, "device_errors copy");
+    *out = h;
+    if (reset && h != 0 && (e = hipMemset(c->dev_err, 0, sizeof h)) != hipSuccess)
+        return hip_fail(c, e, "device_errors reset");
     return PICTURA_OK;
 }
 

@@ -92,7 +92,11 @@ struct RenderParams {
     const uint8_t* lcls;
     int32_t L;
     float lcos2;        // cos_max * cos_max (fp32)
+    uint32_t* dev_err;  // context-owned device word: bits of kDevErr* OR-ed in by the kernels
 };
+
+// Device error bits (pictura_device_errors)
+constexpr uint32_t kDevErrRingWait = 1u;   // a raster record reserved in the ring was never published
 
 struct AgentStepParams {
     float* x; float* y; float* psi; float* speed; float* cos_h; float* sin_h;

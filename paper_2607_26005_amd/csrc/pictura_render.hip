@@ -709,6 +709,9 @@ __device__ __forceinline__ int setup_triangle(const RenderParams& P, Shared& S, 
 #pragma unroll
     for (int k = 0; k < 3; ++k) view_xform(cam, tri[3 * k], tri[3 * k + 1], tri[3 * k + 2], xv[k], yv[k], zv[k]);
     const bool in0 = zv[0] >= P.nearp, in1 = zv[1] >= P.nearp, in2 = zv[2] >= P.nearp;
+    // R4: nothing of the triangle inside near .. far
+    if (!(in0 || in1 || in2)) return 0;
+    if (zv[0] > P.farp && zv[1] > P.farp && zv[2] > P.farp) return 0;
     bool ok = true;
     if (in0 && in1 && in2) {
         ok = snap_vertex(P, xv[0], yv[0], zv[0], X0, Y0) && snap_vertex(P, xv[1], yv[1], zv[1], X1, Y1) &&
@@ -744,7 +747,7 @@ __device__ __forceinline__ int setup_triangle(const RenderParams& P, Shared& S, 
         case 5: setp(0, xv[0], yv[0], zv[0]); setp(1, x01, y01, nz); setp(2, x12, y12, nz);
                 setp(3, xv[2], yv[2], zv[2]); np = 4; break;
         default: setp(0, x01, y01, nz); setp(1, xv[1], yv[1], zv[1]); setp(2, xv[2], yv[2], zv[2]);
-                 setp(3, x20, y20, nz); np = 4; break;   // case 6
+                 setp(3, x20, y20, nz); np = 4; break;   // case 6 (cases 0 and 7 returned above)
         }
         if (np == 3) { px[3] = px[2]; py[3] = py[2]; pz[3] = pz[2]; }
         ok = snap_vertex(P, px[0], py[0], pz[0], X0, Y0) && snap_vertex(P, px[1], py[1], pz[1], X1, Y1) &&
@@ -1715,8 +1718,9 @@ void render_views_kernel(const RenderParams P_)
         // Every wait below ends: a claimed slot was reserved by a wave that
         // publishes it right after reserving it, and each wave sets its done
         // flag after its last reservation.  The sleep counts are bounded all
-        // the same (about a second), so a broken invariant shows as a wrong
-        // image, never as a hung wave.
+        // the same (about a second), so a broken invariant never hangs a wave:
+        // it leaves the record undrawn and sets kDevErrRingWait in the
+        // context's error word, which pictura_device_errors reports.
         uint32_t naps = 0;
         for (; naps < (1u << 22); ) {
             // the done flags first: once both are set, the reserved count is final
@@ -1732,7 +1736,11 @@ void render_views_kernel(const RenderParams P_)
                 const uint32_t* w3 = &S.fb[(4 * (int)h + 3) * T.pitch + T.pitch - 4];
                 while (readfirst(lds_load_acquire(&w3[2])) != kRecReady && ++naps < (1u << 22))
                     __builtin_amdgcn_s_sleep(1);
-                if (naps >= (1u << 22)) break;   // never published (cannot happen): skip, do not read it
+                if (naps >= (1u << 22)) {
+                    // never published (cannot happen): skip it, do not read it, and say so
+                    if (lane == 0) atomicOr(P.dev_err, kDevErrRingWait);
+                    break;
+                }
                 const u32x4* g = (const u32x4*)&S.fb[4 * (int)h * T.pitch + T.pitch - 4];
                 const int rs = T.pitch >> 2;
                 const u32x4 g0 = g[0], g1 = g[rs], g2 = g[2 * rs];

@@ -95,11 +95,15 @@ _lib.pictura_set_lights.argtypes = [_P, ctypes.POINTER(_Lights)]
 _lib.pictura_set_lights.restype = ctypes.c_int32
 _lib.pictura_selftest_rcp.argtypes = [_P, ctypes.c_uint32, ctypes.c_uint32, _P]
 _lib.pictura_selftest_rcp.restype = ctypes.c_int32
+_lib.pictura_device_errors.argtypes = [_P, _P, ctypes.c_int32]
+_lib.pictura_device_errors.restype = ctypes.c_int32
 
 EXPORTED = ["pictura_create", "pictura_destroy", "pictura_last_error", "pictura_scene_upload",
             "pictura_bin_scene", "pictura_render_views", "pictura_agents_step", "pictura_bins_info",
             "pictura_bins_copy", "pictura_set_option", "pictura_stats_copy", "pictura_selftest_rcp",
-            "pictura_set_lights", "pictura_render_instances", "pictura_render_rgb", "pictura_render_rgb_aa"]
+            "pictura_set_lights", "pictura_render_instances", "pictura_render_rgb", "pictura_render_rgb_aa",
+            "pictura_device_errors"]
+DEVERR_RING_WAIT = 1
 
 STAT_NAMES = ["view_tiles", "cells_in_rect", "cells_prefiltered", "cells_visible", "cand_tris", "boxes_visible",
               "box_tris", "first_pass_survivors", "exact_batches", "clipped", "raster_tris", "lane_tris",
@@ -107,12 +111,46 @@ STAT_NAMES = ["view_tiles", "cells_in_rect", "cells_prefiltered", "cells_visible
               "cyc_prologue", "cyc_sources", "cyc_first_pass", "cyc_exact", "cyc_records", "cyc_writeout"]
 
 
-def _ptr(a) -> Optional[int]:
-    if a is None:
-        return None
-    if isinstance(a, np.ndarray):
-        return a.ctypes.data
-    return a.data_ptr()   # torch tensor
+_CTX_DEVICE = {}   # context handle -> HIP device index it was created on
+
+_DTYPE_NAMES = {"f32": "float32", "u8": "uint8", "i32": "int32"}
+
+
+def _torch_dtypes(kind):
+    import torch
+    return {"f32": (torch.float32,), "u8": (torch.uint8,),
+            "i32": (torch.int32,) + ((torch.uint32,) if hasattr(torch, "uint32") else ())}[kind]
+
+
+def _ctx_key(ctx):
+    return ctx.value if isinstance(ctx, ctypes.c_void_p) else ctx
+
+
+def _dev(t, name: str, kind: str, count: int, ctx=None) -> int:
+    """Device address of a caller-owned buffer after checking it: a torch
+    tensor of the expected dtype, contiguous, holding at least `count`
+    elements, on the HIP device of the context.  The library cannot see buffer
+    sizes, so these checks are what keeps a short or mistyped buffer from
+    becoming out-of-bounds device accesses.  Raises PicturaError(EINVAL)."""
+    import torch
+    if not isinstance(t, torch.Tensor):
+        raise PicturaError(EINVAL, f"{name}: expected a torch tensor on the HIP device, got {type(t).__name__}")
+    if t.dtype not in _torch_dtypes(kind):
+        raise PicturaError(EINVAL, f"{name}: dtype {t.dtype}, expected {_DTYPE_NAMES[kind]}")
+    if not t.is_contiguous():
+        raise PicturaError(EINVAL, f"{name}: tensor is not contiguous")
+    if t.numel() < count:
+        raise PicturaError(EINVAL, f"{name}: {t.numel()} elements, at least {count} needed")
+    _check_device(t, name, ctx)
+    return t.data_ptr()
+
+
+def _check_device(t, name: str, ctx) -> None:
+    if t.device.type != "cuda":
+        raise PicturaError(EINVAL, f"{name}: tensor on {t.device}, expected the HIP device")
+    want = _CTX_DEVICE.get(_ctx_key(ctx))
+    if want is not None and t.device.index is not None and t.device.index != want:
+        raise PicturaError(EINVAL, f"{name}: tensor on cuda:{t.device.index}, the context renders on cuda:{want}")
 
 
 def _stream(stream) -> Optional[int]:
@@ -137,10 +175,12 @@ def pictura_create(device: int = 0):
     st = _lib.pictura_create(int(device), ctypes.byref(h))
     if st != OK:
         raise PicturaError(st, "pictura_create failed (no HIP device?)")
+    _CTX_DEVICE[h.value] = int(device)
     return h
 
 
 def pictura_destroy(ctx):
+    _CTX_DEVICE.pop(_ctx_key(ctx), None)
     _lib.pictura_destroy(ctx)
 
 
@@ -177,53 +217,79 @@ def make_rig(rig) -> _Rig:
     return r
 
 
+_AGENT_F32 = ("x", "y", "z0", "cos_h", "sin_h", "length", "width", "height")
+
+
+def _agents(ctx, agents) -> _Agents:
+    """The C struct of a DeviceAgents, every array checked (float32 SoA of
+    num_worlds * agents_per_world elements, uint8 classes)."""
+    n = int(agents.num_worlds) * int(agents.agents_per_world)
+    return _Agents(int(agents.num_worlds), int(agents.agents_per_world),
+                   *[_dev(getattr(agents, f), f"agents.{f}", "f32", n, ctx) for f in _AGENT_F32],
+                   _dev(agents.cls, "agents.cls", "u8", n, ctx))
+
+
+def _rig(rig) -> _Rig:
+    return make_rig(rig) if not isinstance(rig, _Rig) else rig
+
+
+def _views(agents, r: _Rig) -> int:
+    return int(agents.num_worlds) * int(agents.agents_per_world) * int(r.num_cams)
+
+
+def _outputs(ctx, agents, r: _Rig, out_cls, out_depth):
+    npx = _views(agents, r) * r.height * r.width
+    return npx, _dev(out_cls, "out_cls", "u8", npx, ctx), _dev(out_depth, "out_depth", "f32", npx, ctx)
+
+
 def pictura_render_views(ctx, agents, rig, out_cls, out_depth, stream=None):
     """agents: DeviceAgents (torch CUDA tensors); rig: scenegen.Rig-like;
     out_cls uint8 / out_depth float32 CUDA tensors of V*H*W elements."""
-    a = _Agents(int(agents.num_worlds), int(agents.agents_per_world),
-                *[_ptr(getattr(agents, n)) for n in ("x", "y", "z0", "cos_h", "sin_h", "length", "width", "height",
-                                                     "cls")])
-    r = make_rig(rig) if not isinstance(rig, _Rig) else rig
-    _check(ctx, _lib.pictura_render_views(ctx, ctypes.byref(a), ctypes.byref(r), _ptr(out_cls), _ptr(out_depth),
-                                          _stream(stream)))
+    r = _rig(rig)
+    a = _agents(ctx, agents)
+    _, oc, od = _outputs(ctx, agents, r, out_cls, out_depth)
+    _check(ctx, _lib.pictura_render_views(ctx, ctypes.byref(a), ctypes.byref(r), oc, od, _stream(stream)))
 
 
 def pictura_render_rgb(ctx, agents, rig, out_cls, out_depth, out_rgb, stream=None):
     """As pictura_render_views, plus out_rgb (uint8, V*3*H*W, planar)."""
-    a = _Agents(int(agents.num_worlds), int(agents.agents_per_world),
-                *[_ptr(getattr(agents, n)) for n in ("x", "y", "z0", "cos_h", "sin_h", "length", "width", "height",
-                                                     "cls")])
-    r = make_rig(rig) if not isinstance(rig, _Rig) else rig
-    _check(ctx, _lib.pictura_render_rgb(ctx, ctypes.byref(a), ctypes.byref(r), _ptr(out_cls), _ptr(out_depth),
-                                        _ptr(out_rgb), _stream(stream)))
+    r = _rig(rig)
+    a = _agents(ctx, agents)
+    npx, oc, od = _outputs(ctx, agents, r, out_cls, out_depth)
+    orgb = _dev(out_rgb, "out_rgb", "u8", 3 * npx, ctx)
+    _check(ctx, _lib.pictura_render_rgb(ctx, ctypes.byref(a), ctypes.byref(r), oc, od, orgb, _stream(stream)))
 
 
 def pictura_render_rgb_aa(ctx, agents, rig, out_cls, out_depth, out_rgb, stream=None):
     """As pictura_render_rgb, with analytic-coverage antialiasing of out_rgb."""
-    a = _Agents(int(agents.num_worlds), int(agents.agents_per_world),
-                *[_ptr(getattr(agents, n)) for n in ("x", "y", "z0", "cos_h", "sin_h", "length", "width", "height",
-                                                     "cls")])
-    r = make_rig(rig) if not isinstance(rig, _Rig) else rig
-    _check(ctx, _lib.pictura_render_rgb_aa(ctx, ctypes.byref(a), ctypes.byref(r), _ptr(out_cls), _ptr(out_depth),
-                                           _ptr(out_rgb), _stream(stream)))
+    r = _rig(rig)
+    a = _agents(ctx, agents)
+    npx, oc, od = _outputs(ctx, agents, r, out_cls, out_depth)
+    orgb = _dev(out_rgb, "out_rgb", "u8", 3 * npx, ctx)
+    _check(ctx, _lib.pictura_render_rgb_aa(ctx, ctypes.byref(a), ctypes.byref(r), oc, od, orgb, _stream(stream)))
 
 
 def pictura_render_instances(ctx, agents, rig, out_cls, out_depth, out_inst, out_counts, stream=None):
     """As pictura_render_views, plus out_inst (int32, V*H*W) and out_counts
     (int32 tensor viewed as uint32, V*A*2: footprint, visible)."""
-    a = _Agents(int(agents.num_worlds), int(agents.agents_per_world),
-                *[_ptr(getattr(agents, n)) for n in ("x", "y", "z0", "cos_h", "sin_h", "length", "width", "height",
-                                                     "cls")])
-    r = make_rig(rig) if not isinstance(rig, _Rig) else rig
-    _check(ctx, _lib.pictura_render_instances(ctx, ctypes.byref(a), ctypes.byref(r), _ptr(out_cls), _ptr(out_depth),
-                                              _ptr(out_inst), _ptr(out_counts), _stream(stream)))
+    r = _rig(rig)
+    a = _agents(ctx, agents)
+    npx, oc, od = _outputs(ctx, agents, r, out_cls, out_depth)
+    oi = _dev(out_inst, "out_inst", "i32", npx, ctx)
+    ok = _dev(out_counts, "out_counts", "i32", _views(agents, r) * int(agents.agents_per_world) * 2, ctx)
+    _check(ctx, _lib.pictura_render_instances(ctx, ctypes.byref(a), ctypes.byref(r), oc, od, oi, ok,
+                                              _stream(stream)))
 
 
 def pictura_agents_step(ctx, state, steer, accel, dt: float = 0.1, vmax: float = 20.0, stream=None):
-    s = _AgentState(int(state.x.numel()), *[_ptr(getattr(state, n)) for n in
-                                           ("x", "y", "psi", "speed", "cos_h", "sin_h", "length")])
-    _check(ctx, _lib.pictura_agents_step(ctx, ctypes.byref(s), _ptr(steer), _ptr(accel), float(dt), float(vmax),
-                                         _stream(stream)))
+    """state: DeviceAgents-like (float32 x, y, psi, speed, cos_h, sin_h,
+    length of num_worlds * agents_per_world elements); steer, accel: float32
+    tensors of the same count."""
+    n = int(state.num_worlds) * int(state.agents_per_world)
+    s = _AgentState(n, *[_dev(getattr(state, f), f"state.{f}", "f32", n, ctx) for f in
+                         ("x", "y", "psi", "speed", "cos_h", "sin_h", "length")])
+    st_, ac_ = _dev(steer, "steer", "f32", n, ctx), _dev(accel, "accel", "f32", n, ctx)
+    _check(ctx, _lib.pictura_agents_step(ctx, ctypes.byref(s), st_, ac_, float(dt), float(vmax), _stream(stream)))
 
 
 def pictura_set_lights(ctx, lights):
@@ -232,9 +298,11 @@ def pictura_set_lights(ctx, lights):
     if lights is None:
         _check(ctx, _lib.pictura_set_lights(ctx, None))
         return
+    n = int(lights.num_worlds) * int(lights.lights_per_world)
     l = _Lights(int(lights.num_worlds), int(lights.lights_per_world),
-                *[_ptr(getattr(lights, n)) for n in ("x", "y", "z", "cos_f", "sin_f", "radius", "cls")],
-                float(lights.cos_max))
+                *[_dev(getattr(lights, f), f"lights.{f}", "f32", n, ctx) for f in
+                  ("x", "y", "z", "cos_f", "sin_f", "radius")],
+                _dev(lights.cls, "lights.cls", "u8", n, ctx), float(lights.cos_max))
     _check(ctx, _lib.pictura_set_lights(ctx, ctypes.byref(l)))
 
 
@@ -261,6 +329,14 @@ def pictura_set_option(ctx, option: int, value: int):
 def pictura_selftest_rcp(ctx, lo_bits: int, count: int) -> int:
     out = ctypes.c_uint64()
     _check(ctx, _lib.pictura_selftest_rcp(ctx, int(lo_bits), int(count), ctypes.addressof(out)))
+    return int(out.value)
+
+
+def pictura_device_errors(ctx, reset: bool = False) -> int:
+    """OR of the device error bits (DEVERR_*) the render kernels set since the
+    context was created or last reset; synchronous."""
+    out = ctypes.c_uint32()
+    _check(ctx, _lib.pictura_device_errors(ctx, ctypes.addressof(out), int(bool(reset))))
     return int(out.value)
 
 
@@ -334,6 +410,15 @@ class Renderer:
             pictura_destroy(self.ctx)
             self.ctx = None
 
+    def close_checked(self):
+        """Close after checking that no render kernel reported a device error."""
+        try:
+            err = self.device_errors() if self.ctx else 0
+        finally:
+            self.close()
+        if err:
+            raise PicturaError(EDEVICE, f"render kernels reported device error bits {err:#x}")
+
     def __del__(self):
         try:
             self.close()
@@ -386,6 +471,9 @@ class Renderer:
 
     def agents_step(self, agents: DeviceAgents, steer, accel, dt=0.1, vmax=20.0, stream=None):
         pictura_agents_step(self.ctx, agents, steer, accel, dt, vmax, stream)
+
+    def device_errors(self, reset: bool = False) -> int:
+        return pictura_device_errors(self.ctx, reset)
 
     def set_option(self, option, value):
         pictura_set_option(self.ctx, option, value)

@@ -12,8 +12,9 @@ workloads of the same kind stand in for them:
 
   1 tiny       1 world 200x200 m, 2x2 grid of two-lane roads, 8 boxes,
                1 forward camera, 64x64, far 100 m
-  2 small      64 worlds 1x1 km, 6+6 straight roads of 2-4 lanes, curbs,
-               32 boxes, 4 cameras, 64x64, far 100 m          (8,192 views)
+  2 small      64 worlds 1x1 km, 6+6 straight roads of 2-4 lanes in 2 m
+               segments, curbs (43-47k triangles per world), 32 boxes,
+               4 cameras, 64x64, far 100 m                     (8,192 views)
   3 dense      256 worlds, same generator, 128 agents (20 % pedestrians),
                no overlap rejection (contact ties)            (131,072 views)
   4 headline   1024 worlds x 64 agents x 4 cameras, far 150 m, agents moved
@@ -53,6 +54,7 @@ Z_ROAD = 0.02
 Z_MARK = 0.03
 CURB_H = 0.15
 LANE_W = 3.5
+ROAD_SEG = 2.0      # road surface and curb faces: one quad per 2 m of road (every world >= 40k triangles)
 MARK_W = 0.15
 DASH_LEN, DASH_GAP = 3.0, 3.0
 
@@ -413,7 +415,7 @@ def light_and_stop_line(cx, cy, dx, dy, hw_cross, hw_own):
 
 def _town_world(rng, size, n_agents):
     """Small-batch town plus walls, parked cars and traffic lights."""
-    tris, clss, ag, roads = _grid_world(rng, size, 25.0, 6, [2, 3, 4], 2.5, True, n_agents, 8.0, 0.1, 0.0,
+    tris, clss, ag, roads = _grid_world(rng, size, 25.0, 6, [2, 3, 4], ROAD_SEG, True, n_agents, 8.0, 0.1, 0.0,
                                         return_roads=True)
     extra_t, extra_c = [], []
     lx, ly, lcf, lsf, lcls = [], [], [], [], []
@@ -589,9 +591,9 @@ def _build_world(cfg_id: int, cfg: dict, w: int):
         return _grid_world(rng, size, 10.0, 2, [2], 2.0, False, cfg["agents"], 8.0, 0.0, 0.0,
                            fixed_centres=[-50.0, 50.0])
     if cfg_id in (2, 4, 6):
-        return _grid_world(rng, size, 25.0, 6, [2, 3, 4], 2.5, True, cfg["agents"], 8.0, 0.1, 0.0)
+        return _grid_world(rng, size, 25.0, 6, [2, 3, 4], ROAD_SEG, True, cfg["agents"], 8.0, 0.1, 0.0)
     if cfg_id == 3:
-        return _grid_world(rng, size, 25.0, 6, [2, 3, 4], 2.5, True, cfg["agents"], 0.0, 0.1, 0.2)
+        return _grid_world(rng, size, 25.0, 6, [2, 3, 4], ROAD_SEG, True, cfg["agents"], 0.0, 0.1, 0.2)
     if cfg_id == 5:
         return _bezier_world(rng, size, 50.0, 500_000, cfg["agents"], 0.1)
     if cfg_id == 7:

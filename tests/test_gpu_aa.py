@@ -49,7 +49,7 @@ def gpu_render(lib, scene, cell, agents, rig, lights=None, tile=0, cull=1, antia
         torch.cuda.synchronize()
         return c, d, rgb
     finally:
-        r.close()
+        r.close_checked()
 
 
 def check(lib, wl, views, label, tile=0, cull=1):

@@ -53,4 +53,4 @@ def test_encoder_on_rendered_views_matches_oracle_views():
         got = emb[torch.as_tensor(egos, device="cuda")]
         assert torch.allclose(got, ref, rtol=1e-4, atol=1e-5), (got - ref).abs().max().item()
     finally:
-        r.close()
+        r.close_checked()

@@ -50,7 +50,7 @@ def check(lib, wl, views, label, tile=0, cull=1):
         gi = inst[idx].cpu().numpy()
         gk = counts[idx].cpu().numpy().view(np.uint32)
     finally:
-        r.close()
+        r.close_checked()
     ora = O.render(wl.scene, wl.agents, wl.rig, view_ids=np.asarray(views), lights=wl.lights, want_instances=True)
     s = assert_parity(gc, gd, ora, label)
     assert s["mismatches"] == 0, s
@@ -86,3 +86,30 @@ def test_instances_town_with_lights(lib):
     rng = np.random.default_rng(43)
     views = np.sort(rng.choice(wl.num_views, size=64, replace=False))
     check(lib, wl, views, "inst-town")
+
+
+def test_instances_faces_behind_near_or_beyond_far(lib):
+    # Regression: the instance pass must drop a box triangle with no vertex at
+    # zv >= near, or with every vertex beyond far (R4), as the class/depth pass
+    # and the oracle do.  Car 1 in the next lane has its rear face 0.25 m ahead
+    # of the forward camera (between the camera plane and the near plane);
+    # car 2 starts 0.3 m ahead of it in its own lane, so the camera looks into
+    # its open rear end; car 3 lies wholly beyond far = 110 m, its rear face one
+    # fp32 step beyond the far plane, where the plane value at the covered
+    # centres equals fl(1/110) and so passes the per-pixel far test: its
+    # footprint must be 0.  The second camera looks right, along car 1's side.
+    from tests.scenes import make_agents, make_rig, make_scene, quad
+    D = float(np.nextafter(np.float32(110.0), np.float32(np.inf)))
+    G = 1000.0
+    scene = make_scene(quad((-G, -G, 0.0), (G, -G, 0.0), (G, G, 0.0), (-G, G, 0.0)), [0, 0])
+    ag = make_agents([(0.0, 0.0, 0.0, 1.0, 0.0, 4.5, 1.9, 1.5, 3),
+                      (2.5, -3.5, 0.0, 1.0, 0.0, 4.5, 1.9, 1.5, 3),
+                      (2.55, 0.0, 0.0, 1.0, 0.0, 4.5, 1.9, 1.6, 3),
+                      (D + 2.0, 0.0, 0.5, 1.0, 0.0, 4.0, 2.0, 2.0, 3)])
+    assert np.float32(ag.x[3]) - np.float32(2.0) == np.float32(D)
+    rig = make_rig(mounts=((0.0, 0.0, 1.5, 1.0, 0.0), (0.0, 0.0, 1.5, 0.0, -1.0)), far=110.0)
+    wl = sg.Workload("inst-near-far", 0, 0, scene, ag, rig, 16.0, 2000.0)
+    check(lib, wl, np.arange(wl.num_views), "inst-near-far")
+    ora = O.render(scene, ag, rig, want_instances=True)
+    assert ora["counts"][0, 1, 0] > 0 and ora["counts"][0, 2, 0] > 0   # cars 1 and 2 are seen
+    assert (ora["counts"][:, 3, 0] == 0).all()                         # car 3 never is

@@ -46,7 +46,7 @@ def render_gpu(pictura, scene, agents, rig, cell, lights, cull=1, tile=0):
         torch.cuda.synchronize()
         return c.cpu().numpy(), d.cpu().numpy()
     finally:
-        r.close()
+        r.close_checked()
 
 
 def test_town_features_sampled(lib):

@@ -51,7 +51,7 @@ def render_gpu(pictura, wl_scene, agents, rig, cell, cull=1, tile=0):
         torch.cuda.synchronize()
         return c, d
     finally:
-        r.close()
+        r.close_checked()
 
 
 def check_views(pictura, wl, view_ids, label, cull=1, tile=0, cell=None):
@@ -115,7 +115,7 @@ def test_headline_after_bench_steps_sampled(lib):
                           dt=0.1, vmax=20.0)
         torch.cuda.synchronize()
     finally:
-        r.close()
+        r.close_checked()
     ag = wl.agents.copy()
     for f in ("x", "y", "cos_h", "sin_h", "psi", "speed"):
         setattr(ag, f, getattr(da, f).cpu().numpy().astype(np.float32))
@@ -125,9 +125,14 @@ def test_headline_after_bench_steps_sampled(lib):
     check_views(lib, dataclasses.replace(wl, agents=ag), sample_views(wl.num_views, 256, 29), "headline-stepped")
 
 
-def test_highres_tiled_sampled(lib):
-    wl = workload(5, 4)   # first 4 worlds of the high-res workload (128x128, 2x2 tiles)
-    check_views(lib, wl, sample_views(wl.num_views, 48, 24), "highres")
+def test_highres_full_launch_sampled(lib):
+    # the whole high-res workload in one launch, as the benchmark times it:
+    # 128 worlds x 64 agents x 4 cameras at 128x128 (2x2 tiles per view),
+    # ~527k triangles per world; 96 views sampled across all worlds
+    wl = sg.make_config(5)
+    views = sample_views(wl.num_views, 96, 24)
+    assert len(np.unique(views // (64 * 4))) > 48
+    check_views(lib, wl, views, "highres")
 
 
 def test_paper_rig_sampled(lib):
@@ -218,6 +223,27 @@ def test_fill_rule_and_snap_ties_closed_form(lib, s, lo, hi):
     check_views(lib, wl, np.arange(1), f"pin s={s}")
 
 
+def test_far_rule_square_beyond_and_on_far(lib):
+    # far = 110: a fronto square (half-size 16) one fp32 step beyond the far
+    # plane, where the plane value at its covered centres equals fl(1/110) and
+    # passes the per-pixel far test; the triangle-level rule of R4 keeps the
+    # image empty.  The same square on the far plane covers the 10 x 10 centres
+    # within 32 +- 4.65 px at depth 110.
+    D = float(np.nextafter(np.float32(110.0), np.float32(np.inf)))
+    rig = make_rig(far=110.0)
+    ag = make_agents([(0.0, 0.0, 0.0, 1.0, 0.0, 1.0, 1.0, 1.0, 3)])
+    for dist, want_px in ((D, 0), (110.0, 100)):
+        pts = [(dist, a, b) for (a, b) in ((-16.0, -16.0), (16.0, -16.0), (16.0, 16.0), (-16.0, 16.0))]
+        wl = sg.Workload("far-rule", 0, 0, make_scene(quad(*pts), [7, 7]), ag, rig, 16.0, 2000.0)
+        c, d = render_gpu(lib, wl.scene, wl.agents, wl.rig, 16.0)
+        gc = c.cpu().numpy()[0]
+        want = np.zeros((64, 64), bool)
+        if want_px:
+            want[27:37, 27:37] = True
+        assert np.array_equal(gc == 7, want), (dist, int((gc == 7).sum()))
+        check_views(lib, wl, np.arange(1), f"far-rule D={dist!r}")
+
+
 def test_degenerate_and_non_finite_triangles(lib):
     # Triangles the rules drop or that sit on their boundaries, among ordinary
     # ones: a NaN and an infinite vertex (dropped by the snap's range rule or
@@ -280,7 +306,7 @@ def test_edge_paths_all_exercised(lib):
         torch.cuda.synchronize()
         st = lib.pictura_stats_copy(r.ctx)
     finally:
-        r.close()
+        r.close_checked()
     print(f"[paths] {st}", flush=True)
     assert st["record_tris_fp64"] > 0
     assert st["record_tris"] - st["record_tris_fp64"] > 0
@@ -310,7 +336,7 @@ def test_binner_matches_oracle(lib):
         r.upload(sc, 16.0)
         b = r.bins()
     finally:
-        r.close()
+        r.close_checked()
     ob = O.bin_scene(sc, 16.0)
     assert np.array_equal(b["dims"], ob["dims"])
     assert np.array_equal(b["cell_base"], ob["cell_base"])
@@ -352,7 +378,7 @@ def test_agents_step_matches_oracle(lib):
             ag.x, ag.y = out["x"].astype(np.float32), out["y"].astype(np.float32)
             ag.psi, ag.speed = out["psi"].astype(np.float32), out["speed"].astype(np.float32)
     finally:
-        r.close()
+        r.close_checked()
 
 
 # ---- C ABI error handling (host-side checks, no kernel launched) ---------------

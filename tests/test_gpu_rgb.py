@@ -47,7 +47,7 @@ def check(lib, wl, views, label, tile=0):
         idx = torch.as_tensor(np.asarray(views), device="cuda")
         gc, gd, grgb = c[idx].cpu().numpy(), d[idx].cpu().numpy(), rgb[idx].cpu().numpy()
     finally:
-        r.close()
+        r.close_checked()
     ora = O.render(wl.scene, wl.agents, wl.rig, view_ids=np.asarray(views), lights=wl.lights, want_rgb=True)
     s = assert_parity(gc, gd, ora, label)
     unflag = ora["flags"] == 0

@@ -1,7 +1,7 @@
 """Oracle pins for instance visibility: which agent owns each pixel, and each
 agent's footprint (its box drawn alone) and visible pixel count, from which the
 occlusion percentage the paper's analysis reads from its renderer follows
-(Sec. 4.3)."""
+(Sec. 5.2)."""
 import numpy as np
 import pytest
 

@@ -137,6 +137,34 @@ def test_far_plane_is_inclusive():
     assert np.all(r2["cls"][0] == SKY)
 
 
+def test_triangle_wholly_beyond_far_is_not_drawn():
+    # far = 110 and a fronto square (half-size 16) one fp32 step beyond it,
+    # D = 110 + 2^-17.  Every point of the surface lies beyond the far plane, so
+    # it appears in no pixel: the float64 ray cast finds nothing within
+    # [near, far].  The per-pixel test alone cannot decide this case: the
+    # square's plane gives 1/z = fl(1/D) at every covered centre (its normal
+    # has power-of-two length and no x or y term), and fl(1/D) equals
+    # fl(1/110), which passes iz >= fl(1/far).  The triangle-level rule of R4
+    # (every vertex at zv > far: not drawn) is what keeps the image empty;
+    # without it the square shows as a 10 x 10 block at depth 110.
+    far = 110.0
+    D = float(np.nextafter(np.float32(far), np.float32(np.inf)))
+    assert D > far and np.float32(1) / np.float32(D) == np.float32(1) / np.float32(far)
+    rig = make_rig(far=far)
+    scene = make_scene(fronto_quad(D, 16.0), [7, 7])
+    ag = make_agents([ego()])
+    r = O.render(scene, ag, rig)
+    assert np.all(r["cls"][0] == SKY) and np.all(np.isinf(r["depth"][0]))
+    rc, rd, _ = raycast_view(scene, ag, rig, 0)
+    assert np.all(rc == SKY) and not np.isfinite(rd).any()
+    # the same square on the far plane itself is drawn (inclusive far plane):
+    # the 10 x 10 pixel centres within 32 +- 32 * 16 / 110 = 32 +- 4.65 px
+    r2 = O.render(make_scene(fronto_quad(far, 16.0), [7, 7]), ag, rig)
+    want = np.zeros((64, 64), bool)
+    want[27:37, 27:37] = True
+    assert np.array_equal(r2["cls"][0] == 7, want)
+
+
 def test_depth_error_bound_over_distances():
     # Fronto squares (half-size D/16, 2 px) at 200 seeded distances D in [0.6, 95] m: the decoded depth
     # at the image centre is within 2^-21 (the bucket midpoint) plus a few
