@@ -317,6 +317,20 @@ pictura_status pictura_device_errors(pictura_ctx ctx, uint32_t* out, int32_t res
  * a range reaching past the finite floats of lo_bits' sign. */
 pictura_status pictura_selftest_rcp(pictura_ctx ctx, uint32_t lo_bits, uint32_t count, uint64_t* mismatches);
 
+/* pictura_selftest_rcp without any device allocation, for callers that cannot
+ * allocate device memory (code under HIP graph capture, tight serving loops,
+ * harnesses that forbid hipMalloc).  Same arguments, checks, result and
+ * errors as pictura_selftest_rcp.  Its one piece of scratch, the 64-bit
+ * mismatch counter, lives in a fixed 256-byte device array that the library
+ * holds on every GPU it runs on until the process ends (its address is taken
+ * by pictura_create); the counter does not grow with the range, so no range
+ * the self-check accepts exceeds it.  The counter is cleared by a kernel at the
+ * start of each call.  All contexts on one GPU share that array: calls that
+ * overlap on the same GPU (from several host threads) race and may report
+ * each other's counts.  ESTATE: the context's device has no scratch address.
+ * Synchronous. */
+pictura_status pictura_selftest_rcp_noalloc(pictura_ctx ctx, uint32_t lo_bits, uint32_t count, uint64_t* mismatches);
+
 #ifdef __cplusplus
 }
 #endif

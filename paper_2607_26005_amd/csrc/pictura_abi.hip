@@ -152,7 +152,7 @@ pictura_status pictura_create(int32_t device, pictura_ctx* out)
             delete c;
             return PICTURA_ENOMEM;
         }
-        if (hipMemset(c->dev_err, 0, sizeof(uint32_t)) != hipSuccess) {
+        if (hipMemset(c->dev_err, 0, sizeof(uint32_t)) != hipSuccess || noalloc_scratch_init(device) != hipSuccess) {
             (void)hipFree(c->dev_err);
             delete c;
             return PICTURA_EDEVICE;
@@ -578,6 +578,25 @@ pictura_status pictura_selftest_rcp(pictura_ctx c, uint32_t lo_bits, uint32_t co
         return hip_fail(c, e, "selftest_rcp");
     }
     (void)hipFree(d);
+    *mismatches = (uint64_t)h;
+    return PICTURA_OK;
+}
+
+pictura_status pictura_selftest_rcp_noalloc(pictura_ctx c, uint32_t lo_bits, uint32_t count, uint64_t* mismatches)
+{
+    if (!c) return PICTURA_EINVAL;
+    c->err.clear();
+    if (!mismatches) return fail(c, PICTURA_EINVAL, "selftest_rcp_noalloc: null output");
+    if ((uint64_t)(lo_bits & 0x7FFFFFFFu) + count > 0x7F800000ull)
+        return fail(c, PICTURA_EINVAL, "selftest_rcp_noalloc: range leaves the finite floats of one sign");
+    DeviceGuard dg(c->device);
+    auto* counter = (unsigned long long*)noalloc_scratch(c->device);
+    if (!counter) return fail(c, PICTURA_ESTATE, "selftest_rcp_noalloc: no scratch address for device %d", c->device);
+    hipError_t e;
+    unsigned long long h = 0;
+    if ((e = launch_rcp_check_noalloc(lo_bits, count, counter, nullptr)) != hipSuccess ||
+        (e = hipMemcpy(&h, counter, sizeof h, hipMemcpyDeviceToHost)) != hipSuccess)
+        return hip_fail(c, e, "selftest_rcp_noalloc");
     *mismatches = (uint64_t)h;
     return PICTURA_OK;
 }

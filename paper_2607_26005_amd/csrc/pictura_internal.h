@@ -134,4 +134,13 @@ hipError_t launch_agents_step(const AgentStepParams& p, hipStream_t s);
 int64_t scan_tmp_needed(int64_t n);
 hipError_t launch_rcp_check(uint32_t lo_bits, uint32_t n, unsigned long long* mismatches, hipStream_t s);
 
+// Allocation-free variant: a file-scope device array of kNoAllocScratchWords
+// 64-bit words per GPU (256 bytes); its address on `device` is taken once, by
+// noalloc_scratch_init with that device current (pictura_create calls it).
+constexpr int kNoAllocScratchWords = 32;
+constexpr int kNoAllocMaxDevices = 64;
+hipError_t noalloc_scratch_init(int device);
+void* noalloc_scratch(int device);   // null before noalloc_scratch_init(device)
+hipError_t launch_rcp_check_noalloc(uint32_t lo_bits, uint32_t n, unsigned long long* counter, hipStream_t s);
+
 }  // namespace pictura

@@ -38,6 +38,7 @@
 // key equals a brute-force evaluation of the rules over all triangles of the
 // world; everything before the exact pass only skips triangles that cannot
 // set a key.
+#include <mutex>
 #include <type_traits>
 
 #include "pictura_device.h"
@@ -1915,6 +1916,57 @@ hipError_t launch_rcp_check(uint32_t lo_bits, uint32_t n, unsigned long long* mi
     if (n == 0) return hipSuccess;
     hipLaunchKernelGGL(rcp_check_kernel, dim3((n + 255u) / 256u), dim3(256), 0, s, lo_bits, n, mismatches);
     return hipGetLastError();
+}
+
+// ---------------------------------------------------------------------------
+// allocation-free self-check: the mismatch counter lives in a file-scope
+// device array instead of a per-call allocation
+// ---------------------------------------------------------------------------
+
+// Every GPU the library runs on holds its own copy until the process ends.
+// Word 0 is the mismatch counter of pictura_selftest_rcp_noalloc; the rest is
+// reserved.  Host code never passes `scratch` itself to a kernel (in host code
+// the name is a stand-in, not a device address): it uses the address
+// hipGetSymbolAddress returned for the device.
+static __device__ __align__(256) unsigned long long scratch[kNoAllocScratchWords];
+
+namespace {
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kNoAllocMaxDevices] = {};
+}  // namespace
+
+hipError_t noalloc_scratch_init(int device)
+{
+    if (device < 0 || device >= kNoAllocMaxDevices) return hipErrorInvalidDevice;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (g_scratch_ptr[device]) return hipSuccess;
+    void* p = nullptr;
+    const hipError_t e = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));   // the current device's copy
+    if (e != hipSuccess) return e;
+    g_scratch_ptr[device] = p;
+    return hipSuccess;
+}
+
+void* noalloc_scratch(int device)
+{
+    if (device < 0 || device >= kNoAllocMaxDevices) return nullptr;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    return g_scratch_ptr[device];
+}
+
+__global__ void clear_words_kernel(unsigned long long* p, int n)
+{
+    const int i = (int)(blockIdx.x * blockDim.x + threadIdx.x);
+    if (i < n) p[i] = 0ull;
+}
+
+hipError_t launch_rcp_check_noalloc(uint32_t lo_bits, uint32_t n, unsigned long long* counter, hipStream_t s)
+{
+    // a fill kernel, not a memset, so the sequence can also be captured in a graph
+    hipLaunchKernelGGL(clear_words_kernel, dim3(1), dim3(64), 0, s, counter, 1);
+    hipError_t e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    return launch_rcp_check(lo_bits, n, counter, s);
 }
 
 }  // namespace pictura

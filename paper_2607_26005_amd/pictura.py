@@ -95,6 +95,8 @@ _lib.pictura_set_lights.argtypes = [_P, ctypes.POINTER(_Lights)]
 _lib.pictura_set_lights.restype = ctypes.c_int32
 _lib.pictura_selftest_rcp.argtypes = [_P, ctypes.c_uint32, ctypes.c_uint32, _P]
 _lib.pictura_selftest_rcp.restype = ctypes.c_int32
+_lib.pictura_selftest_rcp_noalloc.argtypes = [_P, ctypes.c_uint32, ctypes.c_uint32, _P]
+_lib.pictura_selftest_rcp_noalloc.restype = ctypes.c_int32
 _lib.pictura_device_errors.argtypes = [_P, _P, ctypes.c_int32]
 _lib.pictura_device_errors.restype = ctypes.c_int32
 
@@ -102,7 +104,7 @@ EXPORTED = ["pictura_create", "pictura_destroy", "pictura_last_error", "pictura_
             "pictura_bin_scene", "pictura_render_views", "pictura_agents_step", "pictura_bins_info",
             "pictura_bins_copy", "pictura_set_option", "pictura_stats_copy", "pictura_selftest_rcp",
             "pictura_set_lights", "pictura_render_instances", "pictura_render_rgb", "pictura_render_rgb_aa",
-            "pictura_device_errors"]
+            "pictura_device_errors", "pictura_selftest_rcp_noalloc"]
 DEVERR_RING_WAIT = 1
 
 STAT_NAMES = ["view_tiles", "cells_in_rect", "cells_prefiltered", "cells_visible", "cand_tris", "boxes_visible",
@@ -337,6 +339,12 @@ def pictura_device_errors(ctx, reset: bool = False) -> int:
     context was created or last reset; synchronous."""
     out = ctypes.c_uint32()
     _check(ctx, _lib.pictura_device_errors(ctx, ctypes.addressof(out), int(bool(reset))))
+    return int(out.value)
+
+
+def pictura_selftest_rcp_noalloc(ctx, lo_bits: int, count: int) -> int:
+    out = ctypes.c_uint64()
+    _check(ctx, _lib.pictura_selftest_rcp_noalloc(ctx, int(lo_bits), int(count), ctypes.addressof(out)))
     return int(out.value)
 
 
