@@ -3,12 +3,13 @@
 One step = the kinematic bicycle update of every agent followed by rendering
 every agent's camera views (class + depth) through the C ABI.  Default
 workload: 1024 worlds x 64 agents x 4 cameras at 64x64 (262,144 views per
-step), ~37k static triangles per world, far plane 150 m, seeded synthetic
-inputs resident in HBM before timing.
+step), 44.8k static triangles per world on average, far plane 150 m, seeded
+synthetic inputs resident in HBM before timing.
 
 Prints one JSON line with agent-steps/s, images/s, the render kernel's HBM
-write roofline fraction (HIP events on the launch stream) and the CPU
-oracle timed on a bounded sample of the same workload.
+write roofline fraction (HIP events on the launch stream), the write rate a
+plain streaming-store kernel reaches on the same device in the same run, and
+the CPU oracle timed on a bounded sample of the same workload.
 
     python bench.py [--steps 100] [--warmup 10] [--config 4] [--no-cpu-baseline]
 
@@ -98,6 +99,18 @@ def copy_calibration():
     print(json.dumps({"copy_bytes_per_launch": n, "launches": 3}))
 
 
+def cpu_model() -> str:
+    try:
+        with open("/proc/cpuinfo") as f:
+            for line in f:
+                if line.startswith("model name"):
+                    return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    import platform
+    return platform.processor() or "unknown"
+
+
 def cpu_baseline(wl, target_s):
     from oracle import oracle as O
     threads = os.cpu_count() or 1
@@ -117,7 +130,7 @@ def cpu_baseline(wl, target_s):
     images_s = n / dt
     C = wl.rig.num_cams
     return {"value": images_s / C, "unit": "agent-steps/s", "cores": threads, "kind": "oracle",
-            "images_per_s": images_s,
+            "cpu_model": cpu_model(), "images_per_s": images_s,
             "sample": f"{n} seeded-random views of the same workload (brute force over every triangle of the "
                       f"view's world + every other agent's box), {dt:.1f} s wall on {threads} threads; "
                       f"agent-steps/s = images/s / {C} cameras"}
@@ -220,6 +233,25 @@ def main():
     print(f"# timed {K} steps: {total_ms:.2f} ms (wall {wall * 1e3:.1f} ms); render avg {avg_render_ms:.4f} ms "
           f"min {min(render_ms):.4f} max {max(render_ms):.4f}", file=sys.stderr, flush=True)
 
+    # measured HBM write reference in the same run: the library's store probe
+    # (16-byte non-temporal stores of zeros, the write-out's store pattern)
+    # over the depth output buffer, timed with events on the same stream
+    probe = out_depth.view(torch.uint8).reshape(-1)
+    probe = probe[: probe.numel() // 16 * 16]
+    for _ in range(2):
+        pictura.pictura_store_probe(r.ctx, probe)
+    ev_p0, ev_p1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    n_probe = 10
+    ev_p0.record(stream)
+    for _ in range(n_probe):
+        pictura.pictura_store_probe(r.ctx, probe)
+    ev_p1.record(stream)
+    torch.cuda.synchronize()
+    store_gbs = probe.numel() * n_probe / (ev_p0.elapsed_time(ev_p1) * 1e-3) / 1e9
+    dev_err = r.device_errors()
+    print(f"# store probe: {probe.numel() / 1e9:.2f} GB per launch, {store_gbs:.0f} GB/s; device errors {dev_err:#x}",
+          file=sys.stderr, flush=True)
+
     out_bytes = V * H * W * 5
     if out_rgb is not None:    # + 3 colour bytes per pixel
         out_bytes += V * H * W * 3
@@ -271,7 +303,10 @@ def main():
             "frac": achieved / HBM_PEAK_GBS,
             "algorithmic_bytes_per_launch": out_bytes,
             "traffic": traffic,
+            "measured_store_gbs": store_gbs,
+            "frac_of_measured_store": achieved / store_gbs,
         },
+        "device_errors": dev_err,
         "cpu_baseline": cpu,
     }
     if out_rgb is not None:

@@ -268,6 +268,14 @@ pictura_status pictura_agents_step(pictura_ctx ctx, const pictura_agent_state* s
 
 /* ---- introspection and test controls -------------------------------------- */
 
+/* Reference for the achievable HBM write rate (the render's roofline is an
+ * HBM write bound): writes `bytes` zero bytes to the device buffer dst with
+ * 16-byte non-temporal stores, the store pattern of the render's write-out,
+ * and nothing else.  dst must be 16-byte aligned and bytes a multiple of 16
+ * (EINVAL otherwise); dst must hold at least `bytes` bytes.  Asynchronous on
+ * `stream`: time it with events on that stream. */
+pictura_status pictura_store_probe(pictura_ctx ctx, void* dst, uint64_t bytes, void* stream);
+
 /* Grid geometry after pictura_bin_scene (host memory, synchronous: waits for
  * the binning to finish).  dims[w] = nx, ny; cell_base[w] = first cell of
  * world w (cell_base[num_worlds] = total cells).  Any pointer may be NULL. */

@@ -477,6 +477,19 @@ pictura_status pictura_agents_step(pictura_ctx c, const pictura_agent_state* s, 
     return PICTURA_OK;
 }
 
+pictura_status pictura_store_probe(pictura_ctx c, void* dst, uint64_t bytes, void* stream)
+{
+    if (!c) return PICTURA_EINVAL;
+    c->err.clear();
+    if (!dst) return fail(c, PICTURA_EINVAL, "store_probe: null buffer");
+    if ((reinterpret_cast<uintptr_t>(dst) & 15u) != 0 || (bytes & 15u) != 0)
+        return fail(c, PICTURA_EINVAL, "store_probe: buffer and size must be multiples of 16 bytes");
+    DeviceGuard dg(c->device);
+    const hipError_t e = launch_store_probe(dst, bytes, (hipStream_t)stream);
+    if (e != hipSuccess) return hip_fail(c, e, "store_probe launch");
+    return PICTURA_OK;
+}
+
 pictura_status pictura_bins_info(pictura_ctx c, int32_t* dims, int64_t* cell_base, int64_t* total_cells)
 {
     if (!c) return PICTURA_EINVAL;

@@ -213,4 +213,30 @@ hipError_t launch_agents_step(const AgentStepParams& p, hipStream_t s)
     return hipGetLastError();
 }
 
+// ---------------------------------------------------------------------------
+// streaming-store reference: zeros written with 16-byte non-temporal stores,
+// the store pattern of the render's write-out, at whatever rate HBM accepts
+// ---------------------------------------------------------------------------
+
+typedef unsigned int u32x4_t __attribute__((ext_vector_type(4)));
+
+__global__ void store_probe_kernel(u32x4_t* dst, uint64_t n16)
+{
+    const u32x4_t z = {0u, 0u, 0u, 0u};
+    const uint64_t stride = (uint64_t)gridDim.x * blockDim.x;
+    for (uint64_t i = (uint64_t)blockIdx.x * blockDim.x + threadIdx.x; i < n16; i += stride)
+        __builtin_nontemporal_store(z, dst + i);
+}
+
+hipError_t launch_store_probe(void* dst, uint64_t bytes, hipStream_t s)
+{
+    const uint64_t n16 = bytes / 16u;
+    if (n16 == 0) return hipSuccess;
+    // 8 workgroups of 256 threads per CU slot pair, each thread a strided run of 16-byte stores
+    const uint64_t want = (n16 + 255u) / 256u;
+    const unsigned blocks = (unsigned)(want < 16384u ? want : 16384u);
+    hipLaunchKernelGGL(store_probe_kernel, dim3(blocks), dim3(256), 0, s, (u32x4_t*)dst, n16);
+    return hipGetLastError();
+}
+
 }  // namespace pictura

@@ -131,6 +131,7 @@ struct BinWork {
 hipError_t launch_render(const RenderParams& p, hipStream_t s);
 hipError_t launch_bin(const BinWork& w, hipStream_t s);
 hipError_t launch_agents_step(const AgentStepParams& p, hipStream_t s);
+hipError_t launch_store_probe(void* dst, uint64_t bytes, hipStream_t s);
 int64_t scan_tmp_needed(int64_t n);
 hipError_t launch_rcp_check(uint32_t lo_bits, uint32_t n, unsigned long long* mismatches, hipStream_t s);
 

@@ -97,6 +97,8 @@ _lib.pictura_selftest_rcp.argtypes = [_P, ctypes.c_uint32, ctypes.c_uint32, _P]
 _lib.pictura_selftest_rcp.restype = ctypes.c_int32
 _lib.pictura_selftest_rcp_noalloc.argtypes = [_P, ctypes.c_uint32, ctypes.c_uint32, _P]
 _lib.pictura_selftest_rcp_noalloc.restype = ctypes.c_int32
+_lib.pictura_store_probe.argtypes = [_P, _P, ctypes.c_uint64, _P]
+_lib.pictura_store_probe.restype = ctypes.c_int32
 _lib.pictura_device_errors.argtypes = [_P, _P, ctypes.c_int32]
 _lib.pictura_device_errors.restype = ctypes.c_int32
 
@@ -104,7 +106,7 @@ EXPORTED = ["pictura_create", "pictura_destroy", "pictura_last_error", "pictura_
             "pictura_bin_scene", "pictura_render_views", "pictura_agents_step", "pictura_bins_info",
             "pictura_bins_copy", "pictura_set_option", "pictura_stats_copy", "pictura_selftest_rcp",
             "pictura_set_lights", "pictura_render_instances", "pictura_render_rgb", "pictura_render_rgb_aa",
-            "pictura_device_errors", "pictura_selftest_rcp_noalloc"]
+            "pictura_device_errors", "pictura_selftest_rcp_noalloc", "pictura_store_probe"]
 DEVERR_RING_WAIT = 1
 
 STAT_NAMES = ["view_tiles", "cells_in_rect", "cells_prefiltered", "cells_visible", "cand_tris", "boxes_visible",
@@ -332,6 +334,14 @@ def pictura_selftest_rcp(ctx, lo_bits: int, count: int) -> int:
     out = ctypes.c_uint64()
     _check(ctx, _lib.pictura_selftest_rcp(ctx, int(lo_bits), int(count), ctypes.addressof(out)))
     return int(out.value)
+
+
+def pictura_store_probe(ctx, buf, stream=None):
+    """Fill the whole uint8 tensor `buf` (a multiple of 16 bytes) with zeros
+    using 16-byte non-temporal stores: the HBM write-rate reference."""
+    n = buf.numel() if hasattr(buf, "numel") else 0
+    ptr = _dev(buf, "buf", "u8", n, ctx)
+    _check(ctx, _lib.pictura_store_probe(ctx, ptr, n, _stream(stream)))
 
 
 def pictura_device_errors(ctx, reset: bool = False) -> int:

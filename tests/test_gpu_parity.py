@@ -438,3 +438,22 @@ def test_fast_reciprocal_is_correctly_rounded(lib):
         assert bad == 0
     finally:
         lib.pictura_destroy(ctx)
+
+
+def test_store_probe_writes_exactly_its_range(lib):
+    # the bench's HBM write reference: zeros over exactly the requested bytes,
+    # nothing past them; misaligned sizes and buffers are refused
+    torch = _torch()
+    buf = torch.full((1 << 20,), 0xAB, dtype=torch.uint8, device="cuda")
+    r = lib.Renderer(0)
+    try:
+        lib.pictura_store_probe(r.ctx, buf[: (1 << 20) - 4096])
+        torch.cuda.synchronize()
+        assert int(buf[: (1 << 20) - 4096].sum()) == 0
+        assert bool((buf[(1 << 20) - 4096:] == 0xAB).all())
+        with pytest.raises(lib.PicturaError):
+            lib.pictura_store_probe(r.ctx, buf[:100])
+        with pytest.raises(lib.PicturaError):
+            lib.pictura_store_probe(r.ctx, buf[8:8 + 4096])
+    finally:
+        r.close_checked()
