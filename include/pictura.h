@@ -278,13 +278,21 @@ pictura_status pictura_store_probe(pictura_ctx ctx, void* dst, uint64_t bytes, v
 
 /* Grid geometry after pictura_bin_scene (host memory, synchronous: waits for
  * the binning to finish).  dims[w] = nx, ny; cell_base[w] = first cell of
- * world w (cell_base[num_worlds] = total cells).  Any pointer may be NULL. */
-pictura_status pictura_bins_info(pictura_ctx ctx, int32_t* dims, int64_t* cell_base, int64_t* total_cells);
+ * world w (cell_base[num_worlds] = total cells); *total_prims = the number of
+ * binned primitives.  A primitive is one input triangle, or a pair: input
+ * triangles t and t + 1 of one world with the same class where t + 1 is
+ * (a, c, d) for t = (a, b, c), bit for bit (a quad split along its diagonal),
+ * paired greedily in input order.  The kernels cull and set up a pair once;
+ * its two triangles are still drawn by the rules above, each with its own
+ * depth plane.  Any pointer may be NULL. */
+pictura_status pictura_bins_info(pictura_ctx ctx, int32_t* dims, int64_t* cell_base, int64_t* total_cells,
+                                 int64_t* total_prims);
 
 /* Copy the bins to host memory (synchronous).  cell_start[total_cells + 1]:
- * first re-laid-out triangle of each cell; cell_aabb[total_cells][6]: xmin
- * ymin zmin xmax ymax zmax of the cell's triangles (+inf/-inf when empty);
- * perm[T]: original index of each re-laid-out triangle. */
+ * first re-laid-out primitive of each cell; cell_aabb[total_cells][6]: xmin
+ * ymin zmin xmax ymax zmax of the cell's primitives (+inf/-inf when empty);
+ * perm[total_prims]: for each re-laid-out primitive, the input index of its
+ * first triangle, with bit 31 set for a pair. */
 pictura_status pictura_bins_copy(pictura_ctx ctx, uint32_t* cell_start, float* cell_aabb, uint32_t* perm);
 
 #define PICTURA_OPT_CULL   1 /* 1 (default): cell + triangle frustum culling; 0: every triangle of the world */

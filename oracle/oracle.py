@@ -48,7 +48,7 @@ def lib():
         L.oracle_quantize.restype = None
         L.oracle_quantize.argtypes = [p, ctypes.c_int64, ctypes.c_float, ctypes.c_float, p, p]
         L.oracle_bin.restype = ctypes.c_int
-        L.oracle_bin.argtypes = [ctypes.c_int, p, p, p, ctypes.c_float, p, p, p, p, p, ctypes.c_int64]
+        L.oracle_bin.argtypes = [ctypes.c_int, p, p, p, p, ctypes.c_float, p, p, p, p, p, p, p, ctypes.c_int64]
         L.oracle_agents_step.restype = None
         L.oracle_agents_step.argtypes = [ctypes.c_int64, p, p, p, p, p, p, p,
                                          ctypes.c_double, ctypes.c_double, p, p]
@@ -136,8 +136,10 @@ def quantize(iz, near, far):
 
 
 def bin_scene(scene, cell_size):
-    """Uniform-grid binning: dims [nw,2], cell_base [nw+1], home cell per
-    triangle [T], count per cell, member AABB per cell [cells,6]."""
+    """Uniform-grid binning over primitives (triangles and triangle pairs):
+    dims [nw,2], cell_base [nw+1], prims [P] (first triangle | 1 << 31 for a
+    pair), home cell per primitive [P], count per cell, member AABB per cell
+    [cells,6]."""
     L = lib()
     nw = int(scene.num_worlds)
     b = _c(scene.bounds, np.float32)
@@ -149,17 +151,20 @@ def bin_scene(scene, cell_size):
     dims = np.empty((nw, 2), np.int32)
     base = np.empty(nw + 1, np.int64)
     T = int(scene.tri_offsets[-1])
-    home = np.empty(T, np.int64)
+    prims = np.empty(max(T, 1), np.uint32)
+    home = np.empty(max(T, 1), np.int64)
+    nprim = np.zeros(1, np.int64)
     count = np.empty(ncell_max, np.int32)
     aabb = np.empty((ncell_max, 6), np.float32)
     offs = _c(scene.tri_offsets, np.int64)
     verts = _c(scene.verts, np.float32)
-    rc = L.oracle_bin(nw, _ptr(offs), _ptr(verts), _ptr(b), float(cell_size), _ptr(dims), _ptr(base),
-                      _ptr(home), _ptr(count), _ptr(aabb), ncell_max)
+    cls = _c(scene.cls, np.uint8)
+    rc = L.oracle_bin(nw, _ptr(offs), _ptr(verts), _ptr(cls), _ptr(b), float(cell_size), _ptr(dims), _ptr(base),
+                      _ptr(prims), _ptr(home), _ptr(nprim), _ptr(count), _ptr(aabb), ncell_max)
     if rc != 0:
         raise RuntimeError("oracle_bin failed")
-    nc = int(base[-1])
-    return dict(dims=dims, cell_base=base, home=home, count=count[:nc], aabb=aabb[:nc])
+    nc, npr = int(base[-1]), int(nprim[0])
+    return dict(dims=dims, cell_base=base, prims=prims[:npr], home=home[:npr], count=count[:nc], aabb=aabb[:nc])
 
 
 def agents_step(agents, steer, accel, dt=0.1, vmax=20.0):

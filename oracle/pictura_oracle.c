@@ -703,17 +703,22 @@ void oracle_quantize(const float* iz, int64_t n, float nearp, float farp, uint32
 }
 
 /*
- * Uniform-grid binning of one scene: each triangle belongs to the cell that
- * holds the centre of its xy bounding box (clamped into the grid); a cell
- * records its triangle count and the 3-D bounding box of its members.
+ * Uniform-grid binning of one scene, over primitives.  Walking each world's
+ * triangles in order, triangle t and t + 1 form a pair when they have the same
+ * class and t + 1 is (a, c, d) for t = (a, b, c), the shared a and c equal bit
+ * for bit (a quad split along its diagonal); any other triangle is a
+ * primitive on its own.  prim_out[p] = first triangle | (1 << 31 for a pair).
+ * Each primitive belongs to the cell that holds the centre of the xy
+ * bounding box of its vertices (clamped into the grid); a cell records its
+ * primitive count and the 3-D bounding box of its members' vertices.
  * Grid of world w: origin (bounds[w].xmin, bounds[w].ymin), square cells of
  * `cell` metres, nx = max(1, ceil(width / cell)) columns, ny rows, cells
  * numbered row-major (iy * nx + ix) after those of the previous worlds.
  */
-int oracle_bin(int num_worlds, const int64_t* tri_offsets, const float* verts, const float* bounds,
-               float cell, int32_t* dims_out /*[nw][2]*/, int64_t* cell_base_out /*[nw+1]*/,
-               int64_t* home_out /*[T]*/, int32_t* count_out, float* aabb_out /*[cells][6]*/,
-               int64_t max_cells)
+int oracle_bin(int num_worlds, const int64_t* tri_offsets, const float* verts, const uint8_t* cls,
+               const float* bounds, float cell, int32_t* dims_out /*[nw][2]*/, int64_t* cell_base_out /*[nw+1]*/,
+               uint32_t* prim_out /*[<= T]*/, int64_t* home_out /*[<= T]*/, int64_t* nprim_out,
+               int32_t* count_out, float* aabb_out /*[cells][6]*/, int64_t max_cells)
 {
     int64_t base = 0;
     for (int w = 0; w < num_worlds; ++w) {
@@ -734,14 +739,21 @@ int oracle_bin(int num_worlds, const int64_t* tri_offsets, const float* verts, c
         aabb_out[6 * c + 0] = aabb_out[6 * c + 1] = aabb_out[6 * c + 2] = INFINITY;
         aabb_out[6 * c + 3] = aabb_out[6 * c + 4] = aabb_out[6 * c + 5] = -INFINITY;
     }
+    int64_t np_ = 0;
     for (int w = 0; w < num_worlds; ++w) {
         int32_t nx = dims_out[2 * w], ny = dims_out[2 * w + 1];
-        for (int64_t t = tri_offsets[w]; t < tri_offsets[w + 1]; ++t) {
+        for (int64_t t = tri_offsets[w]; t < tri_offsets[w + 1];) {
             const float* v = verts + 9 * t;
+            int pair = t + 1 < tri_offsets[w + 1] && cls[t] == cls[t + 1] && memcmp(v, v + 9, 12) == 0 &&
+                       memcmp(v + 6, v + 12, 12) == 0;
             float lo[3], hi[3];
             for (int d = 0; d < 3; ++d) {
                 lo[d] = fminf(fminf(v[d], v[3 + d]), v[6 + d]);
                 hi[d] = fmaxf(fmaxf(v[d], v[3 + d]), v[6 + d]);
+                if (pair) {   /* the second triangle's third vertex */
+                    lo[d] = fminf(lo[d], v[15 + d]);
+                    hi[d] = fmaxf(hi[d], v[15 + d]);
+                }
             }
             float mx = (lo[0] + hi[0]) * 0.5f, my = (lo[1] + hi[1]) * 0.5f;
             float fx = floorf((mx - bounds[4 * w + 0]) / cell);
@@ -749,14 +761,18 @@ int oracle_bin(int num_worlds, const int64_t* tri_offsets, const float* verts, c
             int32_t ix = !(fx >= 0.0f) ? 0 : (fx >= (float)(nx - 1) ? nx - 1 : (int32_t)fx);
             int32_t iy = !(fy >= 0.0f) ? 0 : (fy >= (float)(ny - 1) ? ny - 1 : (int32_t)fy);
             int64_t c = cell_base_out[w] + (int64_t)iy * nx + ix;
-            home_out[t] = c;
+            prim_out[np_] = (uint32_t)t | (pair ? 0x80000000u : 0u);
+            home_out[np_] = c;
+            ++np_;
             count_out[c]++;
             for (int d = 0; d < 3; ++d) {
                 if (lo[d] < aabb_out[6 * c + d]) aabb_out[6 * c + d] = lo[d];
                 if (hi[d] > aabb_out[6 * c + 3 + d]) aabb_out[6 * c + 3 + d] = hi[d];
             }
+            t += pair ? 2 : 1;
         }
     }
+    *nprim_out = np_;
     return 0;
 }
 

@@ -23,6 +23,10 @@ struct pictura_ctx_s {
     float* verts = nullptr;
     uint8_t* cls = nullptr;
     int64_t* offsets_d = nullptr;
+    // primitives: triangles and triangle pairs (see SceneDev)
+    int64_t P = 0;
+    uint32_t* prims = nullptr;        // [P] first triangle | kPrimFlagPair
+    int64_t* prim_offsets_d = nullptr;   // [nw + 1]
     bool have_scene = false;
     uint8_t max_cls = 0;   // largest class ID of the static triangles
     // bins
@@ -37,9 +41,10 @@ struct pictura_ctx_s {
     uint32_t* aabb_bits = nullptr;
     uint32_t* margin_bits = nullptr;
     uint32_t* scan_tmp = nullptr;
-    float4* triA = nullptr;
-    float4* triB = nullptr;
-    float2* triC = nullptr;
+    float4* primA = nullptr;
+    float4* primB = nullptr;
+    float4* primC = nullptr;
+    float* primD = nullptr;
     uint32_t* perm = nullptr;
     float4* cell_lo = nullptr;
     float4* cell_hi = nullptr;
@@ -100,8 +105,8 @@ hipError_t dalloc(T*& p, size_t count)
 void free_bins(pictura_ctx c)
 {
     dfree(c->grids); dfree(c->home); dfree(c->rank); dfree(c->cell_start); dfree(c->aabb_bits);
-    dfree(c->margin_bits); dfree(c->scan_tmp); dfree(c->triA); dfree(c->triB); dfree(c->triC);
-    dfree(c->perm); dfree(c->cell_lo); dfree(c->cell_hi);
+    dfree(c->margin_bits); dfree(c->scan_tmp); dfree(c->primA); dfree(c->primB); dfree(c->primC);
+    dfree(c->primD); dfree(c->perm); dfree(c->cell_lo); dfree(c->cell_hi);
     c->binned = false;
     c->total_cells = 0;
     c->grids_h.clear();
@@ -111,8 +116,10 @@ void free_scene(pictura_ctx c)
 {
     free_bins(c);
     dfree(c->verts); dfree(c->cls); dfree(c->offsets_d); dfree(c->stats);
+    dfree(c->prims); dfree(c->prim_offsets_d);
     c->have_scene = false;
     c->T = 0;
+    c->P = 0;
     c->num_worlds = 0;
 }
 
@@ -121,6 +128,27 @@ struct DeviceGuard {
     explicit DeviceGuard(int d) { if (hipGetDevice(&prev) != hipSuccess) prev = -1; (void)hipSetDevice(d); }
     ~DeviceGuard() { if (prev >= 0) (void)hipSetDevice(prev); }
 };
+
+// Primitives of one upload: walking each world's triangles in order, triangle
+// t and t + 1 form a pair when they have the same class and t + 1 = (a, c, d)
+// for t = (a, b, c) (the same a and c, bit for bit); a triangle that starts no
+// pair and is not the second half of one is a primitive of its own.
+void make_prims(int nw, const int64_t* offs, const float* verts, const uint8_t* cls, std::vector<uint32_t>& prims,
+                std::vector<int64_t>& prim_offs)
+{
+    prims.clear();
+    prim_offs.assign(1, 0);
+    for (int w = 0; w < nw; ++w) {
+        for (int64_t t = offs[w]; t < offs[w + 1];) {
+            const float* a = verts + 9 * t;
+            const bool pair = t + 1 < offs[w + 1] && cls[t] == cls[t + 1] && std::memcmp(a, a + 9, 12) == 0 &&
+                              std::memcmp(a + 6, a + 12, 12) == 0;
+            prims.push_back((uint32_t)t | (pair ? kPrimFlagPair : 0u));
+            t += pair ? 2 : 1;
+        }
+        prim_offs.push_back((int64_t)prims.size());
+    }
+}
 
 uint32_t f2u(float f) { uint32_t u; std::memcpy(&u, &f, 4); return u; }
 float u2f(uint32_t u) { float f; std::memcpy(&f, &u, 4); return f; }
@@ -201,11 +229,20 @@ pictura_status pictura_scene_upload(pictura_ctx c, const pictura_scene* s, void*
             !(b[2] > b[0]) || !(b[3] > b[1]))
             return fail(c, PICTURA_EINVAL, "scene_upload: bounds of world %d are not a finite rectangle", w);
     }
+    std::vector<uint32_t> prims;
+    std::vector<int64_t> prim_offs;
+    make_prims(nw, s->tri_offsets, s->verts, s->cls, prims, prim_offs);
+    const int64_t P = (int64_t)prims.size();
+    if (P >= (1ll << 29)) return fail(c, PICTURA_ERANGE, "scene_upload: 2^29 or more primitives (triangles and pairs)");
     DeviceGuard g(c->device);
     hipStream_t st = (hipStream_t)stream;
     free_scene(c);
     hipError_t e;
-    if ((e = dalloc(c->verts, (size_t)T * 9)) != hipSuccess) return hip_fail(c, e, "scene_upload alloc");
+    if ((e = dalloc(c->prims, (size_t)P)) != hipSuccess || (e = dalloc(c->prim_offsets_d, (size_t)nw + 1)) != hipSuccess) {
+        free_scene(c);
+        return hip_fail(c, e, "scene_upload alloc");
+    }
+    if ((e = dalloc(c->verts, (size_t)T * 9)) != hipSuccess) { free_scene(c); return hip_fail(c, e, "scene_upload alloc"); }
     if ((e = dalloc(c->cls, (size_t)T)) != hipSuccess) { free_scene(c); return hip_fail(c, e, "scene_upload alloc"); }
     if ((e = dalloc(c->offsets_d, (size_t)nw + 1)) != hipSuccess) { free_scene(c); return hip_fail(c, e, "scene_upload alloc"); }
     // Synchronous-from-the-caller's-view copies: pageable host memory is staged
@@ -217,7 +254,9 @@ pictura_status pictura_scene_upload(pictura_ctx c, const pictura_scene* s, void*
             return hip_fail(c, e, "scene_upload copy");
         }
     }
-    if ((e = hipMemcpyAsync(c->offsets_d, s->tri_offsets, (size_t)(nw + 1) * sizeof(int64_t), hipMemcpyHostToDevice, st)) != hipSuccess) {
+    if ((e = hipMemcpyAsync(c->offsets_d, s->tri_offsets, (size_t)(nw + 1) * sizeof(int64_t), hipMemcpyHostToDevice, st)) != hipSuccess ||
+        (e = hipMemcpyAsync(c->prim_offsets_d, prim_offs.data(), (size_t)(nw + 1) * sizeof(int64_t), hipMemcpyHostToDevice, st)) != hipSuccess ||
+        (P > 0 && (e = hipMemcpyAsync(c->prims, prims.data(), (size_t)P * sizeof(uint32_t), hipMemcpyHostToDevice, st)) != hipSuccess)) {
         free_scene(c);
         return hip_fail(c, e, "scene_upload copy");
     }
@@ -226,6 +265,7 @@ pictura_status pictura_scene_upload(pictura_ctx c, const pictura_scene* s, void*
     c->bounds_h.assign(s->bounds, s->bounds + 4 * nw);
     c->num_worlds = nw;
     c->T = T;
+    c->P = P;
     c->have_scene = true;
     c->max_cls = max_cls;
     return PICTURA_OK;
@@ -258,15 +298,16 @@ pictura_status pictura_bin_scene(pictura_ctx c, float cell, void* stream)
     DeviceGuard dg(c->device);
     hipStream_t st = (hipStream_t)stream;
     free_bins(c);
-    const int64_t T = c->T;
+    const int64_t P = c->P;
     hipError_t e = hipSuccess;
     const int64_t ntmp = scan_tmp_needed(total + 1);
-    if ((e = dalloc(c->grids, (size_t)nw)) != hipSuccess || (e = dalloc(c->home, (size_t)T)) != hipSuccess ||
-        (e = dalloc(c->rank, (size_t)T)) != hipSuccess || (e = dalloc(c->cell_start, (size_t)total + 1)) != hipSuccess ||
+    if ((e = dalloc(c->grids, (size_t)nw)) != hipSuccess || (e = dalloc(c->home, (size_t)P)) != hipSuccess ||
+        (e = dalloc(c->rank, (size_t)P)) != hipSuccess || (e = dalloc(c->cell_start, (size_t)total + 1)) != hipSuccess ||
         (e = dalloc(c->aabb_bits, (size_t)total * 8)) != hipSuccess || (e = dalloc(c->margin_bits, (size_t)nw)) != hipSuccess ||
-        (e = dalloc(c->scan_tmp, (size_t)ntmp)) != hipSuccess || (e = dalloc(c->triA, (size_t)T)) != hipSuccess ||
-        (e = dalloc(c->triB, (size_t)T)) != hipSuccess || (e = dalloc(c->triC, (size_t)T)) != hipSuccess ||
-        (e = dalloc(c->perm, (size_t)T)) != hipSuccess || (e = dalloc(c->cell_lo, (size_t)total)) != hipSuccess ||
+        (e = dalloc(c->scan_tmp, (size_t)ntmp)) != hipSuccess || (e = dalloc(c->primA, (size_t)P)) != hipSuccess ||
+        (e = dalloc(c->primB, (size_t)P)) != hipSuccess || (e = dalloc(c->primC, (size_t)P)) != hipSuccess ||
+        (e = dalloc(c->primD, (size_t)P)) != hipSuccess ||
+        (e = dalloc(c->perm, (size_t)P)) != hipSuccess || (e = dalloc(c->cell_lo, (size_t)total)) != hipSuccess ||
         (e = dalloc(c->cell_hi, (size_t)total)) != hipSuccess) {
         free_bins(c);
         return hip_fail(c, e, "bin_scene alloc");
@@ -276,11 +317,12 @@ pictura_status pictura_bin_scene(pictura_ctx c, float cell, void* stream)
         return hip_fail(c, e, "bin_scene copy");
     }
     BinWork W{};
-    W.verts = c->verts; W.cls = c->cls; W.tri_offsets = c->offsets_d; W.T = T; W.num_worlds = nw;
+    W.verts = c->verts; W.cls = c->cls; W.prims = c->prims; W.prim_offsets = c->prim_offsets_d; W.P = P;
+    W.num_worlds = nw;
     W.grids = c->grids; W.total_cells = total; W.cell_size = cell;
     W.home = c->home; W.rank = c->rank; W.count = c->cell_start; W.aabb_bits = c->aabb_bits;
     W.margin_bits = c->margin_bits; W.scan_tmp = c->scan_tmp; W.scan_tmp_len = ntmp;
-    W.triA = c->triA; W.triB = c->triB; W.triC = c->triC; W.perm = c->perm;
+    W.primA = c->primA; W.primB = c->primB; W.primC = c->primC; W.primD = c->primD; W.perm = c->perm;
     W.cell_lo = c->cell_lo; W.cell_hi = c->cell_hi;
     if ((e = launch_bin(W, st)) != hipSuccess) { free_bins(c); return hip_fail(c, e, "bin_scene launch"); }
     // the host copy of the grids is needed again for render's argument checks
@@ -325,7 +367,7 @@ static pictura_status render_setup(pictura_ctx c, const pictura_agents* ag, cons
     if (V == 0) { *empty = true; return PICTURA_OK; }
 
     P = RenderParams{};
-    P.scene.triA = c->triA; P.scene.triB = c->triB; P.scene.triC = c->triC;
+    P.scene.primA = c->primA; P.scene.primB = c->primB; P.scene.primC = c->primC; P.scene.primD = c->primD;
     P.scene.cell_start = c->cell_start; P.scene.cell_lo = c->cell_lo; P.scene.cell_hi = c->cell_hi;
     P.scene.grids = c->grids; P.scene.cell_size = c->cell_size; P.scene.num_worlds = c->num_worlds;
     P.ax = ag->x; P.ay = ag->y; P.az0 = ag->z0; P.ac = ag->cos_h; P.as = ag->sin_h;
@@ -490,7 +532,8 @@ pictura_status pictura_store_probe(pictura_ctx c, void* dst, uint64_t bytes, voi
     return PICTURA_OK;
 }
 
-pictura_status pictura_bins_info(pictura_ctx c, int32_t* dims, int64_t* cell_base, int64_t* total_cells)
+pictura_status pictura_bins_info(pictura_ctx c, int32_t* dims, int64_t* cell_base, int64_t* total_cells,
+                                 int64_t* total_prims)
 {
     if (!c) return PICTURA_EINVAL;
     c->err.clear();
@@ -501,6 +544,7 @@ pictura_status pictura_bins_info(pictura_ctx c, int32_t* dims, int64_t* cell_bas
     }
     if (cell_base) cell_base[c->num_worlds] = c->total_cells;
     if (total_cells) *total_cells = c->total_cells;
+    if (total_prims) *total_prims = c->P;
     return PICTURA_OK;
 }
 
@@ -525,7 +569,7 @@ pictura_status pictura_bins_copy(pictura_ctx c, uint32_t* cell_start, float* cel
             o[0] = lo[k].x; o[1] = lo[k].y; o[2] = lo[k].z; o[3] = hi[k].x; o[4] = hi[k].y; o[5] = hi[k].z;
         }
     }
-    if (perm && c->T > 0 && (e = hipMemcpy(perm, c->perm, sizeof(uint32_t) * c->T, hipMemcpyDeviceToHost)) != hipSuccess)
+    if (perm && c->P > 0 && (e = hipMemcpy(perm, c->perm, sizeof(uint32_t) * c->P, hipMemcpyDeviceToHost)) != hipSuccess)
         return hip_fail(c, e, "bins_copy");
     return PICTURA_OK;
 }

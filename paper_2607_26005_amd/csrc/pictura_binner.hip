@@ -1,6 +1,7 @@
-// HIP kernels for gfx950: uniform-grid scene binner (count, exclusive scan,
-// scatter into cell order, per-cell bounding boxes) and the kinematic
-// bicycle step of the agents.
+// HIP kernels for gfx950: uniform-grid scene binner over primitives
+// (triangles and triangle pairs: count, exclusive scan, scatter into cell
+// order, per-cell bounding boxes) and the kinematic bicycle step of the
+// agents.
 #include "pictura_device.h"
 
 #pragma clang fp contract(off)
@@ -34,18 +35,34 @@ __device__ __forceinline__ int world_of(const int64_t* offs, int nw, int64_t t)
     return lo;
 }
 
+// The vertices of primitive p: a, b, c of its first triangle and, for a pair,
+// d (the third vertex of the second triangle (a, c, d)).  Returns 3 or 4.
+__device__ __forceinline__ int prim_verts(const BinWork& W, int64_t p, float* v)
+{
+    const uint32_t e = W.prims[p];
+    const float* a = W.verts + 9 * (int64_t)(e & ~kPrimFlagPair);
+#pragma unroll
+    for (int k = 0; k < 9; ++k) v[k] = a[k];
+    v[9] = v[10] = v[11] = 0.0f;
+    if (!(e & kPrimFlagPair)) return 3;
+    v[9] = a[15]; v[10] = a[16]; v[11] = a[17];
+    return 4;
+}
+
 __global__ void bin_count_kernel(BinWork W)
 {
-    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (t >= W.T) return;
-    const int w = world_of(W.tri_offsets, W.num_worlds, t);
+    const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (p >= W.P) return;
+    const int w = world_of(W.prim_offsets, W.num_worlds, p);
     const WorldGrid g = W.grids[w];
-    const float* v = W.verts + 9 * t;
+    float v[12];
+    const int nv = prim_verts(W, p, v);
     float lo[3], hi[3];
 #pragma unroll
     for (int d = 0; d < 3; ++d) {
         lo[d] = fminf(fminf(v[d], v[3 + d]), v[6 + d]);
         hi[d] = fmaxf(fmaxf(v[d], v[3 + d]), v[6 + d]);
+        if (nv == 4) { lo[d] = fminf(lo[d], v[9 + d]); hi[d] = fmaxf(hi[d], v[9 + d]); }
     }
     const float mx = (lo[0] + hi[0]) * 0.5f, my = (lo[1] + hi[1]) * 0.5f;
     const float fx = floorf((mx - g.ox) / W.cell_size);
@@ -53,8 +70,8 @@ __global__ void bin_count_kernel(BinWork W)
     const int ix = !(fx >= 0.0f) ? 0 : (fx >= (float)(g.nx - 1) ? g.nx - 1 : (int)fx);
     const int iy = !(fy >= 0.0f) ? 0 : (fy >= (float)(g.ny - 1) ? g.ny - 1 : (int)fy);
     const uint32_t c = (uint32_t)(g.cell_base + iy * g.nx + ix);
-    W.home[t] = c;
-    W.rank[t] = atomicAdd(&W.count[c], 1u);
+    W.home[p] = c;
+    W.rank[p] = atomicAdd(&W.count[c], 1u);
     uint32_t* a = W.aabb_bits + 8 * (int64_t)c;
 #pragma unroll
     for (int d = 0; d < 3; ++d) {
@@ -111,14 +128,18 @@ __global__ void scan_add_kernel(uint32_t* data, int64_t n, const uint32_t* tile_
 
 __global__ void bin_scatter_kernel(BinWork W)
 {
-    const int64_t t = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-    if (t >= W.T) return;
-    const uint32_t dst = W.count[W.home[t]] + W.rank[t];   // count[] now holds cell starts
-    const float* v = W.verts + 9 * t;
-    W.triA[dst] = make_float4(v[0], v[1], v[2], v[3]);
-    W.triB[dst] = make_float4(v[4], v[5], v[6], v[7]);
-    W.triC[dst] = make_float2(v[8], __uint_as_float((uint32_t)W.cls[t]));
-    W.perm[dst] = (uint32_t)t;
+    const int64_t p = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (p >= W.P) return;
+    const uint32_t dst = W.count[W.home[p]] + W.rank[p];   // count[] now holds cell starts
+    float v[12];
+    const int nv = prim_verts(W, p, v);
+    const uint32_t e = W.prims[p];
+    const uint32_t cw = (uint32_t)W.cls[e & ~kPrimFlagPair] | (nv == 4 ? kPrimPair : 0u);
+    W.primA[dst] = make_float4(v[0], v[1], v[2], v[3]);
+    W.primB[dst] = make_float4(v[4], v[5], v[6], v[7]);
+    W.primC[dst] = make_float4(v[8], __uint_as_float(cw), v[9], v[10]);
+    W.primD[dst] = v[11];
+    W.perm[dst] = e;
 }
 
 __device__ __forceinline__ int world_of_cell(const WorldGrid* g, int nw, int64_t c)
@@ -168,14 +189,14 @@ hipError_t launch_bin(const BinWork& W, hipStream_t s)
     const int64_t init_n = (n > W.num_worlds ? n : W.num_worlds);
     hipLaunchKernelGGL(bin_init_kernel, dim3(blocks(init_n)), dim3(kBlock), 0, s,
                        W.count, W.aabb_bits, cells, W.margin_bits, W.num_worlds);
-    if (W.T > 0)
-        hipLaunchKernelGGL(bin_count_kernel, dim3(blocks(W.T)), dim3(kBlock), 0, s, W);
+    if (W.P > 0)
+        hipLaunchKernelGGL(bin_count_kernel, dim3(blocks(W.P)), dim3(kBlock), 0, s, W);
     const int64_t tiles = (n + kScanTile - 1) / kScanTile;
     hipLaunchKernelGGL(scan_tiles_kernel, dim3((unsigned)tiles), dim3(kBlock), 0, s, W.count, n, W.scan_tmp);
     hipLaunchKernelGGL(scan_sums_kernel, dim3(1), dim3(kBlock), 0, s, W.scan_tmp, tiles);
     hipLaunchKernelGGL(scan_add_kernel, dim3(blocks(n)), dim3(kBlock), 0, s, W.count, n, W.scan_tmp);
-    if (W.T > 0)
-        hipLaunchKernelGGL(bin_scatter_kernel, dim3(blocks(W.T)), dim3(kBlock), 0, s, W);
+    if (W.P > 0)
+        hipLaunchKernelGGL(bin_scatter_kernel, dim3(blocks(W.P)), dim3(kBlock), 0, s, W);
     if (cells > 0)
         hipLaunchKernelGGL(bin_finalize_kernel, dim3(blocks(cells)), dim3(kBlock), 0, s, W);
     hipLaunchKernelGGL(bin_margin_kernel, dim3(blocks(W.num_worlds)), dim3(kBlock), 0, s, W);

@@ -19,13 +19,22 @@ struct WorldGrid {
     int32_t pad0, pad1;
 };
 
-// Re-laid-out triangle t (cell order) is split over three arrays so that a
-// wave reading 64 consecutive triangles issues three coalesced loads:
-//   A[t] = (x0, y0, z0, x1), B[t] = (y1, z1, x2, y2), C[t] = (z2, bits(class)).
+// The binned unit is a primitive: one triangle (a, b, c), or a pair of input
+// triangles (a, b, c), (a, c, d) that share the edge a-c and the class (a quad
+// split along a diagonal: the generators' ground tiles, road segments,
+// markings and curbs are all such pairs).  A pair is culled, loaded and set up
+// once; its two halves are still separate triangles with their own depth
+// planes.  Re-laid-out primitive p (cell order) is split over four arrays, so
+// that a wave reading 64 consecutive primitives issues coalesced loads:
+//   A[p] = (ax, ay, az, bx), B[p] = (by, bz, cx, cy),
+//   C[p] = (cz, bits(class | pair << 8), dx, dy), D[p] = dz   (d = 0 for a triangle).
+constexpr uint32_t kPrimPair = 256u;   // in the class word of C: the primitive is a pair
+
 struct SceneDev {
-    const float4* triA;
-    const float4* triB;
-    const float2* triC;
+    const float4* primA;
+    const float4* primB;
+    const float4* primC;
+    const float* primD;
     const uint32_t* cell_start;   // [cells + 1]
     const float4* cell_lo;        // [cells] xmin ymin zmin -
     const float4* cell_hi;        // [cells] xmax ymax zmax -
@@ -110,23 +119,28 @@ struct AgentStepParams {
 struct BinWork {
     const float* verts;          // [T][9] original order
     const uint8_t* cls;          // [T]
-    const int64_t* tri_offsets;  // [nw + 1] (device)
-    int64_t T;
+    const uint32_t* prims;       // [P] first triangle of each primitive | kPrimFlagPair
+    const int64_t* prim_offsets; // [nw + 1] (device): world w owns primitives [prim_offsets[w], prim_offsets[w+1])
+    int64_t P;
     int32_t num_worlds;
     WorldGrid* grids;            // [nw]
     int64_t total_cells;
     float cell_size;
-    uint32_t* home;              // [T]
-    uint32_t* rank;              // [T]
+    uint32_t* home;              // [P]
+    uint32_t* rank;              // [P]
     uint32_t* count;             // [cells + 1] -> exclusive scan -> cell_start
     uint32_t* aabb_bits;         // [cells][8] order-preserving bits (6 used)
     uint32_t* margin_bits;       // [nw]
     uint32_t* scan_tmp;          // block sums
     int64_t scan_tmp_len;
-    float4* triA; float4* triB; float2* triC;
-    uint32_t* perm;              // [T]
+    float4* primA; float4* primB; float4* primC; float* primD;
+    uint32_t* perm;              // [P] the primitive's entry of prims, in cell order
     float4* cell_lo; float4* cell_hi;
 };
+
+// prims[p]: index of the primitive's first input triangle, with this bit set
+// when the primitive is the pair (that triangle, the next one)
+constexpr uint32_t kPrimFlagPair = 0x80000000u;
 
 hipError_t launch_render(const RenderParams& p, hipStream_t s);
 hipError_t launch_bin(const BinWork& w, hipStream_t s);

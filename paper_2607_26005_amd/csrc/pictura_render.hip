@@ -58,8 +58,13 @@ typedef unsigned int u32x4 __attribute__((ext_vector_type(4)));
 typedef float f32x4 __attribute__((ext_vector_type(4)));
 
 constexpr uint32_t kClearKey = (0xFFFFFFu << 8) | 4u;
-constexpr uint32_t kBoxFlag = 0x80000000u;     // queue entry: (agent << 4) | face of a box
-constexpr uint32_t kLightFlag = 0x40000000u;   // queue entry: (light << 4) | sector of a traffic light
+// Queue entries.  Static primitive p: (p << 2) | kind (p < 2^29), kind 0 a
+// lone triangle, 1 and 2 the first (a, b, c) and second (a, c, d) half of a
+// pair taken alone, 3 the whole pair with all four vertices in front of the
+// near plane.  Boxes and lights set bit 31 (and lights bit 30 too).
+constexpr uint32_t kBoxFlag = 0x80000000u;     // queue entry: kBoxFlag | (agent << 4) | face of a box
+constexpr uint32_t kLightFlag = 0xC0000000u;   // queue entry: kLightFlag | (light << 4) | sector of a traffic light
+enum { kTri = 0, kHalf0 = 1, kHalf1 = 2, kPair = 3 };
 constexpr int kViewWaves = PICTURA_VIEW_WAVES;   // waves per view tile
 constexpr int kThreads = 64 * kViewWaves;
 constexpr int kWavesPerSimd = 4;  // register budget: four waves per SIMD (as many as the LDS admits)
@@ -357,22 +362,42 @@ __device__ __forceinline__ bool light_visible(const RenderParams& P, const Cam& 
     return hh > 0.0f && hh * hh >= P.lcos2 * q;
 }
 
-__device__ __forceinline__ void load_static(const RenderParams& P, uint32_t t, float* tri, uint32_t& cls)
+// Static primitive p: vertices a, b, c, d in v[0..11] (d = 0 for a lone
+// triangle), the class and whether it is a pair.
+__device__ __forceinline__ void load_prim(const RenderParams& P, uint32_t p, float* v, uint32_t& cls, bool& pair)
 {
-    const float4 A = P.scene.triA[t];
-    const float4 B = P.scene.triB[t];
-    const float2 C = P.scene.triC[t];
-    tri[0] = A.x; tri[1] = A.y; tri[2] = A.z; tri[3] = A.w;
-    tri[4] = B.x; tri[5] = B.y; tri[6] = B.z; tri[7] = B.w; tri[8] = C.x;
-    cls = __float_as_uint(C.y);
+    const float4 A = P.scene.primA[p];
+    const float4 B = P.scene.primB[p];
+    const float4 C = P.scene.primC[p];
+    v[0] = A.x; v[1] = A.y; v[2] = A.z; v[3] = A.w;
+    v[4] = B.x; v[5] = B.y; v[6] = B.z; v[7] = B.w; v[8] = C.x;
+    v[9] = C.z; v[10] = C.w; v[11] = P.scene.primD[p];
+    const uint32_t cw = __float_as_uint(C.y);
+    cls = cw & 255u;
+    pair = (cw & kPrimPair) != 0u;
 }
 
-__device__ __forceinline__ void load_entry(const RenderParams& P, uint32_t e, int64_t abase_w, int64_t lbase_w,
+// The world-space polygon of a queue entry: a triangle in tri[0..8], or for a
+// whole pair the 4-gon (a, b, c, d) in tri[0..11] (returns true).
+__device__ __forceinline__ bool load_entry(const RenderParams& P, uint32_t e, int64_t abase_w, int64_t lbase_w,
                                            float* tri, uint32_t& cls)
 {
-    if (e & kBoxFlag) load_box(P, abase_w + ((e & ~kBoxFlag) >> 4), (int)(e & 15u), tri, cls);
-    else if (e & kLightFlag) load_light(P, lbase_w + ((e & ~kLightFlag) >> 4), (int)(e & 15u), tri, cls);
-    else load_static(P, e, tri, cls);
+    if ((e & kLightFlag) == kLightFlag) {
+        load_light(P, lbase_w + ((e & ~kLightFlag) >> 4), (int)(e & 15u), tri, cls);
+        return false;
+    }
+    if (e & kBoxFlag) {
+        load_box(P, abase_w + ((e & ~kBoxFlag) >> 4), (int)(e & 15u), tri, cls);
+        return false;
+    }
+    bool pair;
+    load_prim(P, e >> 2, tri, cls, pair);
+    const uint32_t kind = e & 3u;
+    if (kind == kHalf1) {   // (a, c, d)
+        tri[3] = tri[6]; tri[4] = tri[7]; tri[5] = tri[8];
+        tri[6] = tri[9]; tri[7] = tri[10]; tri[8] = tri[11];
+    }
+    return kind == kPair;
 }
 
 // Side-plane test of three view-space vertices (conservative, see Tile).
@@ -399,11 +424,15 @@ __device__ __forceinline__ bool box_has_centre(const RenderParams& P, const Tile
                                                float ymx, float mag)
 {
     const float m = T.cm + (mag + P.cabs) * 3.814697265625e-06f;   // base + 2^-18 (|p| + |c|)
-    const float ilo = fmaxf(ceilf(xmn - m - 0.5f), (float)T.x0);
-    const float ihi = fminf(floorf(xmx + m - 0.5f), (float)(T.x0 + T.w - 1));
-    const float jlo = fmaxf(ceilf(ymn - m - 0.5f), (float)T.y0);
-    const float jhi = fminf(floorf(ymx + m - 0.5f), (float)(T.y0 + T.h - 1));
-    return !(ilo > ihi) && !(jlo > jhi);
+    // compared as integers against the tile's (scalar) bounds, after clamping
+    // to +-2^30 (a NaN bound clamps to -2^30, which may cull a triangle with a
+    // non-finite vertex: one that the snap's range rule drops anyway)
+    auto toi = [](float x) { return (int)fminf(fmaxf(x, -1073741824.0f), 1073741824.0f); };
+    const int ilo = max(toi(ceilf(xmn - m - 0.5f)), T.x0);
+    const int ihi = min(toi(floorf(xmx + m - 0.5f)), T.x0 + T.w - 1);
+    const int jlo = max(toi(ceilf(ymn - m - 0.5f)), T.y0);
+    const int jhi = min(toi(floorf(ymx + m - 0.5f)), T.y0 + T.h - 1);
+    return ilo <= ihi && jlo <= jhi;
 }
 
 // First pass: false only if the triangle cannot set a key of the tile.  The
@@ -432,6 +461,50 @@ __device__ __forceinline__ bool first_pass(const RenderParams& P, const Tile& T,
         mag = fmaxf(mag, fmaxf(fabsf(px), fabsf(py)));
     }
     return box_has_centre(P, T, xmn, xmx, ymn, ymx, mag);
+}
+
+// First pass of a static primitive (lane-wise).  r0, r1 for the halves (a, b,
+// c) and (a, c, d) (a lone triangle has only the first): 0 the half cannot
+// set a key of the tile, 1 it can and its vertices all lie in front of the near
+// plane, 2 it can and it reaches behind the near plane.  A pair whose four
+// vertices lie in front of the near plane and neither of whose halves lies
+// wholly beyond far is tested once, by the projected box of all four vertices
+// (conservative for each half); any other primitive tests each half with
+// first_pass.
+__device__ __forceinline__ void first_pass_prim(const RenderParams& P, const Tile& T, const Cam& cam, const float* v,
+                                                bool pair, bool cull, int& r0, int& r1)
+{
+    float xv[4], yv[4], zv[4];
+#pragma unroll
+    for (int k = 0; k < 4; ++k) view_xform(cam, v[3 * k], v[3 * k + 1], v[3 * k + 2], xv[k], yv[k], zv[k]);
+    const bool all4 = zv[0] >= P.nearp && zv[1] >= P.nearp && zv[2] >= P.nearp && zv[3] >= P.nearp;
+    const bool far0 = zv[0] > P.farp && zv[1] > P.farp && zv[2] > P.farp;
+    const bool far1 = zv[0] > P.farp && zv[2] > P.farp && zv[3] > P.farp;
+    if (pair && all4 && !far0 && !far1) {
+        bool pass = true;
+        if (cull) {
+            float xmn = 3.0e38f, xmx = -3.0e38f, ymn = 3.0e38f, ymx = -3.0e38f, mag = 0.0f;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const float r = __builtin_amdgcn_rcpf(zv[k]);
+                const float px = P.cx + P.fx * (xv[k] * r);
+                const float py = P.cy - P.fy * (yv[k] * r);
+                xmn = fminf(xmn, px); xmx = fmaxf(xmx, px);
+                ymn = fminf(ymn, py); ymx = fmaxf(ymx, py);
+                mag = fmaxf(mag, fmaxf(fabsf(px), fabsf(py)));
+            }
+            pass = box_has_centre(P, T, xmn, xmx, ymn, ymx, mag);
+        }
+        r0 = r1 = pass ? 1 : 0;
+        return;
+    }
+    const float h0[9] = {v[0], v[1], v[2], v[3], v[4], v[5], v[6], v[7], v[8]};
+    r0 = first_pass(P, T, cam, h0, cull) ? (zv[0] >= P.nearp && zv[1] >= P.nearp && zv[2] >= P.nearp ? 1 : 2) : 0;
+    r1 = 0;
+    if (pair) {
+        const float h1[9] = {v[0], v[1], v[2], v[6], v[7], v[8], v[9], v[10], v[11]};
+        r1 = first_pass(P, T, cam, h1, cull) ? (zv[0] >= P.nearp && zv[2] >= P.nearp && zv[3] >= P.nearp ? 1 : 2) : 0;
+    }
 }
 
 // ---------------------------------------------------------------------------
@@ -645,15 +718,20 @@ __device__ __forceinline__ void raster_blocks(const RenderParams& P, Shared& S, 
         if constexpr (I32 && Fast) {
             // the block's offsets, as the lane that tested it computed them
             // (broadcast through the LDS crossbar: no vector ALU instruction)
-            const int e0 = Eb[0] + (int)bperm(b, (uint32_t)off[0]);
-            const int e1 = Eb[1] + (int)bperm(b, (uint32_t)off[1]);
-            const int e2 = Eb[2] + (int)bperm(b, (uint32_t)off[2]);
-            const float pxf = pxl + __uint_as_float(bperm(b, __float_as_uint(pxu)));
-            const float pyf = pyl + __uint_as_float(bperm(b, __float_as_uint(pyu)));
+            // (all six fetched before any is used: one LDS round trip per block)
+            const uint32_t ga = bperm(b, boff);
+            const uint32_t g0 = bperm(b, (uint32_t)off[0]), g1 = bperm(b, (uint32_t)off[1]);
+            const uint32_t g2 = bperm(b, (uint32_t)off[2]);
+            const uint32_t gx = bperm(b, __float_as_uint(pxu)), gy = bperm(b, __float_as_uint(pyu));
+            const int e0 = Eb[0] + (int)g0;
+            const int e1 = Eb[1] + (int)g1;
+            const int e2 = Eb[2] + (int)g2;
+            const float pxf = pxl + __uint_as_float(gx);
+            const float pyf = pyl + __uint_as_float(gy);
             const float iz = fmaf(pa, pxf, fmaf(pb, pyf, pc));
             const uint32_t bits = min(__float_as_uint(iz), __float_as_uint(P.izcap));
             const uint32_t key = ((P.qbase - (bits >> 3)) << 8) | cls;
-            addr = bperm(b, boff) + (uint32_t)loff4;
+            addr = ga + (uint32_t)loff4;
             return (((e0 | e1 | e2) >= 0) && iz >= P.izfar) ? key : 0xFFFFFFFFu;
         }
         const uint32_t q = readlane(xy, b);
@@ -958,18 +1036,26 @@ __device__ __forceinline__ void exact_pass(const RenderParams& P, Shared& S, Wav
                                            bool live, uint32_t entry, int64_t abase_w, int64_t lbase_w, float pxl,
                                            float pyl, int loff4, uint32_t* fbo)
 {
-    float tri[9] = {};
+    float tri[12] = {};
     uint32_t cls = 0;
     int np = 0;
+    bool quad = false;   // a whole pair: the 4-gon (a, b, c, d), every vertex in front of the near plane
     int X0 = 0, Y0 = 0, X1 = 0, Y1 = 0, X2 = 0, Y2 = 0, X3 = 0, Y3 = 0;
     if (live) {
-        load_entry(P, entry, abase_w, lbase_w, tri, cls);
+        quad = load_entry(P, entry, abase_w, lbase_w, tri, cls);
         float xv[3], yv[3], zv[3];
 #pragma unroll
         for (int k = 0; k < 3; ++k) view_xform(cam, tri[3 * k], tri[3 * k + 1], tri[3 * k + 2], xv[k], yv[k], zv[k]);
         const bool in0 = zv[0] >= P.nearp, in1 = zv[1] >= P.nearp, in2 = zv[2] >= P.nearp;
         bool ok = true;
-        if (in0 && in1 && in2) {
+        if (quad) {
+            // the pair's halves (a, b, c) and (a, c, d) are the fan pieces of (a, b, c, d)
+            float x3, y3, z3;
+            view_xform(cam, tri[9], tri[10], tri[11], x3, y3, z3);
+            ok = snap_vertex(P, xv[0], yv[0], zv[0], X0, Y0) && snap_vertex(P, xv[1], yv[1], zv[1], X1, Y1) &&
+                 snap_vertex(P, xv[2], yv[2], zv[2], X2, Y2) && snap_vertex(P, x3, y3, z3, X3, Y3);
+            np = 4;
+        } else if (in0 && in1 && in2) {
             ok = snap_vertex(P, xv[0], yv[0], zv[0], X0, Y0) && snap_vertex(P, xv[1], yv[1], zv[1], X1, Y1) &&
                  snap_vertex(P, xv[2], yv[2], zv[2], X2, Y2);
             np = 3;
@@ -1012,19 +1098,33 @@ __device__ __forceinline__ void exact_pass(const RenderParams& P, Shared& S, Wav
         if (!ok) np = 0;
     }
     const int nfan = __ballot(np == 4) != 0 ? 2 : 1;
-    // R3 depth plane of the unclipped triangle (shared by its fan pieces)
-    float pa = 0.0f, pb = 0.0f, pc = 0.0f;
-    if (np != 0 && !depth_plane(P, cam, tri, pa, pb, pc)) np = 0;
+    // R3 depth planes: the unclipped triangle's, shared by the fan pieces of a
+    // clipped triangle; each half of a pair has its own
+    float pa0 = 0.0f, pb0 = 0.0f, pc0 = 0.0f;
+    bool ok0 = np != 0 && depth_plane(P, cam, tri, pa0, pb0, pc0);
+    float pa1 = pa0, pb1 = pb0, pc1 = pc0;
+    bool ok1 = ok0;
+    if (__ballot(quad) != 0) {
+        const float t2[9] = {tri[0], tri[1], tri[2], tri[6], tri[7], tri[8], tri[9], tri[10], tri[11]};
+        float qa = 0.0f, qb = 0.0f, qc = 0.0f;
+        const bool okq = depth_plane(P, cam, t2, qa, qb, qc);
+        if (quad) {
+            pa1 = qa; pb1 = qb; pc1 = qc;
+            ok1 = np != 0 && okq;
+        }
+    }
     const int px0 = 256 * T.x0 + 128, py0 = 256 * T.y0 + 128;
     // fan triangles (p0, p1, p2) and (p0, p2, p3)
 #pragma unroll 1
     for (int f = 0; f < nfan; ++f) {
+        const float pa = f ? pa1 : pa0, pb = f ? pb1 : pb0, pc = f ? pc1 : pc0;
+        const bool piece = f + 2 < np && (f ? ok1 : ok0);
         bool valid = false;
         const int ax = X0, ay = Y0;
         int bx = f == 0 ? X1 : X2, by = f == 0 ? Y1 : Y2;
         int cx = f == 0 ? X2 : X3, cy = f == 0 ? Y2 : Y3;
         int i0 = 0, i1 = -1, j0 = 0, j1 = -1;
-        if (f + 2 < np) {
+        if (piece) {
             const int minX = min(ax, min(bx, cx)), maxX = max(ax, max(bx, cx));
             const int minY = min(ay, min(by, cy)), maxY = max(ay, max(by, cy));
             i0 = max((minX - 128 + 255) >> 8, T.x0); i1 = min((maxX - 128) >> 8, T.x0 + T.w - 1);
@@ -1044,7 +1144,7 @@ __device__ __forceinline__ void exact_pass(const RenderParams& P, Shared& S, Wav
                 }
             }
         }
-        if constexpr (kAA) aa_pieces(P, L, fbo, T, f + 2 < np, ax, ay, bx, by, cx, cy, pa, pb, pc, cls);
+        if constexpr (kAA) aa_pieces(P, L, fbo, T, piece, ax, ay, bx, by, cx, cy, pa, pb, pc, cls);
         // edge setup: edges v1->v2, v2->v0, v0->v1 at the tile's pixel (0, 0),
         // in the int32 form (floor(c / 256), -dy, dx) when every value fits
         uint32_t rv[12] = {0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
@@ -1634,39 +1734,41 @@ void render_views_kernel(const RenderParams P_)
         }
         TACC(kCycSource, t_src);
         if (phase == kStatic) {
-            // first pass over candidate slots s0 .. s0 + 127: both halves' triangles
-            // are loaded before either is tested (one memory round trip)
+            // first pass over candidate primitives s0 .. s0 + 63 (a pair may queue
+            // two entries, so one chunk per step keeps the queue within kQueue:
+            // fewer than 64 entries wait before a step, at most 128 join)
             TSTART(t_first);
             const uint32_t slot = s0 + (uint32_t)lane;
-            // cells overlapping the slots (every visible cell holds a triangle)
-            uint32_t bs0 = 0, bp0 = 0, bs1 = 0, bp1 = 0;
+            // the cell holding each slot (every visible cell holds a primitive)
+            uint32_t bs = 0, bp = 0;
             int c = cfirst;
             for (; c < nvis; ++c) {
                 const uint32_t pc = readlane(my_pre, c);
-                if (pc >= s0 + 128u) break;
+                if (pc >= s0 + 64u) break;
                 const uint32_t sc = readlane(my_start, c);
-                if (slot >= pc) { bs0 = sc; bp0 = pc; }
-                if (slot + 64u >= pc) { bs1 = sc; bp1 = pc; }
+                if (slot >= pc) { bs = sc; bp = pc; }
             }
-            // the cell holding slot s0 + 128: the one that ended the loop if it starts there, else the last visited
-            cfirst = (c < nvis && readlane(my_pre, c) == s0 + 128u) ? c : max(c - 1, 0);
-            const uint32_t e0 = bs0 + (slot - bp0), e1 = bs1 + (slot + 64u - bp1);
-            float t0[9] = {}, t1[9] = {};
-            uint32_t c0 = 0, c1 = 0;
-            if (slot < total) load_static(P, e0, t0, c0);
-            if (slot + 64u < total) load_static(P, e1, t1, c1);
-#pragma unroll 1
-            for (int h = 0; h < 2; ++h) {
-                float tri[9];
-#pragma unroll
-                for (int q = 0; q < 9; ++q) tri[q] = h ? t1[q] : t0[q];
-                const uint32_t sl = slot + 64u * (uint32_t)h;
-                const bool surv = sl < total && first_pass(P, T, cam, tri, cull);
-                if (surv) STAT(kStSurv, 1);
-                STAT1(kStChunks, 1);
-                nq = queue_push(L, nq, surv, h ? e1 : e0);
+            // the cell holding slot s0 + 64: the one that ended the loop if it starts there, else the last visited
+            cfirst = (c < nvis && readlane(my_pre, c) == s0 + 64u) ? c : max(c - 1, 0);
+            const uint32_t e = bs + (slot - bp);
+            float v[12] = {};
+            uint32_t vcls = 0;
+            bool pair = false;
+            int r0 = 0, r1 = 0;
+            if (slot < total) {
+                load_prim(P, e, v, vcls, pair);
+                first_pass_prim(P, T, cam, v, pair, cull, r0, r1);
             }
-            s0 += 128;
+            // the whole pair when both halves pass with every vertex in front of
+            // the near plane; otherwise each passing half (or the lone triangle)
+            const bool whole = r0 == 1 && r1 == 1;
+            const uint32_t k0 = whole ? (uint32_t)kPair : pair ? (uint32_t)kHalf0 : (uint32_t)kTri;
+            if (r0 != 0) STAT(kStSurv, 1);
+            if (r1 != 0) STAT(kStSurv, 1);
+            STAT1(kStChunks, 1);
+            nq = queue_push(L, nq, r0 != 0, (e << 2) | k0);
+            nq = queue_push(L, nq, r1 != 0 && !whole, (e << 2) | (uint32_t)kHalf1);
+            s0 += 64;
             TACC(kCycFirst, t_first);
         } else if (phase != kDone) {
             // first pass over box (or light) slots s0 .. s0 + 63

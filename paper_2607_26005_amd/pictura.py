@@ -77,7 +77,7 @@ _lib.pictura_render_views.argtypes = [_P, ctypes.POINTER(_Agents), ctypes.POINTE
 _lib.pictura_render_views.restype = ctypes.c_int32
 _lib.pictura_agents_step.argtypes = [_P, ctypes.POINTER(_AgentState), _P, _P, ctypes.c_float, ctypes.c_float, _P]
 _lib.pictura_agents_step.restype = ctypes.c_int32
-_lib.pictura_bins_info.argtypes = [_P, _P, _P, _P]
+_lib.pictura_bins_info.argtypes = [_P, _P, _P, _P, _P]
 _lib.pictura_bins_info.restype = ctypes.c_int32
 _lib.pictura_bins_copy.argtypes = [_P, _P, _P, _P]
 _lib.pictura_bins_copy.restype = ctypes.c_int32
@@ -311,19 +311,22 @@ def pictura_set_lights(ctx, lights):
 
 
 def pictura_bins_info(ctx, num_worlds: int):
+    """(dims [nw, 2], cell_base [nw + 1], total cells, total primitives)"""
     dims = np.empty((num_worlds, 2), np.int32)
     base = np.empty(num_worlds + 1, np.int64)
     total = ctypes.c_int64()
-    _check(ctx, _lib.pictura_bins_info(ctx, dims.ctypes.data, base.ctypes.data, ctypes.addressof(total)))
-    return dims, base, int(total.value)
+    prims = ctypes.c_int64()
+    _check(ctx, _lib.pictura_bins_info(ctx, dims.ctypes.data, base.ctypes.data, ctypes.addressof(total),
+                                       ctypes.addressof(prims)))
+    return dims, base, int(total.value), int(prims.value)
 
 
-def pictura_bins_copy(ctx, total_cells: int, num_tris: int):
+def pictura_bins_copy(ctx, total_cells: int, num_prims: int):
     start = np.empty(total_cells + 1, np.uint32)
     aabb = np.empty((total_cells, 6), np.float32)
-    perm = np.empty(max(num_tris, 1), np.uint32)
+    perm = np.empty(max(num_prims, 1), np.uint32)
     _check(ctx, _lib.pictura_bins_copy(ctx, start.ctypes.data, aabb.ctypes.data, perm.ctypes.data))
-    return start, aabb, perm[:num_tris]
+    return start, aabb, perm[:num_prims]
 
 
 def pictura_set_option(ctx, option: int, value: int):
@@ -501,6 +504,6 @@ class Renderer:
         self.lights = lights   # the context keeps the pointers: hold the tensors
 
     def bins(self):
-        dims, base, total = pictura_bins_info(self.ctx, self.num_worlds)
-        start, aabb, perm = pictura_bins_copy(self.ctx, total, self.num_tris)
+        dims, base, total, prims = pictura_bins_info(self.ctx, self.num_worlds)
+        start, aabb, perm = pictura_bins_copy(self.ctx, total, prims)
         return dict(dims=dims, cell_base=base, cell_start=start, aabb=aabb, perm=perm)

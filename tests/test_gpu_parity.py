@@ -344,11 +344,12 @@ def test_binner_matches_oracle(lib):
     assert np.array_equal(counts, ob["count"].astype(np.int64))
     ne = counts > 0
     assert np.array_equal(b["aabb"][ne], ob["aabb"][ne])
-    # each cell holds exactly the oracle's set of triangles
+    # the same primitives (triangle pairs), each in the oracle's cell
     perm = b["perm"].astype(np.int64)
-    assert np.array_equal(np.sort(perm), np.arange(sc.num_tris))
+    assert np.array_equal(np.sort(perm), np.sort(ob["prims"].astype(np.int64)))
+    home_of = dict(zip(ob["prims"].astype(np.int64).tolist(), ob["home"].tolist()))
     cell_of_slot = np.repeat(np.arange(len(counts)), counts)
-    assert np.array_equal(ob["home"][perm], cell_of_slot)
+    assert np.array_equal(np.asarray([home_of[p] for p in perm.tolist()]), cell_of_slot)
 
 
 def test_agents_step_matches_oracle(lib):

@@ -464,27 +464,68 @@ def test_quantizer_cap_is_the_power_of_two_above_one_over_near():
 # binner: home cell contains the bbox centre; AABBs are tight
 # ---------------------------------------------------------------------------
 
+def _pairs_by_rule(sc):
+    """The pairing rule written out in numpy: per world, in input order,
+    t and t + 1 pair when the classes match and t + 1 = (a, c, d) for
+    t = (a, b, c) bit for bit; returns (first triangle, is pair) per primitive."""
+    v = sc.verts.reshape(-1, 9).view(np.uint32)
+    out = []
+    for w in range(sc.num_worlds):
+        t, e = int(sc.tri_offsets[w]), int(sc.tri_offsets[w + 1])
+        while t < e:
+            pair = t + 1 < e and sc.cls[t] == sc.cls[t + 1] and (v[t, 0:3] == v[t + 1, 0:3]).all() and \
+                (v[t, 6:9] == v[t + 1, 3:6]).all()
+            out.append((t, pair))
+            t += 2 if pair else 1
+    return out
+
+
+def test_binner_pairing_rule_cases():
+    a, b, c, d, e = (0.0, 0.0, 0.0), (4.0, 0.0, 0.0), (4.0, 3.0, 0.0), (0.0, 3.0, 0.0), (-2.0, 1.0, 0.0)
+    tris = [[a, b, c], [a, c, d],          # a quad split along a-c: a pair
+            [a, b, c], [a, c, d],          # the same quad, second triangle of another class: no pair
+            [a, b, c], [b, c, d],          # shares an edge, but not as (a, c, d): no pair
+            [a, b, c], [a, c, d], [a, d, e],   # a fan: the first two pair, the third stands alone
+            [a, b, c]]                     # last triangle of the world
+    cls = [1, 1, 2, 3, 1, 1, 5, 5, 5, 1]
+    from paper_2607_26005_amd.scenegen import Scene
+    v = np.asarray(tris, np.float32).reshape(-1, 9)
+    sc = Scene(2, v, np.asarray(cls, np.uint8), np.asarray([0, 9, 10], np.int64),
+               np.asarray([(-50.0, -50.0, 50.0, 50.0)] * 2, np.float32))
+    bn = O.bin_scene(sc, 16.0)
+    want = [(0, True), (2, False), (3, False), (4, False), (5, False), (6, True), (8, False), (9, False)]
+    got = [(int(p & 0x7FFFFFFF), bool(p >> 31)) for p in bn["prims"]]
+    assert got == want == _pairs_by_rule(sc)
+    assert bn["count"].sum() == len(want)
+
+
 def test_binner_home_cells_and_aabbs():
     from paper_2607_26005_amd import scenegen as sg
     wl = sg.make_config(2, num_worlds=2)
     sc = wl.scene
     b = O.bin_scene(sc, 16.0)
-    assert b["count"].sum() == sc.num_tris
+    rule = _pairs_by_rule(sc)
+    assert [(int(p & 0x7FFFFFFF), bool(p >> 31)) for p in b["prims"]] == rule
+    assert all(pr for _, pr in rule)            # the generators emit every quad as such a pair
+    assert b["count"].sum() == len(rule) == sc.num_tris // 2
     v = sc.verts.astype(np.float64).reshape(-1, 3, 3)
-    lo, hi = v.min(1), v.max(1)
+    # a primitive's vertices: its first triangle's and, for a pair, the next triangle's third vertex
+    pv = np.stack([np.concatenate([v[t], v[t + 1][2:3] if pr else v[t][2:3]]) for t, pr in rule])
+    lo, hi = pv.min(1), pv.max(1)
     mid = 0.5 * (lo + hi)
+    first = np.asarray([t for t, _ in rule])
     for w in range(sc.num_worlds):
         nx, ny = b["dims"][w]
-        a, e = sc.tri_offsets[w], sc.tri_offsets[w + 1]
-        cell = b["home"][a:e] - b["cell_base"][w]
+        sel = (first >= sc.tri_offsets[w]) & (first < sc.tri_offsets[w + 1])
+        cell = b["home"][sel] - b["cell_base"][w]
         ix, iy = cell % nx, cell // nx
         x0 = sc.bounds[w, 0] + 16.0 * ix
         y0 = sc.bounds[w, 1] + 16.0 * iy
-        inside = (mid[a:e, 0] >= sc.bounds[w, 0]) & (mid[a:e, 0] < sc.bounds[w, 2]) & \
-                 (mid[a:e, 1] >= sc.bounds[w, 1]) & (mid[a:e, 1] < sc.bounds[w, 3])
+        m = mid[sel]
+        inside = (m[:, 0] >= sc.bounds[w, 0]) & (m[:, 0] < sc.bounds[w, 2]) & \
+                 (m[:, 1] >= sc.bounds[w, 1]) & (m[:, 1] < sc.bounds[w, 3])
         tol = 1e-3
-        ok = (mid[a:e, 0] >= x0 - tol) & (mid[a:e, 0] <= x0 + 16 + tol) & \
-             (mid[a:e, 1] >= y0 - tol) & (mid[a:e, 1] <= y0 + 16 + tol)
+        ok = (m[:, 0] >= x0 - tol) & (m[:, 0] <= x0 + 16 + tol) & (m[:, 1] >= y0 - tol) & (m[:, 1] <= y0 + 16 + tol)
         assert np.all(ok[inside])
     home = b["home"]
     for c in np.random.default_rng(0).choice(len(b["count"]), 300, replace=False):
