@@ -300,9 +300,90 @@ static void coverage_fragments(const Params* P, Frame* F, const int32_t* vx, con
     }
 }
 
-/* Rasterize one snapped triangle (R6, R7) into the frame. */
-static void raster_tri(const Params* P, Frame* F, int32_t X0, int32_t Y0, int32_t X1, int32_t Y1,
-                       int32_t X2, int32_t Y2, float pa, float pb, float pc, uint32_t cls)
+/* R14 for a surface drawn as one convex 4-gon (a triangle pair, or a
+ * triangle clipped to four vertices): q[0..3] the snapped vertices in a
+ * positive order.  The same estimate over its four edges q_k -> q_(k+1):
+ * a = (((c_0 + c_1) + c_2) + c_3) - 3, clamped; the key at the centre is that
+ * of the plane given (the first piece's).  A pixel covered partly by each of
+ * the two pieces thus gets their summed coverage. */
+static void quad_fragments(const Params* P, Frame* F, const int32_t* qx, const int32_t* qy, float pa, float pb,
+                           float pc, uint32_t cls)
+{
+    int32_t lo_x = qx[0], hi_x = qx[0], lo_y = qy[0], hi_y = qy[0];
+    for (int k = 1; k < 4; ++k) {
+        if (qx[k] < lo_x) lo_x = qx[k];
+        if (qx[k] > hi_x) hi_x = qx[k];
+        if (qy[k] < lo_y) lo_y = qy[k];
+        if (qy[k] > hi_y) hi_y = qy[k];
+    }
+    int64_t i0 = floor_div256((int64_t)lo_x - 384 + 255), i1 = floor_div256((int64_t)hi_x + 128);
+    int64_t j0 = floor_div256((int64_t)lo_y - 384 + 255), j1 = floor_div256((int64_t)hi_y + 128);
+    if (i0 < 0) i0 = 0;
+    if (j0 < 0) j0 = 0;
+    if (i1 > P->W - 1) i1 = P->W - 1;
+    if (j1 > P->H - 1) j1 = P->H - 1;
+    float inv_len[4];
+    for (int e = 0; e < 4; ++e) {
+        int64_t dx = (int64_t)qx[(e + 1) % 4] - qx[e], dy = (int64_t)qy[(e + 1) % 4] - qy[e];
+        float len = sqrtf((float)(dx * dx + dy * dy));
+        inv_len[e] = 1.0f / (256.0f * len);
+    }
+    for (int64_t j = j0; j <= j1; ++j) {
+        for (int64_t i = i0; i <= i1; ++i) {
+            int64_t px = 256 * i + 128, py = 256 * j + 128;
+            float sum = 0.0f;
+            for (int e = 0; e < 4; ++e) {
+                int64_t ax = qx[e], ay = qy[e];
+                int64_t dx = (int64_t)qx[(e + 1) % 4] - ax, dy = (int64_t)qy[(e + 1) % 4] - ay;
+                int64_t E = dx * (py - ay) - dy * (px - ax);
+                float c = fmaf((float)E, inv_len[e], 0.5f);
+                if (c < 0.0f) c = 0.0f;
+                if (c > 1.0f) c = 1.0f;
+                sum = sum + c;
+            }
+            float a = sum - 3.0f;
+            if (a < 0.0f) a = 0.0f;
+            if (a > 1.0f) a = 1.0f;
+            uint32_t a8 = (uint32_t)rintf(255.0f * a);
+            if (a8 == 0u || a8 == 255u) continue;
+            float pxf = ((float)i + 0.5f) - P->cx;
+            float pyf = ((float)j + 0.5f) - P->cy;
+            float iz = fmaf(pa, pxf, fmaf(pb, pyf, pc));
+            uint32_t q;
+            if (!quantize_iz(P, iz, &q)) continue;
+            uint32_t key = (q << 8) | cls;
+            uint32_t o = ((key >> 16) << 16) | ((key & 255u) << 8) | (255u - a8);
+            int p = (int)(j * P->W + i);
+            if (o < F->frag[p]) F->frag[p] = o;
+        }
+    }
+}
+
+/* The snapped 4-gon (x[k], y[k]) as one surface for R14: when it is
+ * strictly convex (every turn of the same sign, none zero), its vertices in a
+ * positive order (reversed when every turn is negative) in qx, qy, and 1;
+ * otherwise 0 and each fan piece leaves its own fragments. */
+static int convex_quad(const int32_t* x, const int32_t* y, int32_t* qx, int32_t* qy)
+{
+    int pos = 0, neg = 0;
+    for (int k = 0; k < 4; ++k) {
+        int64_t ux = (int64_t)x[(k + 1) % 4] - x[k], uy = (int64_t)y[(k + 1) % 4] - y[k];
+        int64_t vx = (int64_t)x[(k + 2) % 4] - x[(k + 1) % 4], vy = (int64_t)y[(k + 2) % 4] - y[(k + 1) % 4];
+        int64_t cr = ux * vy - uy * vx;
+        if (cr > 0) ++pos;
+        if (cr < 0) ++neg;
+    }
+    if (pos != 4 && neg != 4) return 0;
+    static const int fwd[4] = {0, 1, 2, 3}, rev[4] = {0, 3, 2, 1};
+    const int* o = pos == 4 ? fwd : rev;
+    for (int k = 0; k < 4; ++k) { qx[k] = x[o[k]]; qy[k] = y[o[k]]; }
+    return 1;
+}
+
+/* Rasterize one snapped triangle (R6, R7) into the frame (with its R14
+ * fragments unless `frag` is 0: its surface leaves them as a whole). */
+static void raster_tri_f(const Params* P, Frame* F, int32_t X0, int32_t Y0, int32_t X1, int32_t Y1,
+                         int32_t X2, int32_t Y2, float pa, float pb, float pc, uint32_t cls, int frag)
 {
     int64_t area2 = (int64_t)(X1 - X0) * (int64_t)(Y2 - Y0) - (int64_t)(Y1 - Y0) * (int64_t)(X2 - X0);
     if (area2 == 0) return;
@@ -310,7 +391,7 @@ static void raster_tri(const Params* P, Frame* F, int32_t X0, int32_t Y0, int32_
         int32_t tx = X1, ty = Y1;
         X1 = X2; Y1 = Y2; X2 = tx; Y2 = ty;
     }
-    if (F->frag) {
+    if (F->frag && frag) {
         const int32_t vx[3] = {X0, X1, X2}, vy[3] = {Y0, Y1, Y2};
         coverage_fragments(P, F, vx, vy, pa, pb, pc, cls);
     }
@@ -365,6 +446,12 @@ static void raster_tri(const Params* P, Frame* F, int32_t X0, int32_t Y0, int32_
     }
 }
 
+static void raster_tri(const Params* P, Frame* F, int32_t X0, int32_t Y0, int32_t X1, int32_t Y1,
+                       int32_t X2, int32_t Y2, float pa, float pb, float pc, uint32_t cls)
+{
+    raster_tri_f(P, F, X0, Y0, X1, Y1, X2, Y2, pa, pb, pc, cls, 1);
+}
+
 /* One world-space triangle through R2..R7. */
 static void draw_triangle(const Params* P, const Cam* cam, Frame* F, const float* t, uint32_t cls)
 {
@@ -400,8 +487,47 @@ static void draw_triangle(const Params* P, const Cam* cam, Frame* F, const float
     int32_t SX[4], SY[4];
     for (int k = 0; k < np; ++k)
         if (!snap(P, poly[k], &SX[k], &SY[k])) return;
+    /* R14: a triangle clipped to a convex 4-gon leaves its fragments as one surface */
+    int32_t qx[4], qy[4];
+    const int whole = F->frag && np == 4 && convex_quad(SX, SY, qx, qy);
     for (int f = 1; f + 1 < np; ++f)
-        raster_tri(P, F, SX[0], SY[0], SX[f], SY[f], SX[f + 1], SY[f + 1], pa, pb, pc, cls);
+        raster_tri_f(P, F, SX[0], SY[0], SX[f], SY[f], SX[f + 1], SY[f + 1], pa, pb, pc, cls, !whole);
+    if (whole) quad_fragments(P, F, qx, qy, pa, pb, pc, cls);
+}
+
+/* A triangle pair (a, b, c), (a, c, d) of the scene (see oracle_bin's pairing
+ * rule).  Its two triangles are drawn by R2..R7 exactly as two separate
+ * triangles; for R14 the pair is one surface when all four vertices lie in
+ * front of the near plane, neither triangle lies wholly beyond far, both
+ * triangles are drawn (every snap within range, both planes defined) and the
+ * snapped 4-gon (a, b, c, d) is strictly convex: its fragments then come from
+ * the 4-gon with the first triangle's plane. */
+static void draw_pair(const Params* P, const Cam* cam, Frame* F, const float* t1, const float* t2, uint32_t cls)
+{
+    if (!F->frag) {
+        draw_triangle(P, cam, F, t1, cls);
+        draw_triangle(P, cam, F, t2, cls);
+        return;
+    }
+    V3 v[4];
+    for (int k = 0; k < 3; ++k) v[k] = to_view(cam, t1[3 * k], t1[3 * k + 1], t1[3 * k + 2]);
+    v[3] = to_view(cam, t2[6], t2[7], t2[8]);
+    int all4 = v[0].z >= P->nearp && v[1].z >= P->nearp && v[2].z >= P->nearp && v[3].z >= P->nearp;
+    int far0 = v[0].z > P->farp && v[1].z > P->farp && v[2].z > P->farp;
+    int far1 = v[0].z > P->farp && v[2].z > P->farp && v[3].z > P->farp;
+    float pa0, pb0, pc0, pa1, pb1, pc1;
+    int32_t SX[4], SY[4], qx[4], qy[4];
+    int ok = all4 && !far0 && !far1 && depth_plane(cam, P, t1, &pa0, &pb0, &pc0) &&
+             depth_plane(cam, P, t2, &pa1, &pb1, &pc1);
+    for (int k = 0; k < 4 && ok; ++k) ok = snap(P, v[k], &SX[k], &SY[k]);
+    if (!ok || !convex_quad(SX, SY, qx, qy)) {
+        draw_triangle(P, cam, F, t1, cls);
+        draw_triangle(P, cam, F, t2, cls);
+        return;
+    }
+    raster_tri_f(P, F, SX[0], SY[0], SX[1], SY[1], SX[2], SY[2], pa0, pb0, pc0, cls, 0);
+    raster_tri_f(P, F, SX[0], SY[0], SX[2], SY[2], SX[3], SY[3], pa1, pb1, pc1, cls, 0);
+    quad_fragments(P, F, qx, qy, pa0, pb0, pc0, cls);
 }
 
 static const int BOX_TRIS[12][3] = {
@@ -568,8 +694,14 @@ int oracle_render(int num_worlds, const int64_t* tri_offsets, const float* verts
                 if (F.cover) F.cover[p] = 0;
                 if (F.frag) F.frag[p] = 0xFFFFFFFFu;
             }
-            for (int64_t t = tri_offsets[w]; t < tri_offsets[w + 1]; ++t)
-                draw_triangle(&P, &cam, &F, verts + 9 * t, tcls[t]);
+            for (int64_t t = tri_offsets[w]; t < tri_offsets[w + 1];) {
+                const float* a = verts + 9 * t;
+                int pair = t + 1 < tri_offsets[w + 1] && tcls[t] == tcls[t + 1] && memcmp(a, a + 9, 12) == 0 &&
+                           memcmp(a + 6, a + 12, 12) == 0;
+                if (pair) draw_pair(&P, &cam, &F, a, a + 9, tcls[t]);
+                else draw_triangle(&P, &cam, &F, a, tcls[t]);
+                t += pair ? 2 : 1;
+            }
             for (int64_t b = 0; b < agents_per_world; ++b) {
                 int64_t h = w * agents_per_world + b;
                 if (h == g) continue; /* the ego's own body is not drawn */

@@ -835,17 +835,23 @@ __device__ __forceinline__ int setup_triangle(const RenderParams& P, Shared& S, 
     return ok ? np : 0;
 }
 
-// R14 (colour antialiasing): the fragments a fan piece leaves on the pixels
-// its edges cross.  For every tile pixel whose centre lies within one pixel
-// of the piece's snapped bounding box: with E_k the exact edge function of R6
-// at the centre (no top-left bias) and L_k the edge's length in subpixels,
-// E_k / (256 L_k) is the centre's distance to the edge in pixels (positive
-// inside); c_k = min(max(fma(fl(E_k), fl(1 / (256 L_k)), 0.5), 0), 1),
-// coverage a = min(max(((c_0 + c_1) + c_2) - 2, 0), 1), a8 = rint(255 a).  A
-// pixel with 0 < a8 < 255 whose key (R7, the piece's plane at the centre)
-// exists takes the minimum of (key >> 16) << 16 | (key & 255) << 8 |
-// (255 - a8) in the edge buffer.  fl(E_k) is the same value whichever exact
-// integer type carries E_k.
+// R14 (colour antialiasing): the fragments a surface leaves on the pixels its
+// edges cross.  A surface is a fan piece, or a whole convex 4-gon: a pair
+// whose two halves are both drawn, or a triangle clipped to four vertices,
+// when the snapped 4-gon is strictly convex (its pieces then leave no
+// fragments of their own, so the diagonal does not cut the coverage of a
+// surface narrower than a pixel).  For every tile pixel whose centre lies
+// within one pixel of the surface's snapped bounding box: with E_k the exact
+// edge function of R6 at the centre (no top-left bias) and L_k the edge's
+// length in subpixels, E_k / (256 L_k) is the centre's distance to the edge in
+// pixels (positive inside); c_k = min(max(fma(fl(E_k), fl(1 / (256 L_k)),
+// 0.5), 0), 1), coverage a = min(max(((c_0 + c_1) + c_2) - 2, 0), 1) for a
+// triangle (edges b->c, c->a, a->b) and min(max((((c_0 + c_1) + c_2) + c_3) -
+// 3, 0), 1) for a 4-gon (edges p_k -> p_k+1), a8 = rint(255 a).  A pixel with
+// 0 < a8 < 255 whose key (R7, the first piece's plane at the centre) exists
+// takes the minimum of (key >> 16) << 16 | (key & 255) << 8 | (255 - a8) in
+// the edge buffer.  fl(E_k) is the same value whichever exact integer type
+// carries E_k.
 __device__ __forceinline__ float aa_cover(double e, float r)
 {
     return fminf(fmaxf(fmaf((float)e, r, 0.5f), 0.0f), 1.0f);
@@ -856,12 +862,13 @@ __device__ __forceinline__ float aa_cover(int e, float r)
     return fminf(fmaxf(fmaf((float)e, r, 0.5f), 0.0f), 1.0f);
 }
 
-// Coverage fragment of one pixel (c the three edge coverages): the edge
-// buffer word, or 0xFFFFFFFF when the pixel takes none.
-__device__ __forceinline__ uint32_t aa_fragment(const RenderParams& P, float c0, float c1, float c2, float pxf,
-                                                float pyf, float pa, float pb, float pc, uint32_t cls)
+// Coverage fragment of one pixel (c the edge coverages, c3 used by a 4-gon
+// only): the edge buffer word, or 0xFFFFFFFF when the pixel takes none.
+__device__ __forceinline__ uint32_t aa_fragment(const RenderParams& P, bool q4, float c0, float c1, float c2, float c3,
+                                                float pxf, float pyf, float pa, float pb, float pc, uint32_t cls)
 {
-    const float a = fminf(fmaxf(((c0 + c1) + c2) - 2.0f, 0.0f), 1.0f);
+    const float s = (c0 + c1) + c2;
+    const float a = fminf(fmaxf(q4 ? (s + c3) - 3.0f : s - 2.0f, 0.0f), 1.0f);
     const uint32_t a8 = (uint32_t)rintf(255.0f * a);
     const uint32_t key = pixel_key(P, pxf, pyf, pa, pb, pc, cls);
     const bool frag = a8 != 0u && a8 != 255u && key != 0xFFFFFFFFu;
@@ -876,14 +883,15 @@ __device__ __forceinline__ uint32_t aa_fragment(const RenderParams& P, float c0,
 constexpr int kAaSmall = 64;   // most window pixels of a packed piece
 
 __device__ __forceinline__ void aa_packed(const RenderParams& P, WaveLds& L, uint32_t* fbo, const Tile& T, bool on,
-                                          int i0, int j0, int w, int npx_, const int* e, const int* sa,
-                                          const int* sb, const float* r, float pa, float pb, float pc, uint32_t cls)
+                                          bool q4, bool any4, int i0, int j0, int w, int npx_, const int* e,
+                                          const int* sa, const int* sb, const float* r, float pa, float pb, float pc,
+                                          uint32_t cls)
 {
     const int lane = lane_id();
     const uint32_t npx = on ? (uint32_t)npx_ : 0u;
     const uint32_t incl = wave_incl_sum(npx);
     const uint32_t n = readlane(incl, 63), pre = incl - npx;
-    const uint32_t geo = (uint32_t)i0 | (uint32_t)j0 << 8 | (uint32_t)w << 16 | cls << 24;
+    const uint32_t geo = (uint32_t)i0 | (q4 ? 128u : 0u) | (uint32_t)j0 << 8 | (uint32_t)w << 16 | cls << 24;
     const float rw = __builtin_amdgcn_rcpf((float)w);   // row = floor((p + 0.5) / w) for p < 2^12
     uint32_t carry = 0;
     uint32_t* mark = L.u.cells.start;
@@ -902,17 +910,19 @@ __device__ __forceinline__ void aa_packed(const RenderParams& P, WaveLds& L, uin
         const int tn = (int)bperm(t, npx);
         const int jj = (int)(((float)p + 0.5f) * __uint_as_float(bperm(t, __float_as_uint(rw))));
         const int ii = p - jj * tw;
-        const int x = (int)(g & 255u) + ii, y = (int)((g >> 8) & 255u) + jj;   // tile pixel
-        float c[3];
+        const int x = (int)(g & 127u) + ii, y = (int)((g >> 8) & 255u) + jj;   // tile pixel
+        float c[4] = {0.0f, 0.0f, 0.0f, 1.0f};
 #pragma unroll
-        for (int k = 0; k < 3; ++k) {
+        for (int k = 0; k < 4; ++k) {
+            if (k == 3 && !any4) break;
             const int ek = (int)bperm(t, (uint32_t)e[k]) + __mul24((int)bperm(t, (uint32_t)sa[k]), ii) +
                            __mul24((int)bperm(t, (uint32_t)sb[k]), jj);
             c[k] = aa_cover(ek, __uint_as_float(bperm(t, __float_as_uint(r[k]))));
         }
         const float pxf = ((float)(T.x0 + x) + 0.5f) - P.cx;
         const float pyf = ((float)(T.y0 + y) + 0.5f) - P.cy;
-        const uint32_t f = aa_fragment(P, c[0], c[1], c[2], pxf, pyf, __uint_as_float(bperm(t, __float_as_uint(pa))),
+        const uint32_t f = aa_fragment(P, (g & 128u) != 0u, c[0], c[1], c[2], c[3], pxf, pyf,
+                                       __uint_as_float(bperm(t, __float_as_uint(pa))),
                                        __uint_as_float(bperm(t, __float_as_uint(pb))),
                                        __uint_as_float(bperm(t, __float_as_uint(pc))), g >> 24);
         // p in range keeps the address inside the window, hence the tile
@@ -922,57 +932,72 @@ __device__ __forceinline__ void aa_packed(const RenderParams& P, WaveLds& L, uin
     }
 }
 
-// Window of a piece: the tile pixels whose centre lies within one pixel of
-// its snapped bounding box, 256 i + 128 in [minX - 256, maxX + 256].  Pieces
-// whose window has at most kAaSmall pixels and whose box spans below 2^14
-// subpixels take the packed path; the others are swept by the whole wave one
-// at a time in 8x8 blocks (lane = pixel), E_k evaluated in fp64 from its exact
-// integer value at the tile origin plus exact integer steps: exact while
+// Window of a surface: the tile pixels whose centre lies within one pixel of
+// its snapped bounding box, 256 i + 128 in [minX - 256, maxX + 256].
+// Surfaces whose window has at most kAaSmall pixels and whose box spans below
+// 2^14 subpixels take the packed path; the others are swept by the whole wave
+// one at a time in 8x8 blocks (lane = pixel), E_k evaluated in fp64 from its
+// exact integer value at the tile origin plus exact integer steps: exact while
 // |E_k| < 2^53, and beyond that c_k is 0 or 1 whatever the rounding
 // (|E_k| / (256 L_k) > 2^14 with L_k < 2^31).  c_k grows with E_k, so a block
 // whose largest E_k gives c_k = 0 for some edge, or whose smallest E_k give
-// c_k = 1 for every edge, has no fragment and is skipped.
-__device__ void aa_pieces(const RenderParams& P, WaveLds& L, uint32_t* fbo, const Tile& T, bool ok, int ax, int ay,
-                          int bx, int by, int cx, int cy, float pa, float pb, float pc, uint32_t cls)
+// c_k = 1 for every edge, has no fragment and is skipped.  The surface is the
+// triangle (a, b, c) in either orientation, or with q4 the 4-gon (a, b, c, d)
+// in positive orientation; a triangle's fourth edge is a constant c_3 = 1
+// that its coverage does not use.
+__device__ void aa_pieces(const RenderParams& P, WaveLds& L, uint32_t* fbo, const Tile& T, bool ok, bool q4, int ax,
+                          int ay, int bx, int by, int cx, int cy, int dx4, int dy4, float pa, float pb, float pc,
+                          uint32_t cls)
 {
     const int lane = lane_id(), lx = lane & 7, ly = lane >> 3;
     int i0 = 0, i1 = -1, j0 = 0, j1 = -1;
-    int dxs[3] = {0, 0, 0}, dys[3] = {0, 0, 0};
-    long long e0[3] = {0, 0, 0};
-    float rden[3] = {0.0f, 0.0f, 0.0f};
+    int dxs[4] = {0, 0, 0, 0}, dys[4] = {0, 0, 0, 0};
+    long long e0[4] = {0, 0, 0, 1ll << 30};
+    float rden[4] = {0.0f, 0.0f, 0.0f, 1.0f};
     bool small = false;
     if (ok) {
-        const long long area2 = (long long)(bx - ax) * (long long)(cy - ay) - (long long)(by - ay) * (long long)(cx - ax);
-        if (area2 < 0) {
-            const int tx = bx, ty = by;
-            bx = cx; by = cy; cx = tx; cy = ty;
+        int vx[4], vy[4];   // edge k runs from v_k to v_k+1 (cyclically over 3 or 4)
+        if (q4) {
+            vx[0] = ax; vx[1] = bx; vx[2] = cx; vx[3] = dx4;
+            vy[0] = ay; vy[1] = by; vy[2] = cy; vy[3] = dy4;
+        } else {
+            const long long area2 =
+                (long long)(bx - ax) * (long long)(cy - ay) - (long long)(by - ay) * (long long)(cx - ax);
+            if (area2 < 0) {
+                const int tx = bx, ty = by;
+                bx = cx; by = cy; cx = tx; cy = ty;
+            }
+            ok = area2 != 0;
+            vx[0] = bx; vx[1] = cx; vx[2] = ax; vx[3] = ax;
+            vy[0] = by; vy[1] = cy; vy[2] = ay; vy[3] = ay;
         }
-        const int minX = min(ax, min(bx, cx)), maxX = max(ax, max(bx, cx));
-        const int minY = min(ay, min(by, cy)), maxY = max(ay, max(by, cy));
+        const int minX = min(min(vx[0], vx[1]), min(vx[2], vx[3])), maxX = max(max(vx[0], vx[1]), max(vx[2], vx[3]));
+        const int minY = min(min(vy[0], vy[1]), min(vy[2], vy[3])), maxY = max(max(vy[0], vy[1]), max(vy[2], vy[3]));
         i0 = max((minX - 384 + 255) >> 8, T.x0) - T.x0; i1 = min((maxX + 128) >> 8, T.x0 + T.w - 1) - T.x0;
         j0 = max((minY - 384 + 255) >> 8, T.y0) - T.y0; j1 = min((maxY + 128) >> 8, T.y0 + T.h - 1) - T.y0;
-        ok = area2 != 0 && i0 <= i1 && j0 <= j1;
+        ok = ok && i0 <= i1 && j0 <= j1;
         small = ok && (maxX - minX) < 16384 && (maxY - minY) < 16384 && (i1 - i0 + 1) * (j1 - j0 + 1) <= kAaSmall;
         // edge functions at the window's first pixel (small) or at the tile's
         const int px0 = 256 * (T.x0 + (small ? i0 : 0)) + 128, py0 = 256 * (T.y0 + (small ? j0 : 0)) + 128;
-        const int ex[3] = {bx, cx, ax}, ey[3] = {by, cy, ay};
-        const int fx[3] = {cx, ax, bx}, fy[3] = {cy, ay, by};
 #pragma unroll
-        for (int k = 0; k < 3; ++k) {
-            const int dx = fx[k] - ex[k], dy = fy[k] - ey[k];
-            e0[k] = (long long)dx * (long long)(py0 - ey[k]) - (long long)dy * (long long)(px0 - ex[k]);
+        for (int k = 0; k < 4; ++k) {
+            if (k == 3 && !q4) break;
+            const int nk = k == 3 || (k == 2 && !q4) ? 0 : k + 1;
+            const int dx = vx[nk] - vx[k], dy = vy[nk] - vy[k];
+            e0[k] = (long long)dx * (long long)(py0 - vy[k]) - (long long)dy * (long long)(px0 - vx[k]);
             dxs[k] = dx;
             dys[k] = dy;
             const float len = sqrtf((float)((long long)dx * dx + (long long)dy * dy));
             rden[k] = 1.0f / (256.0f * len);
         }
     }
+    const bool any4 = __ballot(ok && q4) != 0;
     if (__ballot(small) != 0) {
-        const int e[3] = {(int)e0[0], (int)e0[1], (int)e0[2]};
-        const int sa[3] = {-256 * dys[0], -256 * dys[1], -256 * dys[2]};
-        const int sb[3] = {256 * dxs[0], 256 * dxs[1], 256 * dxs[2]};
-        aa_packed(P, L, fbo, T, small, i0, j0, i1 - i0 + 1, (i1 - i0 + 1) * (j1 - j0 + 1), e, sa, sb, rden, pa, pb, pc,
-                  cls);
+        const int e[4] = {(int)e0[0], (int)e0[1], (int)e0[2], (int)e0[3]};
+        const int sa[4] = {-256 * dys[0], -256 * dys[1], -256 * dys[2], -256 * dys[3]};
+        const int sb[4] = {256 * dxs[0], 256 * dxs[1], 256 * dxs[2], 256 * dxs[3]};
+        aa_packed(P, L, fbo, T, small, q4, any4, i0, j0, i1 - i0 + 1, (i1 - i0 + 1) * (j1 - j0 + 1), e, sa, sb, rden,
+                  pa, pb, pc, cls);
     }
     uint64_t m = __ballot(ok && !small);
     while (m) {
@@ -980,10 +1005,11 @@ __device__ void aa_pieces(const RenderParams& P, WaveLds& L, uint32_t* fbo, cons
         m &= m - 1;
         const int ri0 = (int)readlane((uint32_t)i0, l), ri1 = (int)readlane((uint32_t)i1, l);
         const int rj0 = (int)readlane((uint32_t)j0, l), rj1 = (int)readlane((uint32_t)j1, l);
-        double re[3], rsx[3], rsy[3];
-        float rr[3];
+        const bool rq4 = readlane(q4 ? 1u : 0u, l) != 0u;
+        double re[4], rsx[4], rsy[4];
+        float rr[4];
 #pragma unroll
-        for (int k = 0; k < 3; ++k) {
+        for (int k = 0; k < 4; ++k) {
             const unsigned long long u = (unsigned long long)e0[k];
             re[k] = (double)(long long)(((unsigned long long)readlane((uint32_t)(u >> 32), l) << 32) |
                                         readlane((uint32_t)u, l));
@@ -1003,7 +1029,7 @@ __device__ void aa_pieces(const RenderParams& P, WaveLds& L, uint32_t* fbo, cons
                 const int bj0 = rj0 + 8 * ly, bj1 = min(bj0 + 7, rj1);
                 bool out = false, in = true;
 #pragma unroll
-                for (int k = 0; k < 3; ++k) {
+                for (int k = 0; k < 4; ++k) {
                     const double emax = fma(rsy[k], (double)(rsy[k] > 0.0 ? bj1 : bj0),
                                             fma(rsx[k], (double)(rsx[k] > 0.0 ? bi1 : bi0), re[k]));
                     const double emin = fma(rsy[k], (double)(rsy[k] > 0.0 ? bj0 : bj1),
@@ -1021,9 +1047,10 @@ __device__ void aa_pieces(const RenderParams& P, WaveLds& L, uint32_t* fbo, cons
             const int i = ri0 + 8 * (b & 7) + lx, j = rj0 + 8 * (b >> 3) + ly;   // tile pixel
             if (i > ri1 || j > rj1) continue;
             const double di = (double)i, dj = (double)j;
-            const uint32_t f = aa_fragment(P, aa_cover(fma(rsy[0], dj, fma(rsx[0], di, re[0])), rr[0]),
+            const uint32_t f = aa_fragment(P, rq4, aa_cover(fma(rsy[0], dj, fma(rsx[0], di, re[0])), rr[0]),
                                            aa_cover(fma(rsy[1], dj, fma(rsx[1], di, re[1])), rr[1]),
                                            aa_cover(fma(rsy[2], dj, fma(rsx[2], di, re[2])), rr[2]),
+                                           aa_cover(fma(rsy[3], dj, fma(rsx[3], di, re[3])), rr[3]),
                                            ((float)(T.x0 + i) + 0.5f) - P.cx, ((float)(T.y0 + j) + 0.5f) - P.cy, rpa,
                                            rpb, rpc, rcls);
             atomicMin(&fbo[j * 64 + i], f);
@@ -1040,6 +1067,7 @@ __device__ __forceinline__ void exact_pass(const RenderParams& P, Shared& S, Wav
     uint32_t cls = 0;
     int np = 0;
     bool quad = false;   // a whole pair: the 4-gon (a, b, c, d), every vertex in front of the near plane
+    bool snap0 = true, snap1 = true;   // a whole pair's halves: every vertex snapped
     int X0 = 0, Y0 = 0, X1 = 0, Y1 = 0, X2 = 0, Y2 = 0, X3 = 0, Y3 = 0;
     if (live) {
         quad = load_entry(P, entry, abase_w, lbase_w, tri, cls);
@@ -1052,8 +1080,14 @@ __device__ __forceinline__ void exact_pass(const RenderParams& P, Shared& S, Wav
             // the pair's halves (a, b, c) and (a, c, d) are the fan pieces of (a, b, c, d)
             float x3, y3, z3;
             view_xform(cam, tri[9], tri[10], tri[11], x3, y3, z3);
-            ok = snap_vertex(P, xv[0], yv[0], zv[0], X0, Y0) && snap_vertex(P, xv[1], yv[1], zv[1], X1, Y1) &&
-                 snap_vertex(P, xv[2], yv[2], zv[2], X2, Y2) && snap_vertex(P, x3, y3, z3, X3, Y3);
+            const bool s0 = snap_vertex(P, xv[0], yv[0], zv[0], X0, Y0);
+            const bool s1 = snap_vertex(P, xv[1], yv[1], zv[1], X1, Y1);
+            const bool s2 = snap_vertex(P, xv[2], yv[2], zv[2], X2, Y2);
+            const bool s3 = snap_vertex(P, x3, y3, z3, X3, Y3);
+            // R5: a vertex out of range drops only the halves that use it
+            snap0 = s0 && s1 && s2;
+            snap1 = s0 && s2 && s3;
+            ok = snap0 || snap1;
             np = 4;
         } else if (in0 && in1 && in2) {
             ok = snap_vertex(P, xv[0], yv[0], zv[0], X0, Y0) && snap_vertex(P, xv[1], yv[1], zv[1], X1, Y1) &&
@@ -1101,7 +1135,8 @@ __device__ __forceinline__ void exact_pass(const RenderParams& P, Shared& S, Wav
     // R3 depth planes: the unclipped triangle's, shared by the fan pieces of a
     // clipped triangle; each half of a pair has its own
     float pa0 = 0.0f, pb0 = 0.0f, pc0 = 0.0f;
-    bool ok0 = np != 0 && depth_plane(P, cam, tri, pa0, pb0, pc0);
+    const bool okp0 = np != 0 && depth_plane(P, cam, tri, pa0, pb0, pc0);
+    bool ok0 = okp0 && snap0;
     float pa1 = pa0, pb1 = pb0, pc1 = pc0;
     bool ok1 = ok0;
     if (__ballot(quad) != 0) {
@@ -1110,7 +1145,29 @@ __device__ __forceinline__ void exact_pass(const RenderParams& P, Shared& S, Wav
         const bool okq = depth_plane(P, cam, t2, qa, qb, qc);
         if (quad) {
             pa1 = qa; pb1 = qb; pc1 = qc;
-            ok1 = np != 0 && okq;
+            ok1 = np != 0 && okq && snap1;
+        }
+    }
+    // R14: a 4-gon (whole pair or clipped triangle) with both pieces drawn
+    // is one surface when strictly convex; (q_k) its positive order
+    bool aaq = false;
+    int qx[4] = {X0, X1, X2, X3}, qy[4] = {Y0, Y1, Y2, Y3};
+    if constexpr (kAA) {
+        if (np == 4 && ok0 && ok1) {
+            int pos = 0, neg = 0;
+#pragma unroll
+            for (int k = 0; k < 4; ++k) {
+                const int k1 = (k + 1) & 3, k2 = (k + 2) & 3;
+                const long long cr = (long long)(qx[k1] - qx[k]) * (long long)(qy[k2] - qy[k1]) -
+                                     (long long)(qy[k1] - qy[k]) * (long long)(qx[k2] - qx[k1]);
+                pos += cr > 0;
+                neg += cr < 0;
+            }
+            aaq = pos == 4 || neg == 4;
+            if (neg == 4) {   // (q0, q3, q2, q1)
+                qx[1] = X3; qy[1] = Y3;
+                qx[3] = X1; qy[3] = Y1;
+            }
         }
     }
     const int px0 = 256 * T.x0 + 128, py0 = 256 * T.y0 + 128;
@@ -1144,7 +1201,11 @@ __device__ __forceinline__ void exact_pass(const RenderParams& P, Shared& S, Wav
                 }
             }
         }
-        if constexpr (kAA) aa_pieces(P, L, fbo, T, piece, ax, ay, bx, by, cx, cy, pa, pb, pc, cls);
+        if constexpr (kAA) {
+            const bool sq = aaq && f == 0;   // the whole surface, with the first piece's plane
+            aa_pieces(P, L, fbo, T, sq || (piece && !aaq), sq, sq ? qx[0] : ax, sq ? qy[0] : ay, sq ? qx[1] : bx,
+                      sq ? qy[1] : by, sq ? qx[2] : cx, sq ? qy[2] : cy, qx[3], qy[3], pa, pb, pc, cls);
+        }
         // edge setup: edges v1->v2, v2->v0, v0->v1 at the tile's pixel (0, 0),
         // in the int32 form (floor(c / 256), -dy, dx) when every value fits
         uint32_t rv[12] = {0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};

@@ -169,3 +169,57 @@ def test_coplanar_neighbours_blend_across_their_shared_edge():
     assert all(tuple(rgb[:, j, 10]) == want for j in range(64))
     assert (rgb[:, :, 11:] == np.asarray(PAL[LANE], np.uint8)[:, None, None]).all()
     assert (rgb[:, :, :10] == np.asarray(PAL[WALL], np.uint8)[:, None, None]).all()
+
+
+def _strip(xl, xr):
+    """A marking 500 rows tall between columns xl and xr, built as one
+    triangle pair (a, b, c), (a, c, d) split along its diagonal."""
+    return quad((D, _y(xl), _z(300.0)), (D, _y(xr), _z(300.0)), (D, _y(xr), _z(-200.0)), (D, _y(xl), _z(-200.0)))
+
+
+def test_split_strip_narrower_than_a_pixel_blends_at_full_width():
+    # a 76/256 px wide strip inside pixel 20 (no centre covered): the pair is
+    # one surface, so every row blends the strip's whole width, 255 * 76/256
+    # rounded = 76, wherever the diagonal crosses the row
+    o = _render(_strip(XL, XR), [LANE, LANE])
+    assert (o["cls"][0] == SKY).all()
+    rgb = o["rgb"][0]
+    want = _blend(PAL[LANE], PAL[SKY], 76)
+    assert all(tuple(rgb[:, j, 20]) == want for j in range(64)), [tuple(rgb[:, j, 20]) for j in (0, 31, 63)]
+    mask = np.ones((64, 64), bool)
+    mask[:, 20] = False
+    assert (rgb[:, mask] == np.asarray(PAL[SKY], np.uint8)[:, None]).all()
+    # the same two triangles in the other order are not a pair: each half is
+    # then its own surface and only the larger piece of the row shows
+    t = _strip(XL, XR)
+    p = _render([t[1], t[0]], [LANE, LANE])
+    a8 = [int(np.rint((int(p["rgb"][0][0, j, 20]) - PAL[SKY][0]) * 255 / (PAL[LANE][0] - PAL[SKY][0])))
+          for j in range(64)]
+    assert max(a8) < 76 and min(a8) > 0, a8
+
+
+def test_split_wide_strip_keeps_its_edge_coverage():
+    # 2.25 px wide (columns 20.25 .. 22.5): pixel 20 holds three quarters of
+    # its area (centre covered: plain strip), 22 half of it (centre on the
+    # right edge, which the top-left rule leaves out: sky under a half blend)
+    o = _render(_strip(20.25, 22.5), [LANE, LANE])
+    rgb = o["rgb"][0]
+    assert (o["cls"][0][:, 20:22] == LANE).all() and (o["cls"][0][:, 22] == SKY).all()
+    assert (rgb[:, :, 20:22] == np.asarray(PAL[LANE], np.uint8)[:, None, None]).all()
+    want = _blend(PAL[LANE], PAL[SKY], 128)   # rint(255 * 0.5)
+    assert all(tuple(rgb[:, j, 22]) == want for j in range(64))
+
+
+def _dart():
+    return (D, _y(18.0), _z(60.0)), (D, _y(30.0), _z(50.0)), (D, _y(21.0), _z(30.0)), (D, _y(30.0), _z(10.0))
+
+
+def test_pair_that_is_not_convex_keeps_per_triangle_fragments():
+    # a dart (reflex vertex at c) is no convex surface: its two triangles
+    # leave their own fragments, exactly as the same triangles do when listed
+    # in the other order (which does not pair them)
+    a, b, c, d = _dart()
+    paired = _render([[a, b, c], [a, c, d]], [LANE, LANE])
+    apart = _render([[a, c, d], [a, b, c]], [LANE, LANE])
+    assert (paired["cls"][0] == LANE).sum() > 0
+    assert np.array_equal(paired["rgb"][0], apart["rgb"][0])

@@ -12,6 +12,7 @@ from paper_2607_26005_amd import scenegen as sg
 from tests.parity import assert_parity
 from tests.scenes import make_agents, make_rig, make_scene, quad
 from tests import test_aa as pins
+from tests import test_oracle_pins as pin_scenes
 
 pytestmark = pytest.mark.gpu
 
@@ -77,12 +78,18 @@ def test_aa_pin_scenes_bit_exact(lib):
     rig = make_rig(res=64, f=64.0, mounts=((0.0, 0.0, 0.0, 1.0, 0.0),))
     left = quad((16.0, pins._y(-400.0), pins._z(300.0)), (16.0, pins._y(10.75), pins._z(300.0)),
                 (16.0, pins._y(10.75), pins._z(-200.0)), (16.0, pins._y(-400.0), pins._z(-200.0)))
+    da, db, dc, dd = pins._dart()
     scenes = {
         "edge": (pins._wall(10.75), [7, 7]),
         "sliver": (pins._sliver(pins.XL, pins.XR, pins.XB), [2]),
         "sliver-front": (pins._sliver(pins.XL, pins.XR, pins.XB, x=12.0) + pins._wall(0.0), [2, 7, 7]),
         "sliver-behind": (pins._sliver(pins.XL, pins.XR, pins.XB, x=24.0) + pins._wall(0.0), [2, 7, 7]),
         "coplanar": (left + pins._wall(10.75), [7, 7, 2, 2]),
+        "split-strip": (pins._strip(pins.XL, pins.XR), [2, 2]),
+        "split-strip-unpaired": (pins._strip(pins.XL, pins.XR)[::-1], [2, 2]),
+        "split-wide-strip": (pins._strip(20.25, 22.5), [2, 2]),
+        "dart": ([[da, db, dc], [da, dc, dd]], [2, 2]),
+        "unsnappable-vertex": (pin_scenes._pair_with_unsnappable_vertex()[0], [7, 7]),
     }
     for name, (tris, cls) in scenes.items():
         sc = make_scene(np.asarray(tris, np.float32), cls)

@@ -165,6 +165,33 @@ def test_triangle_wholly_beyond_far_is_not_drawn():
     assert np.array_equal(r2["cls"][0] == 7, want)
 
 
+def _pair_with_unsnappable_vertex():
+    """Pair (a, b, c), (a, c, d) at 16 m (f = 64: column 32 - 4 y, row 32 - 4 z)
+    whose vertex d sits just past the near plane 40 km to the side: it
+    projects 64 * 40000 / 0.5625 ~ 4.6e6 px from the centre, beyond the 2^21
+    px (2^29 subpixel) range of R5."""
+    a, b, c = (16.0, 6.0, 6.0), (16.0, -2.0, 6.0), (16.0, -2.0, -2.0)   # columns/rows 8 and 40
+    d = (0.5625, 40000.0, 0.0)
+    assert 64.0 * 40000.0 / 0.5625 > 2.0 ** 21
+    return [[a, b, c], [a, c, d]], [a, b, c]
+
+
+def test_vertex_out_of_snap_range_drops_only_its_triangles():
+    # R5 drops the triangles that use the vertex, not the whole pair: the
+    # image is that of (a, b, c) alone, which the float64 ray cast confirms
+    pair, first = _pair_with_unsnappable_vertex()
+    ag = make_agents([ego()])
+    rig = make_rig(res=64, f=64.0)
+    r = O.render(make_scene(np.asarray(pair, np.float32), [7, 7]), ag, rig, want_rgb=True, antialias=True)
+    alone = make_scene(np.asarray([first], np.float32), [7])
+    r1 = O.render(alone, ag, rig, want_rgb=True, antialias=True)
+    assert (r["cls"][0] == 7).sum() > 400
+    assert np.array_equal(r["cls"], r1["cls"]) and np.array_equal(r["depth"], r1["depth"])
+    assert np.array_equal(r["rgb"], r1["rgb"])
+    rc, _, _ = raycast_view(alone, ag, rig, 0)
+    assert ((r["cls"][0] == 7) != (rc == 7)).sum() <= 40   # only on the triangle's edges
+
+
 def test_depth_error_bound_over_distances():
     # Fronto squares (half-size D/16, 2 px) at 200 seeded distances D in [0.6, 95] m: the decoded depth
     # at the image centre is within 2^-21 (the bucket midpoint) plus a few
