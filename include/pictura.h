@@ -296,7 +296,7 @@ pictura_status pictura_bins_info(pictura_ctx ctx, int32_t* dims, int64_t* cell_b
 pictura_status pictura_bins_copy(pictura_ctx ctx, uint32_t* cell_start, float* cell_aabb, uint32_t* perm);
 
 #define PICTURA_OPT_CULL   1 /* 1 (default): cell + triangle frustum culling; 0: every triangle of the world */
-#define PICTURA_OPT_TILE   2 /* 0 (default): 64x64 LDS tiles; n in 8..64: force n x n tiles */
+#define PICTURA_OPT_TILE   2 /* 0 (default): 64x64 LDS tiles; n in 8..64: force n x n tiles (antialiased colour: at most 32 columns wide) */
 #define PICTURA_OPT_STATS  3 /* 1: count the render kernel's work (cells, triangles, pixels); 0 (default): off */
 /* Set a context option.  Images never depend on any option. */
 pictura_status pictura_set_option(pictura_ctx ctx, int32_t option, int32_t value);
@@ -312,11 +312,15 @@ pictura_status pictura_set_option(pictura_ctx ctx, int32_t option, int32_t value
  * chunks of 64 candidates, then shader-clock cycles summed over waves spent
  * in:
  * prologue, cell and agent tests, first pass, exact pass (with records),
- * record raster (part of the exact pass), final barrier and write-out.
+ * record raster (part of the exact pass), final barrier and write-out; then,
+ * for the antialiased colour mode: surfaces whose fragments are evaluated
+ * packed over the lanes, the window pixels and 64-pixel steps of those,
+ * surfaces swept in 8x8 blocks, blocks swept, fragments written.
  * reset != 0 zeroes the counters. */
 pictura_status pictura_stats_copy(pictura_ctx ctx, uint64_t* out, int32_t n, int32_t reset);
 
 #define PICTURA_DEVERR_RING_WAIT 1u /* a raster record reserved in a view's record ring was never published */
+#define PICTURA_DEVERR_TILE 2u      /* a view tile wider than its mode admits reached a kernel (not drawn) */
 /* Device-side errors the render kernels found (the kernels cannot return a
  * status): *out receives the OR of the PICTURA_DEVERR_* bits set by every
  * render call on this context since it was created or last reset; 0 means

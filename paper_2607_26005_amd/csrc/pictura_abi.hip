@@ -461,6 +461,14 @@ static pictura_status render_rgb(pictura_ctx c, const pictura_agents* ag, const 
     P.out_rgb = out_rgb;
     P.rfar = 1.0f / P.farp;
     P.aa = aa ? 1 : 0;
+    if (aa && P.tile_w > kAaTileW) {
+        // the edge buffer shares the framebuffer's LDS: tiles of at most 32 columns
+        P.tile_w = kAaTileW;
+        P.tiles_x = (P.W + kAaTileW - 1) / kAaTileW;
+        P.num_blocks = P.num_views * P.tiles_x * P.tiles_y;
+        if (P.num_blocks > 0x7FFFFFFFll) return fail(c, PICTURA_ERANGE, "render_rgb: too many view tiles in one call");
+        P.div_tiles = make_div31((uint32_t)(P.tiles_x * P.tiles_y));
+    }
     hipError_t e = launch_render(P, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(c, e, "render_rgb launch");
     return PICTURA_OK;

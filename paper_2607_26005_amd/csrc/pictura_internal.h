@@ -8,7 +8,7 @@
 namespace pictura {
 
 constexpr int kBlock = 256;          // threads per workgroup of the binning kernels
-constexpr int kNumStats = 24;        // optional work counters of the render kernel
+constexpr int kNumStats = 30;        // optional work counters of the render kernel
 
 // Grid of one world.  Cells are numbered row-major from cell_base.
 struct WorldGrid {
@@ -106,6 +106,10 @@ struct RenderParams {
 
 // Device error bits (pictura_device_errors)
 constexpr uint32_t kDevErrRingWait = 1u;   // a raster record reserved in the ring was never published
+constexpr uint32_t kDevErrTile = 2u;       // a view tile wider than its mode's LDS layout admits (not drawn)
+// Antialiased colour: view tiles are at most this many columns wide, so the
+// edge buffer fits in the framebuffer words such a tile leaves unused.
+constexpr int kAaTileW = 32;
 
 struct AgentStepParams {
     float* x; float* y; float* psi; float* speed; float* cos_h; float* sin_h;

@@ -132,9 +132,10 @@ constexpr uint32_t kRecReady = 0x5EC0DE01u;   // differs from the clear key the 
 enum Stat {
     kStTiles = 0, kStCellsRect, kStCellsPre, kStCellsVis, kStCand, kStBoxesVis, kStBoxTris, kStSurv,
     kStExact, kStClipped, kStRasterTris, kStLaneTris, kStLanePx, kStRecTris, kStRecWide, kStBlocksTested,
-    kStBlocksPassed, kStChunks, kCycPrologue, kCycSource, kCycFirst, kCycExact, kCycRecords, kCycWriteout
+    kStBlocksPassed, kStChunks, kCycPrologue, kCycSource, kCycFirst, kCycExact, kCycRecords, kCycWriteout,
+    kStAaPacked, kStAaPackedPx, kStAaPackedSteps, kStAaSwept, kStAaBlocks, kStAaFrags
 };
-static_assert(kCycWriteout + 1 == kNumStats, "stat count");
+static_assert(kStAaFrags + 1 == kNumStats, "stat count");
 
 // Optional work counters (P.stats non-null): LDS per block, flushed once.
 #define STAT(k, n) do { if (P.stats) atomicAdd(&S.stat[(k)], (uint32_t)(n)); } while (0)
@@ -417,7 +418,7 @@ __device__ __forceinline__ bool outside_tile(const RenderParams& P, const Tile& 
 
 // Can a box of projected x in [xmn, xmx], y in [ymn, ymx] (approximate
 // projections whose magnitude is at most mag) hold a pixel centre of the
-// tile (with antialiasing: within one pixel of the tile)?  The margin covers
+// tile (with antialiasing: come within half a pixel of one)?  The margin covers
 // half a subpixel of snapping plus the error of the hardware reciprocal and of
 // the fp32 arithmetic.
 __device__ __forceinline__ bool box_has_centre(const RenderParams& P, const Tile& T, float xmn, float xmx, float ymn,
@@ -598,6 +599,8 @@ __device__ __forceinline__ void raster_packed(const RenderParams& P, Shared& S, 
     const uint32_t n = readlane(incl, 63), pre = incl - npx;
     const uint32_t geo = (uint32_t)(i0 - T.x0) | (uint32_t)(j0 - T.y0) << 8 | (uint32_t)w << 16 | cls << 24;
     const float rw = __builtin_amdgcn_rcpf((float)w);   // row = floor((p + 0.5) / w) for p < 2^12
+    STAT1(kStAaPackedPx, n);
+    STAT1(kStAaPackedSteps, (n + 63u) >> 6);
     uint32_t carry = 0;
     uint32_t* mark = L.u.cells.start;
     for (uint32_t s0 = 0; s0 < n; s0 += 64) {
@@ -880,9 +883,9 @@ __device__ __forceinline__ uint32_t aa_fragment(const RenderParams& P, bool q4, 
 // 64 lanes (as the packed raster does).  With spans below 2^14 subpixels the
 // edge function at any window pixel is below 2^30 in magnitude, so it is an
 // int32 value plus int32 steps from the window's first pixel.
-constexpr int kAaSmall = 64;   // most window pixels of a packed piece
+constexpr int kAaSmall = 128;   // most window pixels of a packed piece
 
-__device__ __forceinline__ void aa_packed(const RenderParams& P, WaveLds& L, uint32_t* fbo, const Tile& T, bool on,
+__device__ __forceinline__ void aa_packed(const RenderParams& P, Shared& S, WaveLds& L, uint32_t* fbo, const Tile& T, bool on,
                                           bool q4, bool any4, int i0, int j0, int w, int npx_, const int* e,
                                           const int* sa, const int* sb, const float* r, float pa, float pb, float pc,
                                           uint32_t cls)
@@ -893,6 +896,8 @@ __device__ __forceinline__ void aa_packed(const RenderParams& P, WaveLds& L, uin
     const uint32_t n = readlane(incl, 63), pre = incl - npx;
     const uint32_t geo = (uint32_t)i0 | (q4 ? 128u : 0u) | (uint32_t)j0 << 8 | (uint32_t)w << 16 | cls << 24;
     const float rw = __builtin_amdgcn_rcpf((float)w);   // row = floor((p + 0.5) / w) for p < 2^12
+    STAT1(kStAaPackedPx, n);
+    STAT1(kStAaPackedSteps, (n + 63u) >> 6);
     uint32_t carry = 0;
     uint32_t* mark = L.u.cells.start;
     for (uint32_t s0 = 0; s0 < n; s0 += 64) {
@@ -927,13 +932,25 @@ __device__ __forceinline__ void aa_packed(const RenderParams& P, WaveLds& L, uin
                                        __uint_as_float(bperm(t, __float_as_uint(pc))), g >> 24);
         // p in range keeps the address inside the window, hence the tile
         const bool inr = (slot < n) & (p >= 0) & (p < tn);
-        atomicMin(&fbo[inr ? y * 64 + x : lane], inr ? f : 0xFFFFFFFFu);
+        STAT(kStAaFrags, inr && f != 0xFFFFFFFFu ? 1 : 0);
+        atomicMin(&fbo[inr ? y * kAaTileW + x : lane], inr ? f : 0xFFFFFFFFu);
         __builtin_amdgcn_wave_barrier();
     }
 }
 
-// Window of a surface: the tile pixels whose centre lies within one pixel of
-// its snapped bounding box, 256 i + 128 in [minX - 256, maxX + 256].
+// Window of a surface: the tile pixels whose centre lies within half a pixel
+// of its snapped bounding box, 256 i + 128 in [minX - 128, maxX + 128].  The
+// rule considers centres within one pixel, but one more than half a pixel
+// beyond the box (say left of the leftmost vertex v) takes no fragment: the
+// two edges at v leave from v rightwards, at angles phi_1 < phi_2 within
+// [-pi/2, pi/2] of the x axis; with d_k the centre's inside distance to edge
+// k, d_1 + d_2 = 2 sin(theta/2) (dy sin psi - g cos psi) for the centre at
+// (-g, dy) from v, psi the bisector's angle and theta = phi_2 - phi_1, and
+// d_1 + d_2 > 0 together with d_2 > -1/2 would need g cos(theta/2) <
+// sin(psi) / 2 <= cos(theta/2) / 2 (as phi_2 <= pi/2), which g > 1/2 rules
+// out (likewise d_1 > -1/2 for psi < 0).  So c_1 + c_2 <= 1 and the sum of
+// all coverages is at most 2 (a triangle) or 3 (a 4-gon): a = 0, and the
+// fp32 rounding (below 1e-6) keeps rint(255 a) at 0.
 // Surfaces whose window has at most kAaSmall pixels and whose box spans below
 // 2^14 subpixels take the packed path; the others are swept by the whole wave
 // one at a time in 8x8 blocks (lane = pixel), E_k evaluated in fp64 from its
@@ -945,7 +962,7 @@ __device__ __forceinline__ void aa_packed(const RenderParams& P, WaveLds& L, uin
 // triangle (a, b, c) in either orientation, or with q4 the 4-gon (a, b, c, d)
 // in positive orientation; a triangle's fourth edge is a constant c_3 = 1
 // that its coverage does not use.
-__device__ void aa_pieces(const RenderParams& P, WaveLds& L, uint32_t* fbo, const Tile& T, bool ok, bool q4, int ax,
+__device__ void aa_pieces(const RenderParams& P, Shared& S, WaveLds& L, uint32_t* fbo, const Tile& T, bool ok, bool q4, int ax,
                           int ay, int bx, int by, int cx, int cy, int dx4, int dy4, float pa, float pb, float pc,
                           uint32_t cls)
 {
@@ -973,8 +990,8 @@ __device__ void aa_pieces(const RenderParams& P, WaveLds& L, uint32_t* fbo, cons
         }
         const int minX = min(min(vx[0], vx[1]), min(vx[2], vx[3])), maxX = max(max(vx[0], vx[1]), max(vx[2], vx[3]));
         const int minY = min(min(vy[0], vy[1]), min(vy[2], vy[3])), maxY = max(max(vy[0], vy[1]), max(vy[2], vy[3]));
-        i0 = max((minX - 384 + 255) >> 8, T.x0) - T.x0; i1 = min((maxX + 128) >> 8, T.x0 + T.w - 1) - T.x0;
-        j0 = max((minY - 384 + 255) >> 8, T.y0) - T.y0; j1 = min((maxY + 128) >> 8, T.y0 + T.h - 1) - T.y0;
+        i0 = max((minX - 1) >> 8, T.x0) - T.x0; i1 = min(maxX >> 8, T.x0 + T.w - 1) - T.x0;
+        j0 = max((minY - 1) >> 8, T.y0) - T.y0; j1 = min(maxY >> 8, T.y0 + T.h - 1) - T.y0;
         ok = ok && i0 <= i1 && j0 <= j1;
         small = ok && (maxX - minX) < 16384 && (maxY - minY) < 16384 && (i1 - i0 + 1) * (j1 - j0 + 1) <= kAaSmall;
         // edge functions at the window's first pixel (small) or at the tile's
@@ -992,11 +1009,13 @@ __device__ void aa_pieces(const RenderParams& P, WaveLds& L, uint32_t* fbo, cons
         }
     }
     const bool any4 = __ballot(ok && q4) != 0;
+    STAT(kStAaPacked, small ? 1 : 0);
+    STAT(kStAaSwept, ok && !small ? 1 : 0);
     if (__ballot(small) != 0) {
         const int e[4] = {(int)e0[0], (int)e0[1], (int)e0[2], (int)e0[3]};
         const int sa[4] = {-256 * dys[0], -256 * dys[1], -256 * dys[2], -256 * dys[3]};
         const int sb[4] = {256 * dxs[0], 256 * dxs[1], 256 * dxs[2], 256 * dxs[3]};
-        aa_packed(P, L, fbo, T, small, q4, any4, i0, j0, i1 - i0 + 1, (i1 - i0 + 1) * (j1 - j0 + 1), e, sa, sb, rden,
+        aa_packed(P, S, L, fbo, T, small, q4, any4, i0, j0, i1 - i0 + 1, (i1 - i0 + 1) * (j1 - j0 + 1), e, sa, sb, rden,
                   pa, pb, pc, cls);
     }
     uint64_t m = __ballot(ok && !small);
@@ -1041,6 +1060,7 @@ __device__ void aa_pieces(const RenderParams& P, WaveLds& L, uint32_t* fbo, cons
             }
             bm = __ballot(need);
         }
+        STAT1(kStAaBlocks, __popcll(bm));
         while (bm) {
             const int b = __builtin_ctzll(bm);
             bm &= bm - 1;
@@ -1053,7 +1073,8 @@ __device__ void aa_pieces(const RenderParams& P, WaveLds& L, uint32_t* fbo, cons
                                            aa_cover(fma(rsy[3], dj, fma(rsx[3], di, re[3])), rr[3]),
                                            ((float)(T.x0 + i) + 0.5f) - P.cx, ((float)(T.y0 + j) + 0.5f) - P.cy, rpa,
                                            rpb, rpc, rcls);
-            atomicMin(&fbo[j * 64 + i], f);
+            STAT(kStAaFrags, f != 0xFFFFFFFFu ? 1 : 0);
+            atomicMin(&fbo[j * kAaTileW + i], f);
         }
     }
 }
@@ -1201,11 +1222,6 @@ __device__ __forceinline__ void exact_pass(const RenderParams& P, Shared& S, Wav
                 }
             }
         }
-        if constexpr (kAA) {
-            const bool sq = aaq && f == 0;   // the whole surface, with the first piece's plane
-            aa_pieces(P, L, fbo, T, sq || (piece && !aaq), sq, sq ? qx[0] : ax, sq ? qy[0] : ay, sq ? qx[1] : bx,
-                      sq ? qy[1] : by, sq ? qx[2] : cx, sq ? qy[2] : cy, qx[3], qy[3], pa, pb, pc, cls);
-        }
         // edge setup: edges v1->v2, v2->v0, v0->v1 at the tile's pixel (0, 0),
         // in the int32 form (floor(c / 256), -dy, dx) when every value fits
         uint32_t rv[12] = {0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0, 0};
@@ -1305,6 +1321,20 @@ __device__ __forceinline__ void exact_pass(const RenderParams& P, Shared& S, Wav
             }
         }
         TACC(kCycRecords, t_rec);
+    }
+    // R14 fragments after both pieces' keys (the two buffers take minima, so
+    // the order does not matter; here fewer values are live)
+    if constexpr (kAA) {
+#pragma unroll 1
+        for (int f = 0; f < nfan; ++f) {
+            const bool piece = f + 2 < np && (f ? ok1 : ok0);
+            const bool sq = aaq && f == 0;   // the whole surface, with the first piece's plane
+            const int bx = f == 0 ? X1 : X2, by = f == 0 ? Y1 : Y2;
+            const int cx = f == 0 ? X2 : X3, cy = f == 0 ? Y2 : Y3;
+            aa_pieces(P, S, L, fbo, T, sq || (piece && !aaq), sq, sq ? qx[0] : X0, sq ? qy[0] : Y0, sq ? qx[1] : bx,
+                      sq ? qy[1] : by, sq ? qx[2] : cx, sq ? qy[2] : cy, qx[3], qy[3], f ? pa1 : pa0, f ? pb1 : pb0,
+                      f ? pc1 : pc0, cls);
+        }
     }
 }
 
@@ -1535,10 +1565,12 @@ __device__ void draw_box_instances(const RenderParams& P, Shared& S, InstLds& I,
 struct NoInstLds {};
 
 // Colour antialiasing (R14): the edge buffer, the nearest partial-coverage
-// fragment of every pixel.
-struct alignas(16) AaLds {
-    uint32_t fbo[64 * 64];   // tile pixel (i, j) at j * 64 + i; 0xFFFFFFFF none
-};
+// fragment of every pixel, tile pixel (i, j) at j * kAaTileW + i (0xFFFFFFFF
+// none).  A tile at most kAaTileW columns wide fills its framebuffer rows at a
+// pitch of kAaTileW + 4 words; the edge buffer takes the words after them, so
+// this mode needs no LDS beyond the class/depth kernel's.
+constexpr int kAaFboOff = 64 * (kAaTileW + 4);
+static_assert(kAaFboOff + 64 * kAaTileW <= kFbCap, "edge buffer inside the framebuffer array");
 
 // kMode 0: class and depth (and colour without antialiasing); 1: the
 // instance variant; 2: colour with antialiasing.  The variants' LDS admits
@@ -1549,7 +1581,7 @@ struct alignas(16) AaLds {
 // constant null and culling constantly on, so every counting site and the
 // unculled paths fold away (and so does the colour code outside modes 2 and 3).
 template <int kMode, bool kDebug>
-__global__ __launch_bounds__(kThreads, kMode == 1 || kMode == 2 ? 2 : kWavesPerSimd)
+__global__ __launch_bounds__(kThreads, kMode == 1 ? 2 : kMode == 2 ? 4 : kWavesPerSimd)
 void render_views_kernel(const RenderParams P_)
 {
     constexpr bool kInst = kMode == 1, kAA = kMode == 2;
@@ -1560,7 +1592,7 @@ void render_views_kernel(const RenderParams P_)
     }
     if constexpr (kMode == 0 || kMode == 1) P.out_rgb = nullptr;
     __shared__ Shared S;
-    __shared__ typename std::conditional<kInst, InstLds, typename std::conditional<kAA, AaLds, NoInstLds>::type>::type I;
+    __shared__ typename std::conditional<kInst, InstLds, NoInstLds>::type I;
     const int tid = threadIdx.x, lane = lane_id(), wid = tid >> 6;
     WaveLds& L = S.wv[wid];
     TSTART(t_kernel);
@@ -1594,14 +1626,21 @@ void render_views_kernel(const RenderParams P_)
     T.w = min(P.tile_w, P.W - T.x0);
     T.h = min(P.tile_h, P.H - T.y0);
     T.pitch = ((T.w + 31) & ~31) + 4;
+    if constexpr (kAA) {
+        // the host keeps tiles within kAaTileW columns; a wider one is not drawn
+        if (T.w > kAaTileW) {
+            if (threadIdx.x == 0) atomicOr(P.dev_err, kDevErrTile);
+            return;
+        }
+    }
     // culling reaches the pixel centres of the tile, and with antialiasing the
-    // centres within one more pixel, where a surface's edge fragments land
-    constexpr float tpad = kAA ? 1.5f : 0.5f;
+    // centres within half a pixel more, where a surface's edge fragments land
+    constexpr float tpad = kAA ? 1.0f : 0.5f;
     T.kl = ((float)T.x0 - tpad) - P.cx;
     T.kr = ((float)(T.x0 + T.w) + tpad) - P.cx;
     T.kt = P.cy - ((float)T.y0 - tpad);
     T.kb = P.cy - ((float)(T.y0 + T.h) + tpad);
-    T.cm = kAA ? 1.00390625f : 0.00390625f;
+    T.cm = kAA ? 0.50390625f : 0.00390625f;
     const int npx = T.w * T.h;
     static_assert(sizeof(Shared) <= 65536, "LDS");
     const bool cull = P.cull != 0;
@@ -1621,7 +1660,7 @@ void render_views_kernel(const RenderParams P_)
         for (int p = tid; p < 64 * 64; p += kThreads) I.inst[p] = 0xFFFFFFFFu;
     }
     if constexpr (kAA) {
-        for (int p = tid; p < 64 * 64; p += kThreads) I.fbo[p] = 0xFFFFFFFFu;
+        for (int p = tid; p < 64 * kAaTileW; p += kThreads) S.fb[kAaFboOff + p] = 0xFFFFFFFFu;
     }
 
     // world-space frustum planes of the tile: four side planes through the
@@ -1864,7 +1903,7 @@ void render_views_kernel(const RenderParams P_)
             STAT1(kStExact, 1);
             TSTART(t_ex);
             uint32_t* fbo = nullptr;
-            if constexpr (kAA) fbo = I.fbo;
+            if constexpr (kAA) fbo = S.fb + kAaFboOff;
             exact_pass<kAA>(P, S, L, T, cam, live, entry, abase_w, lbase_w, pxl, pyl, loff4, fbo);
             TACC(kCycExact, t_ex);
         }
@@ -2023,7 +2062,7 @@ void render_views_kernel(const RenderParams P_)
             if constexpr (kAA) {
                 // R14: a partial-coverage fragment not behind the centre's surface and
                 // of another shading id blends over it
-                const uint32_t ko = I.fbo[row * 64 + col];
+                const uint32_t ko = S.fb[kAaFboOff + row * kAaTileW + col];
                 if (ko != 0xFFFFFFFFu && (ko >> 16) <= (key >> 16) && ((ko >> 8) & 255u) != (key & 255u)) {
                     uint32_t o3[3];
                     shade_rgb(P, ((ko >> 16) << 16) | ((ko >> 8) & 255u), o3);

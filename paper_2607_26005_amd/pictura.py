@@ -112,7 +112,9 @@ DEVERR_RING_WAIT = 1
 STAT_NAMES = ["view_tiles", "cells_in_rect", "cells_prefiltered", "cells_visible", "cand_tris", "boxes_visible",
               "box_tris", "first_pass_survivors", "exact_batches", "clipped", "raster_tris", "lane_tris",
               "lane_px", "record_tris", "record_tris_fp64", "blocks_tested", "blocks_passed", "first_pass_chunks",
-              "cyc_prologue", "cyc_sources", "cyc_first_pass", "cyc_exact", "cyc_records", "cyc_writeout"]
+              "cyc_prologue", "cyc_sources", "cyc_first_pass", "cyc_exact", "cyc_records", "cyc_writeout",
+              "aa_surfaces_packed", "aa_packed_px", "aa_packed_steps", "aa_surfaces_swept", "aa_blocks_swept",
+              "aa_fragments"]
 
 
 _CTX_DEVICE = {}   # context handle -> HIP device index it was created on

@@ -223,3 +223,56 @@ def test_pair_that_is_not_convex_keeps_per_triangle_fragments():
     apart = _render([[a, c, d], [a, b, c]], [LANE, LANE])
     assert (paired["cls"][0] == LANE).sum() > 0
     assert np.array_equal(paired["rgb"][0], apart["rgb"][0])
+
+
+def _coverage(poly, px, py):
+    """R14 coverage of a positively oriented convex polygon (snapped
+    subpixel vertices) at pixel centres (px, py) in subpixels, in float64."""
+    n = len(poly)
+    s = 0.0
+    for k in range(n):
+        (ax, ay), (bx, by) = poly[k], poly[(k + 1) % n]
+        dx, dy = bx - ax, by - ay
+        e = dx * (py - ay) - dy * (px - ax)
+        s = s + np.clip(e / (256.0 * np.hypot(dx, dy)) + 0.5, 0.0, 1.0)
+    return np.clip(s - (n - 1), 0.0, 1.0)
+
+
+def test_no_fragment_more_than_half_a_pixel_beyond_the_box():
+    # the kernel evaluates R14 only at centres within half a pixel of a
+    # surface's snapped box: farther centres must get a = 0 for every
+    # triangle and convex 4-gon (slivers and sharp corners included)
+    rng = np.random.default_rng(17)
+    checked = 0
+    for it in range(3000):
+        n = 3 if it % 2 else 4
+        scale = [64.0, 400.0, 2000.0][it % 3]
+        if n == 3:
+            pts = rng.integers(-int(scale), int(scale), size=(3, 2)).astype(np.float64)
+            if it % 5 == 0:   # a sliver
+                pts[2] = np.rint(pts[0] + (pts[1] - pts[0]) * rng.uniform(0.2, 0.8)) + rng.integers(-3, 4, size=2)
+        else:
+            ang = np.sort(rng.uniform(0, 2 * np.pi, size=4))
+            rad = rng.uniform(0.2, 1.0, size=2) * scale
+            pts = np.rint(np.stack([rad[0] * np.cos(ang), rad[1] * np.sin(ang)], 1))
+        area2 = sum(pts[k, 0] * pts[(k + 1) % n, 1] - pts[(k + 1) % n, 0] * pts[k, 1] for k in range(n))
+        if area2 == 0:
+            continue
+        if area2 < 0:
+            pts = pts[::-1]
+        if n == 4:   # strictly convex only
+            cr = [(pts[(k + 1) % 4, 0] - pts[k, 0]) * (pts[(k + 2) % 4, 1] - pts[(k + 1) % 4, 1]) -
+                  (pts[(k + 1) % 4, 1] - pts[k, 1]) * (pts[(k + 2) % 4, 0] - pts[(k + 1) % 4, 0]) for k in range(4)]
+            if min(cr) <= 0:
+                continue
+        lo, hi = pts.min(0), pts.max(0)
+        # centres in the band (0.5, 1] px beyond each side, along the whole box
+        i = np.arange(np.floor((lo[0] - 512) / 256), np.ceil((hi[0] + 512) / 256) + 1)
+        j = np.arange(np.floor((lo[1] - 512) / 256), np.ceil((hi[1] + 512) / 256) + 1)
+        cx, cy = np.meshgrid(256 * i + 128, 256 * j + 128)
+        band = (((cx < lo[0] - 128) | (cx > hi[0] + 128) | (cy < lo[1] - 128) | (cy > hi[1] + 128)) &
+                (cx >= lo[0] - 256) & (cx <= hi[0] + 256) & (cy >= lo[1] - 256) & (cy <= hi[1] + 256))
+        a = _coverage([tuple(p) for p in pts], cx[band], cy[band])
+        assert (np.rint(255.0 * a) == 0).all(), (pts, a.max())
+        checked += int(band.sum())
+    assert checked > 20000
