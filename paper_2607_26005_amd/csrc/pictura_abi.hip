@@ -446,6 +446,20 @@ pictura_status pictura_render_views(pictura_ctx c, const pictura_agents* ag, con
     return PICTURA_OK;
 }
 
+// The antialiased and instance modes keep a per-pixel side buffer in the
+// framebuffer's LDS: their tiles are at most kSideTileW columns wide.  False
+// if the launch would then hold too many view tiles.
+static bool narrow_tiles(RenderParams& P)
+{
+    if (P.tile_w <= kSideTileW) return true;
+    P.tile_w = kSideTileW;
+    P.tiles_x = (P.W + kSideTileW - 1) / kSideTileW;
+    P.num_blocks = P.num_views * P.tiles_x * P.tiles_y;
+    if (P.num_blocks > 0x7FFFFFFFll) return false;
+    P.div_tiles = make_div31((uint32_t)(P.tiles_x * P.tiles_y));
+    return true;
+}
+
 static pictura_status render_rgb(pictura_ctx c, const pictura_agents* ag, const pictura_rig* rig, uint8_t* out_cls,
                                  float* out_depth, uint8_t* out_rgb, void* stream, bool aa)
 {
@@ -461,14 +475,7 @@ static pictura_status render_rgb(pictura_ctx c, const pictura_agents* ag, const 
     P.out_rgb = out_rgb;
     P.rfar = 1.0f / P.farp;
     P.aa = aa ? 1 : 0;
-    if (aa && P.tile_w > kAaTileW) {
-        // the edge buffer shares the framebuffer's LDS: tiles of at most 32 columns
-        P.tile_w = kAaTileW;
-        P.tiles_x = (P.W + kAaTileW - 1) / kAaTileW;
-        P.num_blocks = P.num_views * P.tiles_x * P.tiles_y;
-        if (P.num_blocks > 0x7FFFFFFFll) return fail(c, PICTURA_ERANGE, "render_rgb: too many view tiles in one call");
-        P.div_tiles = make_div31((uint32_t)(P.tiles_x * P.tiles_y));
-    }
+    if (aa && !narrow_tiles(P)) return fail(c, PICTURA_ERANGE, "render_rgb: too many view tiles in one call");
     hipError_t e = launch_render(P, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(c, e, "render_rgb launch");
     return PICTURA_OK;
@@ -500,8 +507,8 @@ pictura_status pictura_render_instances(pictura_ctx c, const pictura_agents* ag,
     if (st != PICTURA_OK || empty) return st;
     P.out_inst = out_inst;
     P.out_counts = out_counts;
-    const size_t nbytes = (size_t)P.num_views * (size_t)P.A * 2u * sizeof(uint32_t);
-    hipError_t e = hipMemsetAsync(out_counts, 0, nbytes, (hipStream_t)stream);
+    if (!narrow_tiles(P)) return fail(c, PICTURA_ERANGE, "render_instances: too many view tiles in one call");
+    hipError_t e = launch_fill_u32(out_counts, (size_t)P.num_views * (size_t)P.A * 2u, 0u, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(c, e, "render_instances clear");
     e = launch_render(P, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(c, e, "render_instances launch");

@@ -107,9 +107,10 @@ struct RenderParams {
 // Device error bits (pictura_device_errors)
 constexpr uint32_t kDevErrRingWait = 1u;   // a raster record reserved in the ring was never published
 constexpr uint32_t kDevErrTile = 2u;       // a view tile wider than its mode's LDS layout admits (not drawn)
-// Antialiased colour: view tiles are at most this many columns wide, so the
-// edge buffer fits in the framebuffer words such a tile leaves unused.
-constexpr int kAaTileW = 32;
+// Antialiased colour and instance visibility: view tiles are at most this
+// many columns wide, so the per-pixel side buffer of these modes (fragments,
+// owners) fits in the framebuffer words such a tile leaves unused.
+constexpr int kSideTileW = 32;
 
 struct AgentStepParams {
     float* x; float* y; float* psi; float* speed; float* cos_h; float* sin_h;
@@ -161,5 +162,9 @@ constexpr int kNoAllocMaxDevices = 64;
 hipError_t noalloc_scratch_init(int device);
 void* noalloc_scratch(int device);   // null before noalloc_scratch_init(device)
 hipError_t launch_rcp_check_noalloc(uint32_t lo_bits, uint32_t n, unsigned long long* counter, hipStream_t s);
+
+// Fill n 32-bit words at p with `value` on stream s (a kernel, so a caller
+// may capture it in a graph).
+hipError_t launch_fill_u32(uint32_t* p, size_t n, uint32_t value, hipStream_t s);
 
 }  // namespace pictura

@@ -115,6 +115,7 @@ struct alignas(16) WaveLds {
             uint32_t count[64];
         } cells;
         uint32_t agents[64];
+        uint32_t bits[128];   // instance mode, after the static pass: coverage of one box, 2 words per tile row
     } u;
     uint32_t q[kQueue];
 };
@@ -933,7 +934,7 @@ __device__ __forceinline__ void aa_packed(const RenderParams& P, Shared& S, Wave
         // p in range keeps the address inside the window, hence the tile
         const bool inr = (slot < n) & (p >= 0) & (p < tn);
         STAT(kStAaFrags, inr && f != 0xFFFFFFFFu ? 1 : 0);
-        atomicMin(&fbo[inr ? y * kAaTileW + x : lane], inr ? f : 0xFFFFFFFFu);
+        atomicMin(&fbo[inr ? y * kSideTileW + x : lane], inr ? f : 0xFFFFFFFFu);
         __builtin_amdgcn_wave_barrier();
     }
 }
@@ -1074,7 +1075,7 @@ __device__ void aa_pieces(const RenderParams& P, Shared& S, WaveLds& L, uint32_t
                                            ((float)(T.x0 + i) + 0.5f) - P.cx, ((float)(T.y0 + j) + 0.5f) - P.cy, rpa,
                                            rpb, rpc, rcls);
             STAT(kStAaFrags, f != 0xFFFFFFFFu ? 1 : 0);
-            atomicMin(&fbo[j * kAaTileW + i], f);
+            atomicMin(&fbo[j * kSideTileW + i], f);
         }
     }
 }
@@ -1455,21 +1456,17 @@ __device__ __forceinline__ float decode_depth(const RenderParams& P, uint32_t ke
 // visible surface, and how many pixels each box covers when drawn alone
 // ---------------------------------------------------------------------------
 
-struct alignas(16) InstLds {
-    uint32_t inst[64 * 64];            // tile pixel (i, j) at j * 64 + i: lowest owning agent, 0xFFFFFFFF none
-    uint32_t bits[kViewWaves][128];    // per wave: coverage of the box being drawn, 2 words per tile row
-};
 
 // Draw agent `agent`'s box (world index h) alone with the rules R2-R7 and the
 // same arithmetic as the raster: every covered pixel sets its coverage bit, and
 // a pixel whose key equals the final key of the view keeps the lowest such
 // agent.  Adds the number of covered pixels to the agent's footprint.  One
 // wave; simple lane-per-pixel sweeps with exact int64 edge values.
-__device__ void draw_box_instances(const RenderParams& P, Shared& S, InstLds& I, const Tile& T, const Cam& cam,
+__device__ void draw_box_instances(const RenderParams& P, Shared& S, uint32_t* inst, const Tile& T, const Cam& cam,
                                    int64_t h, uint32_t agent, int64_t v)
 {
     const int lane = lane_id(), wid = threadIdx.x >> 6;
-    uint32_t* bits = I.bits[wid];
+    uint32_t* bits = S.wv[wid].u.bits;
     bits[lane] = 0u;
     bits[lane + 64] = 0u;
     __builtin_amdgcn_wave_barrier();
@@ -1549,7 +1546,7 @@ __device__ void draw_box_instances(const RenderParams& P, Shared& S, InstLds& I,
                     const uint32_t key = pixel_key(P, pxf, pyf, rpa, rpb, rpc, rcls);
                     if (cov && key != 0xFFFFFFFFu) {
                         atomicOr(&bits[2 * j + (i >> 5)], 1u << (i & 31));
-                        if (key == S.fb[j * T.pitch + i]) atomicMin(&I.inst[j * 64 + i], agent);
+                        if (key == S.fb[j * T.pitch + i]) atomicMin(&inst[j * kSideTileW + i], agent);
                     }
                 }
             }
@@ -1562,26 +1559,23 @@ __device__ void draw_box_instances(const RenderParams& P, Shared& S, InstLds& I,
     __builtin_amdgcn_wave_barrier();
 }
 
-struct NoInstLds {};
+// Side buffer of the antialiased and instance modes, tile pixel (i, j) at
+// j * kSideTileW + i: the edge buffer of R14 (the nearest partial-coverage
+// fragment, 0xFFFFFFFF none) or the lowest owning agent (0xFFFFFFFF none).  A
+// tile at most kSideTileW columns wide fills its framebuffer rows at a pitch
+// of kSideTileW + 4 words; the side buffer takes the words after them, so
+// these modes need no LDS beyond the class/depth kernel's.
+constexpr int kSideOff = 64 * (kSideTileW + 4);
+static_assert(kSideOff + 64 * kSideTileW <= kFbCap, "side buffer inside the framebuffer array");
 
-// Colour antialiasing (R14): the edge buffer, the nearest partial-coverage
-// fragment of every pixel, tile pixel (i, j) at j * kAaTileW + i (0xFFFFFFFF
-// none).  A tile at most kAaTileW columns wide fills its framebuffer rows at a
-// pitch of kAaTileW + 4 words; the edge buffer takes the words after them, so
-// this mode needs no LDS beyond the class/depth kernel's.
-constexpr int kAaFboOff = 64 * (kAaTileW + 4);
-static_assert(kAaFboOff + 64 * kAaTileW <= kFbCap, "edge buffer inside the framebuffer array");
-
-// kMode 0: class and depth (and colour without antialiasing); 1: the
-// instance variant; 2: colour with antialiasing.  The variants' LDS admits
-// two waves per SIMD, so they may use twice the registers.
+// Every mode runs four waves per SIMD (the LDS of eight view tiles per CU).
 // kMode: 0 class and depth, 1 with instance visibility, 2 with antialiased
 // colour, 3 with colour.  kDebug: the work counters and the option to turn
 // culling off are read at run time; otherwise the counter pointer is a
 // constant null and culling constantly on, so every counting site and the
 // unculled paths fold away (and so does the colour code outside modes 2 and 3).
 template <int kMode, bool kDebug>
-__global__ __launch_bounds__(kThreads, kMode == 1 ? 2 : kMode == 2 ? 4 : kWavesPerSimd)
+__global__ __launch_bounds__(kThreads, kWavesPerSimd)
 void render_views_kernel(const RenderParams P_)
 {
     constexpr bool kInst = kMode == 1, kAA = kMode == 2;
@@ -1592,7 +1586,6 @@ void render_views_kernel(const RenderParams P_)
     }
     if constexpr (kMode == 0 || kMode == 1) P.out_rgb = nullptr;
     __shared__ Shared S;
-    __shared__ typename std::conditional<kInst, InstLds, NoInstLds>::type I;
     const int tid = threadIdx.x, lane = lane_id(), wid = tid >> 6;
     WaveLds& L = S.wv[wid];
     TSTART(t_kernel);
@@ -1626,9 +1619,9 @@ void render_views_kernel(const RenderParams P_)
     T.w = min(P.tile_w, P.W - T.x0);
     T.h = min(P.tile_h, P.H - T.y0);
     T.pitch = ((T.w + 31) & ~31) + 4;
-    if constexpr (kAA) {
-        // the host keeps tiles within kAaTileW columns; a wider one is not drawn
-        if (T.w > kAaTileW) {
+    if constexpr (kAA || kInst) {
+        // the host keeps tiles within kSideTileW columns; a wider one is not drawn
+        if (T.w > kSideTileW) {
             if (threadIdx.x == 0) atomicOr(P.dev_err, kDevErrTile);
             return;
         }
@@ -1656,11 +1649,8 @@ void render_views_kernel(const RenderParams P_)
     const int loff4 = ((lane >> 3) * T.pitch + (lane & 7)) * 4;
     if (P.stats && tid < kNumStats) S.stat[tid] = 0;
     if (tid < 4) S.ctl[tid] = 0;
-    if constexpr (kInst) {
-        for (int p = tid; p < 64 * 64; p += kThreads) I.inst[p] = 0xFFFFFFFFu;
-    }
-    if constexpr (kAA) {
-        for (int p = tid; p < 64 * kAaTileW; p += kThreads) S.fb[kAaFboOff + p] = 0xFFFFFFFFu;
+    if constexpr (kAA || kInst) {
+        for (int p = tid; p < 64 * kSideTileW; p += kThreads) S.fb[kSideOff + p] = 0xFFFFFFFFu;
     }
 
     // world-space frustum planes of the tile: four side planes through the
@@ -1903,7 +1893,7 @@ void render_views_kernel(const RenderParams P_)
             STAT1(kStExact, 1);
             TSTART(t_ex);
             uint32_t* fbo = nullptr;
-            if constexpr (kAA) fbo = S.fb + kAaFboOff;
+            if constexpr (kAA) fbo = S.fb + kSideOff;
             exact_pass<kAA>(P, S, L, T, cam, live, entry, abase_w, lbase_w, pxl, pyl, loff4, fbo);
             TACC(kCycExact, t_ex);
         }
@@ -1981,7 +1971,7 @@ void render_views_kernel(const RenderParams P_)
                 const int l = __builtin_ctzll(m);
                 m &= m - 1;
                 const uint32_t agent = readlane((uint32_t)ai, l);
-                draw_box_instances(P, S, I, T, cam, abase_w + agent, agent, v);
+                draw_box_instances(P, S, S.fb + kSideOff, T, cam, abase_w + agent, agent, v);
             }
         }
         __syncthreads();
@@ -1989,9 +1979,17 @@ void render_views_kernel(const RenderParams P_)
         const int64_t view_px = (int64_t)P.W * P.H;
         for (int p = tid; p < npx; p += kThreads) {
             const int row = p / T.w, col = p % T.w;
-            const uint32_t id = I.inst[row * 64 + col];
+            const uint32_t id = S.fb[kSideOff + row * kSideTileW + col];
             P.out_inst[v * view_px + (int64_t)(T.y0 + row) * P.W + T.x0 + col] = (int32_t)id;
-            if (id != 0xFFFFFFFFu) atomicAdd(&P.out_counts[2 * (v * P.A + id) + 1], 1u);
+            // one atomic per distinct owner among the wave's pixels
+            uint64_t m = __ballot(id != 0xFFFFFFFFu);
+            while (m) {
+                const uint32_t o = readlane(id, __builtin_ctzll(m));
+                const uint64_t same = __ballot(id == o);
+                if (lane == (int)__builtin_ctzll(same))
+                    atomicAdd(&P.out_counts[2 * (v * P.A + o) + 1], (uint32_t)__popcll(same));
+                m &= ~same;
+            }
         }
     }
 
@@ -2062,7 +2060,7 @@ void render_views_kernel(const RenderParams P_)
             if constexpr (kAA) {
                 // R14: a partial-coverage fragment not behind the centre's surface and
                 // of another shading id blends over it
-                const uint32_t ko = S.fb[kAaFboOff + row * kAaTileW + col];
+                const uint32_t ko = S.fb[kSideOff + row * kSideTileW + col];
                 if (ko != 0xFFFFFFFFu && (ko >> 16) <= (key >> 16) && ((ko >> 8) & 255u) != (key & 255u)) {
                     uint32_t o3[3];
                     shade_rgb(P, ((ko >> 16) << 16) | ((ko >> 8) & 255u), o3);
@@ -2154,6 +2152,20 @@ void* noalloc_scratch(int device)
     if (device < 0 || device >= kNoAllocMaxDevices) return nullptr;
     std::lock_guard<std::mutex> lock(g_scratch_mu);
     return g_scratch_ptr[device];
+}
+
+__global__ void fill_u32_kernel(uint32_t* p, size_t n, uint32_t value)
+{
+    const size_t stride = (size_t)gridDim.x * blockDim.x;
+    for (size_t i = (size_t)blockIdx.x * blockDim.x + threadIdx.x; i < n; i += stride) p[i] = value;
+}
+
+hipError_t launch_fill_u32(uint32_t* p, size_t n, uint32_t value, hipStream_t s)
+{
+    if (n == 0) return hipSuccess;
+    const size_t blocks = (n + 255) / 256;
+    hipLaunchKernelGGL(fill_u32_kernel, dim3((unsigned)(blocks < 4096 ? blocks : 4096)), dim3(256), 0, s, p, n, value);
+    return hipGetLastError();
 }
 
 __global__ void clear_words_kernel(unsigned long long* p, int n)
