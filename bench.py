@@ -37,19 +37,21 @@ HBM_PEAK_GBS = 8000.0   # MI355X HBM3E peak
 
 # HBM bytes per launch of render_views_kernel on the headline workload, from
 # rocprofv3 FETCH_SIZE and WRITE_SIZE runs (one counter per run), each scaled
-# by what the counter reads for a plain 1 GiB device copy (FETCH_SIZE x1.99994,
+# by what the counter reads for a plain 1 GiB device copy (FETCH_SIZE x1.99995,
 # WRITE_SIZE x1.0).  The figures hold only for the kernel sources they were
 # measured on (and the workload generator); when the fingerprint differs,
 # `traffic` is reported as null.
 TRAFFIC = {
     "config": 4,
-    "sources_sha256": "18cfa04c8b617f6de132ed6f378130d5fb7f43cdc50d6814d021bdda7c6d3637",
-    "fetch_bytes": 1.4811e9,
+    "sources_sha256": "cabf5926ebd65d0d8bd3657d10a10fd5054c0ccecd48505c2b5c8a42461b5079",
+    "fetch_bytes": 1.1539e9,
     "write_bytes": 5368709120,
 }
 TRAFFIC_SOURCES = ["paper_2607_26005_amd/csrc/pictura_render.hip",
                    "paper_2607_26005_amd/csrc/pictura_internal.h",
                    "paper_2607_26005_amd/csrc/pictura_device.h",
+                   "paper_2607_26005_amd/csrc/pictura_abi.hip",      # primitive layout in HBM
+                   "paper_2607_26005_amd/csrc/pictura_binner.hip",   # cell order of the primitives
                    "paper_2607_26005_amd/build.py",
                    "paper_2607_26005_amd/scenegen.py"]   # the workload (scene, cell size) too
 
@@ -78,6 +80,9 @@ def parse():
     ap.add_argument("--encoder", action="store_true",
                     help="also run the image encoder on each step's views (in-loop coupling)")
     ap.add_argument("--cpu-seconds", type=float, default=15.0)
+    ap.add_argument("--stats", action="store_true",
+                    help="after the timed region, one more launch with the work counters on (debug instantiation); "
+                         "prints them per view tile")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="run only a plain device copy of known size (counter calibration)")
     args = ap.parse_args()
@@ -248,6 +253,15 @@ def main():
     ev_p1.record(stream)
     torch.cuda.synchronize()
     store_gbs = probe.numel() * n_probe / (ev_p0.elapsed_time(ev_p1) * 1e-3) / 1e9
+    if args.stats:
+        r.set_option(pictura.OPT_STATS, 1)
+        render()
+        torch.cuda.synchronize()
+        st = pictura.pictura_stats_copy(r.ctx, reset=True)
+        r.set_option(pictura.OPT_STATS, 0)
+        nt = max(st["view_tiles"], 1)
+        print("# work per view tile (one more launch, debug instantiation): " +
+              ", ".join(f"{k}={v / nt:.1f}" for k, v in st.items() if v), file=sys.stderr, flush=True)
     dev_err = r.device_errors()
     print(f"# store probe: {probe.numel() / 1e9:.2f} GB per launch, {store_gbs:.0f} GB/s; device errors {dev_err:#x}",
           file=sys.stderr, flush=True)
@@ -263,7 +277,8 @@ def main():
     r.close()
 
     traffic = None
-    if args.config == TRAFFIC["config"] and args.worlds is None and kernel_fingerprint() == TRAFFIC["sources_sha256"]:
+    if (args.config == TRAFFIC["config"] and args.worlds is None and not args.rgb and not args.instances
+            and not args.encoder and kernel_fingerprint() == TRAFFIC["sources_sha256"]):
         traffic = TRAFFIC["fetch_bytes"] + TRAFFIC["write_bytes"]
 
     cpu = None

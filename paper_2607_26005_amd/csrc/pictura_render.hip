@@ -600,8 +600,6 @@ __device__ __forceinline__ void raster_packed(const RenderParams& P, Shared& S, 
     const uint32_t n = readlane(incl, 63), pre = incl - npx;
     const uint32_t geo = (uint32_t)(i0 - T.x0) | (uint32_t)(j0 - T.y0) << 8 | (uint32_t)w << 16 | cls << 24;
     const float rw = __builtin_amdgcn_rcpf((float)w);   // row = floor((p + 0.5) / w) for p < 2^12
-    STAT1(kStAaPackedPx, n);
-    STAT1(kStAaPackedSteps, (n + 63u) >> 6);
     uint32_t carry = 0;
     uint32_t* mark = L.u.cells.start;
     for (uint32_t s0 = 0; s0 < n; s0 += 64) {
