@@ -318,6 +318,9 @@ def main():
             "frac": achieved / HBM_PEAK_GBS,
             "algorithmic_bytes_per_launch": out_bytes,
             "traffic": traffic,
+            "traffic_source": ("rocprofv3 FETCH_SIZE + WRITE_SIZE per launch, copy-calibrated, profiled on these kernel "
+                               "sources (profiles/render_views_kernel_throughput_headline_64x64.md)"
+                               if traffic is not None else None),
             "measured_store_gbs": store_gbs,
             "frac_of_measured_store": achieved / store_gbs,
         },
@@ -328,10 +331,10 @@ def main():
         line["config"]["step"] += " with the shaded colour image (planar RGB)"
         if args.aa:
             line["config"]["step"] += ", antialiased (analytic coverage, one sample per pixel)"
-        line["roofline"]["traffic"] = None
+        line["roofline"]["traffic"] = line["roofline"]["traffic_source"] = None
     if out_inst is not None:
         line["config"]["step"] += " with instance visibility (owner per pixel, footprint and visible pixels per agent)"
-        line["roofline"]["traffic"] = None
+        line["roofline"]["traffic"] = line["roofline"]["traffic_source"] = None
     if enc is not None:
         line["config"]["step"] += " + image encoder (5 conv layers, 16 queries x 1 cross-attention per camera, fp32)"
         line["encoder_ms"] = ms_step - avg_render_ms
