@@ -446,9 +446,9 @@ pictura_status pictura_render_views(pictura_ctx c, const pictura_agents* ag, con
     return PICTURA_OK;
 }
 
-// The antialiased and instance modes keep a per-pixel side buffer in the
-// framebuffer's LDS: their tiles are at most kSideTileW columns wide.  False
-// if the launch would then hold too many view tiles.
+// The antialiased mode keeps a per-pixel side buffer in the framebuffer's
+// LDS: its tiles are at most kSideTileW columns wide.  False if the launch
+// would then hold too many view tiles.
 static bool narrow_tiles(RenderParams& P)
 {
     if (P.tile_w <= kSideTileW) return true;
@@ -507,7 +507,6 @@ pictura_status pictura_render_instances(pictura_ctx c, const pictura_agents* ag,
     if (st != PICTURA_OK || empty) return st;
     P.out_inst = out_inst;
     P.out_counts = out_counts;
-    if (!narrow_tiles(P)) return fail(c, PICTURA_ERANGE, "render_instances: too many view tiles in one call");
     hipError_t e = launch_fill_u32(out_counts, (size_t)P.num_views * (size_t)P.A * 2u, 0u, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(c, e, "render_instances clear");
     e = launch_render(P, (hipStream_t)stream);

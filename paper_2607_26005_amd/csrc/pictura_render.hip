@@ -1456,17 +1456,25 @@ __device__ __forceinline__ float decode_depth(const RenderParams& P, uint32_t ke
 
 
 // Draw agent `agent`'s box (world index h) alone with the rules R2-R7 and the
-// same arithmetic as the raster: every covered pixel sets its coverage bit, and
-// a pixel whose key equals the final key of the view keeps the lowest such
-// agent.  Adds the number of covered pixels to the agent's footprint.  One
-// wave; simple lane-per-pixel sweeps with exact int64 edge values.
-__device__ void draw_box_instances(const RenderParams& P, Shared& S, uint32_t* inst, const Tile& T, const Cam& cam,
+// same arithmetic as the raster: every covered pixel sets its coverage bit,
+// and a pixel whose key equals the final key of the view and that no box has
+// claimed yet is claimed by this agent, which is written to the instance image.
+// The caller draws the boxes in ascending agent order, so each pixel goes to
+// the lowest agent whose own frame holds its final key (one triangle of the
+// box with that key there is the same as the box's own minimum being it, as
+// the final key is the minimum over every triangle).  The claim bits sit in
+// the framebuffer's padding columns (words pitch - 4 and pitch - 3 of each row,
+// idle once the record ring has drained).  Adds the covered pixels to the
+// agent's footprint and the claimed ones to its visible count.  One wave;
+// simple lane-per-pixel sweeps with exact int64 edge values.
+__device__ void draw_box_instances(const RenderParams& P, Shared& S, const Tile& T, const Cam& cam,
                                    int64_t h, uint32_t agent, int64_t v)
 {
     const int lane = lane_id(), wid = threadIdx.x >> 6;
     uint32_t* bits = S.wv[wid].u.bits;
     bits[lane] = 0u;
     bits[lane + 64] = 0u;
+    uint32_t nclaim = 0;   // pixels this lane claimed
     __builtin_amdgcn_wave_barrier();
     const bool live = lane < 12;
     float tri[9] = {};
@@ -1544,7 +1552,14 @@ __device__ void draw_box_instances(const RenderParams& P, Shared& S, uint32_t* i
                     const uint32_t key = pixel_key(P, pxf, pyf, rpa, rpb, rpc, rcls);
                     if (cov && key != 0xFFFFFFFFu) {
                         atomicOr(&bits[2 * j + (i >> 5)], 1u << (i & 31));
-                        if (key == S.fb[j * T.pitch + i]) atomicMin(&inst[j * kSideTileW + i], agent);
+                        if (key == S.fb[j * T.pitch + i]) {
+                            const uint32_t b = 1u << (i & 31);
+                            if (!(atomicOr(&S.fb[j * T.pitch + T.pitch - 4 + (i >> 5)], b) & b)) {
+                                ++nclaim;
+                                P.out_inst[v * (int64_t)P.W * P.H + (int64_t)(T.y0 + j) * P.W + T.x0 + i] =
+                                    (int32_t)agent;
+                            }
+                        }
                     }
                 }
             }
@@ -1553,16 +1568,17 @@ __device__ void draw_box_instances(const RenderParams& P, Shared& S, uint32_t* i
     __builtin_amdgcn_wave_barrier();
     const uint32_t cnt = (uint32_t)(__popc(bits[lane]) + __popc(bits[lane + 64]));
     const uint32_t tot = readlane(wave_incl_sum(cnt), 63);
+    const uint32_t vis = readlane(wave_incl_sum(nclaim), 63);
     if (lane == 0 && tot != 0) atomicAdd(&P.out_counts[2 * (v * P.A + agent)], tot);
+    if (lane == 0 && vis != 0) atomicAdd(&P.out_counts[2 * (v * P.A + agent) + 1], vis);
     __builtin_amdgcn_wave_barrier();
 }
 
-// Side buffer of the antialiased and instance modes, tile pixel (i, j) at
-// j * kSideTileW + i: the edge buffer of R14 (the nearest partial-coverage
-// fragment, 0xFFFFFFFF none) or the lowest owning agent (0xFFFFFFFF none).  A
-// tile at most kSideTileW columns wide fills its framebuffer rows at a pitch
-// of kSideTileW + 4 words; the side buffer takes the words after them, so
-// these modes need no LDS beyond the class/depth kernel's.
+// Side buffer of the antialiased mode, tile pixel (i, j) at j * kSideTileW + i:
+// the edge buffer of R14 (the nearest partial-coverage fragment, 0xFFFFFFFF
+// none).  A tile at most kSideTileW columns wide fills its framebuffer rows at
+// a pitch of kSideTileW + 4 words; the side buffer takes the words after them,
+// so this mode needs no LDS beyond the class/depth kernel's.
 constexpr int kSideOff = 64 * (kSideTileW + 4);
 static_assert(kSideOff + 64 * kSideTileW <= kFbCap, "side buffer inside the framebuffer array");
 
@@ -1617,7 +1633,7 @@ void render_views_kernel(const RenderParams P_)
     T.w = min(P.tile_w, P.W - T.x0);
     T.h = min(P.tile_h, P.H - T.y0);
     T.pitch = ((T.w + 31) & ~31) + 4;
-    if constexpr (kAA || kInst) {
+    if constexpr (kAA) {
         // the host keeps tiles within kSideTileW columns; a wider one is not drawn
         if (T.w > kSideTileW) {
             if (threadIdx.x == 0) atomicOr(P.dev_err, kDevErrTile);
@@ -1647,7 +1663,7 @@ void render_views_kernel(const RenderParams P_)
     const int loff4 = ((lane >> 3) * T.pitch + (lane & 7)) * 4;
     if (P.stats && tid < kNumStats) S.stat[tid] = 0;
     if (tid < 4) S.ctl[tid] = 0;
-    if constexpr (kAA || kInst) {
+    if constexpr (kAA) {
         for (int p = tid; p < 64 * kSideTileW; p += kThreads) S.fb[kSideOff + p] = 0xFFFFFFFFu;
     }
 
@@ -1954,40 +1970,39 @@ void render_views_kernel(const RenderParams P_)
     __syncthreads();
 
     if constexpr (kInst) {
-        // every non-ego box that can reach the tile, the waves taking alternate agents
-        for (int ac = 0; ac * 64 * kViewWaves < P.A; ++ac) {
-            const int ai = (ac * 64 + lane) * kViewWaves + wid;
-            bool vis = ai < P.A && ai != a;
-            if (vis && cull) {
-                const int64_t h = abase_w + ai;
-                const float x = P.ax[h], y = P.ay[h], z0 = P.az0[h];
-                const float R = 0.5f * (P.al[h] + P.aw[h]) * 1.0009765625f + 0.0009765625f;
-                vis = aabb_visible(P, T, F, cam, x - R, y - R, z0, x + R, y + R, z0 + P.ah[h]);
-            }
-            uint64_t m = __ballot(vis);
-            while (m) {
-                const int l = __builtin_ctzll(m);
-                m &= m - 1;
-                const uint32_t agent = readlane((uint32_t)ai, l);
-                draw_box_instances(P, S, S.fb + kSideOff, T, cam, abase_w + agent, agent, v);
+        // claim bits of the tile's pixels: two padding words per framebuffer row
+        for (int r = tid; r < T.h; r += kThreads) {
+            S.fb[r * T.pitch + T.pitch - 4] = 0u;
+            S.fb[r * T.pitch + T.pitch - 3] = 0u;
+        }
+        __syncthreads();
+        // every non-ego box that can reach the tile, in ascending agent order, by one wave
+        if (wid == 0) {
+            for (int ac = 0; ac * 64 < P.A; ++ac) {
+                const int ai = ac * 64 + lane;
+                bool vis = ai < P.A && ai != a;
+                if (vis && cull) {
+                    const int64_t h = abase_w + ai;
+                    const float x = P.ax[h], y = P.ay[h], z0 = P.az0[h];
+                    const float R = 0.5f * (P.al[h] + P.aw[h]) * 1.0009765625f + 0.0009765625f;
+                    vis = aabb_visible(P, T, F, cam, x - R, y - R, z0, x + R, y + R, z0 + P.ah[h]);
+                }
+                uint64_t m = __ballot(vis);
+                while (m) {
+                    const int l = __builtin_ctzll(m);
+                    m &= m - 1;
+                    const uint32_t agent = readlane((uint32_t)ai, l);
+                    draw_box_instances(P, S, T, cam, abase_w + agent, agent, v);
+                }
             }
         }
         __syncthreads();
-        // the instance image and each agent's visible pixels
+        // pixels no box claimed own nothing
         const int64_t view_px = (int64_t)P.W * P.H;
         for (int p = tid; p < npx; p += kThreads) {
             const int row = p / T.w, col = p % T.w;
-            const uint32_t id = S.fb[kSideOff + row * kSideTileW + col];
-            P.out_inst[v * view_px + (int64_t)(T.y0 + row) * P.W + T.x0 + col] = (int32_t)id;
-            // one atomic per distinct owner among the wave's pixels
-            uint64_t m = __ballot(id != 0xFFFFFFFFu);
-            while (m) {
-                const uint32_t o = readlane(id, __builtin_ctzll(m));
-                const uint64_t same = __ballot(id == o);
-                if (lane == (int)__builtin_ctzll(same))
-                    atomicAdd(&P.out_counts[2 * (v * P.A + o) + 1], (uint32_t)__popcll(same));
-                m &= ~same;
-            }
+            const uint32_t claimed = (S.fb[row * T.pitch + T.pitch - 4 + (col >> 5)] >> (col & 31)) & 1u;
+            if (!claimed) P.out_inst[v * view_px + (int64_t)(T.y0 + row) * P.W + T.x0 + col] = -1;
         }
     }
 
