@@ -1997,12 +1997,11 @@ void render_views_kernel(const RenderParams P_)
             }
         }
         __syncthreads();
-        // pixels no box claimed own nothing
-        const int64_t view_px = (int64_t)P.W * P.H;
-        for (int p = tid; p < npx; p += kThreads) {
-            const int row = p / T.w, col = p % T.w;
-            const uint32_t claimed = (S.fb[row * T.pitch + T.pitch - 4 + (col >> 5)] >> (col & 31)) & 1u;
-            if (!claimed) P.out_inst[v * view_px + (int64_t)(T.y0 + row) * P.W + T.x0 + col] = -1;
+        // pixels no box claimed own nothing (a wave per row, a lane per column: tiles are at most 64 wide)
+        int32_t* const ibase = P.out_inst + v * (int64_t)P.W * P.H + (int64_t)T.y0 * P.W + T.x0;
+        for (int row = wid; row < T.h; row += kViewWaves) {
+            const uint32_t cw = S.fb[row * T.pitch + T.pitch - 4 + (lane >> 5)];
+            if (lane < T.w && !((cw >> (lane & 31)) & 1u)) ibase[(int64_t)row * P.W + lane] = -1;
         }
     }
 
