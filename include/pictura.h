@@ -201,22 +201,31 @@ pictura_status pictura_render_rgb(pictura_ctx ctx, const pictura_agents* agents,
  * that thin structures such as lane lines stay visible at low resolution,
  * Sec. 3.2, rendering features, and App. on render quality).  out_cls and
  * out_depth are those of pictura_render_views (the pixel centre's surface).
- * Each fan piece of rule R6 leaves a fragment on every pixel whose centre is
- * within one pixel of its snapped bounding box and that it covers in part:
- * with E_k the edge function of R6 at the centre (no top-left bias) and L_k
- * the edge's length, both in subpixels, c_k = min(max(fma(fl(E_k),
- * fl(1 / (256 L_k)), 0.5), 0), 1), coverage a = min(max(((c_0 + c_1) + c_2) -
- * 2, 0), 1), a8 = rint(255 a), fp32; the fragment exists when 0 < a8 < 255
- * and the piece's depth plane passes R7's test at the centre.  A pixel keeps
- * its nearest fragment, ordered by o = (key >> 16) << 16 | (key & 255) << 8 |
- * (255 - a8) with key the fragment's R7 key.  With key_c the pixel's final
- * key, when o >> 16 <= key_c >> 16 (the fragment is not behind the centre's
- * surface) and (o >> 8) & 255 != key_c & 255 (another shading id), the
- * pixel's colour is (C_o * a8 + C_c * (255 - a8) + 127) /
- * 255 per channel in integers, C_o the R13 colour of the key ((o >> 16) << 16)
- * | ((o >> 8) & 255) and C_c that of key_c; otherwise C_c.  Runs a kernel
- * variant with an extra 16 KiB LDS edge buffer per tile at half the
- * occupancy.  Buffers, errors and ordering as pictura_render_rgb. */
+ * A surface is a snapped 4-gon whose two fan pieces are both drawn and whose
+ * turns all have one sign, none zero: a pair of scene triangles (a, b, c),
+ * (a, c, d) of one class (see pictura_scene_upload) with all four vertices in
+ * front of the near plane and neither triangle wholly beyond far, or a
+ * triangle that the near clip turns into a 4-gon; otherwise each fan piece of
+ * rule R6 is a surface of its own.  A surface leaves a fragment on every pixel
+ * whose centre is within one pixel of its snapped bounding box and that it
+ * covers in part: with E_k the edge function of R6 at the centre (no top-left
+ * bias) and L_k the edge's length, both in subpixels, c_k = min(max(
+ * fma(fl(E_k), fl(1 / (256 L_k)), 0.5), 0), 1), coverage a = min(max(((c_0 +
+ * c_1) + c_2) - 2, 0), 1) for a triangle (edges v1->v2, v2->v0, v0->v1) and
+ * min(max((((c_0 + c_1) + c_2) + c_3) - 3, 0), 1) for a 4-gon in positive
+ * order (edges p_k->p_k+1), a8 = rint(255 a), fp32; the fragment exists when
+ * 0 < a8 < 255 and the depth plane of the surface's first piece passes R7's
+ * test at the centre.  A pixel keeps its nearest fragment, ordered by o =
+ * (key >> 16) << 16 | (key & 255) << 8 | (255 - a8) with key the fragment's R7
+ * key.  With key_c the pixel's final key, when o >> 16 <= key_c >> 16 (the
+ * fragment is not behind the centre's surface) and (o >> 8) & 255 != key_c &
+ * 255 (another shading id), the pixel's colour is (C_o * a8 + C_c * (255 -
+ * a8) + 127) / 255 per channel in integers, C_o the R13 colour of the key
+ * ((o >> 16) << 16) | ((o >> 8) & 255) and C_c that of key_c; otherwise C_c.
+ * During the call the kernel keeps each pixel's nearest fragment in the words
+ * of out_depth and writes the depths over them at the end, so out_depth must
+ * not overlap out_cls or out_rgb.  Buffers, errors and ordering as
+ * pictura_render_rgb. */
 pictura_status pictura_render_rgb_aa(pictura_ctx ctx, const pictura_agents* agents, const pictura_rig* rig,
                                      uint8_t* out_cls, float* out_depth, uint8_t* out_rgb, void* stream);
 
@@ -320,7 +329,6 @@ pictura_status pictura_set_option(pictura_ctx ctx, int32_t option, int32_t value
 pictura_status pictura_stats_copy(pictura_ctx ctx, uint64_t* out, int32_t n, int32_t reset);
 
 #define PICTURA_DEVERR_RING_WAIT 1u /* a raster record reserved in a view's record ring was never published */
-#define PICTURA_DEVERR_TILE 2u      /* a view tile wider than its mode admits reached a kernel (not drawn) */
 /* Device-side errors the render kernels found (the kernels cannot return a
  * status): *out receives the OR of the PICTURA_DEVERR_* bits set by every
  * render call on this context since it was created or last reset; 0 means

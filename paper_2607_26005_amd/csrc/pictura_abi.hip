@@ -446,20 +446,6 @@ pictura_status pictura_render_views(pictura_ctx c, const pictura_agents* ag, con
     return PICTURA_OK;
 }
 
-// The antialiased mode keeps a per-pixel side buffer in the framebuffer's
-// LDS: its tiles are at most kSideTileW columns wide.  False if the launch
-// would then hold too many view tiles.
-static bool narrow_tiles(RenderParams& P)
-{
-    if (P.tile_w <= kSideTileW) return true;
-    P.tile_w = kSideTileW;
-    P.tiles_x = (P.W + kSideTileW - 1) / kSideTileW;
-    P.num_blocks = P.num_views * P.tiles_x * P.tiles_y;
-    if (P.num_blocks > 0x7FFFFFFFll) return false;
-    P.div_tiles = make_div31((uint32_t)(P.tiles_x * P.tiles_y));
-    return true;
-}
-
 static pictura_status render_rgb(pictura_ctx c, const pictura_agents* ag, const pictura_rig* rig, uint8_t* out_cls,
                                  float* out_depth, uint8_t* out_rgb, void* stream, bool aa)
 {
@@ -475,7 +461,6 @@ static pictura_status render_rgb(pictura_ctx c, const pictura_agents* ag, const 
     P.out_rgb = out_rgb;
     P.rfar = 1.0f / P.farp;
     P.aa = aa ? 1 : 0;
-    if (aa && !narrow_tiles(P)) return fail(c, PICTURA_ERANGE, "render_rgb: too many view tiles in one call");
     hipError_t e = launch_render(P, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(c, e, "render_rgb launch");
     return PICTURA_OK;

@@ -106,11 +106,7 @@ struct RenderParams {
 
 // Device error bits (pictura_device_errors)
 constexpr uint32_t kDevErrRingWait = 1u;   // a raster record reserved in the ring was never published
-constexpr uint32_t kDevErrTile = 2u;       // a view tile wider than its mode's LDS layout admits (not drawn)
-// Antialiased colour: view tiles are at most this many columns wide, so the
-// per-pixel edge buffer fits in the framebuffer words such a tile leaves
-// unused.
-constexpr int kSideTileW = 32;
+
 
 struct AgentStepParams {
     float* x; float* y; float* psi; float* speed; float* cos_h; float* sin_h;

@@ -932,7 +932,7 @@ __device__ __forceinline__ void aa_packed(const RenderParams& P, Shared& S, Wave
         // p in range keeps the address inside the window, hence the tile
         const bool inr = (slot < n) & (p >= 0) & (p < tn);
         STAT(kStAaFrags, inr && f != 0xFFFFFFFFu ? 1 : 0);
-        atomicMin(&fbo[inr ? y * kSideTileW + x : lane], inr ? f : 0xFFFFFFFFu);
+        if (inr && f != 0xFFFFFFFFu) atomicMin(&fbo[y * P.W + x], f);
         __builtin_amdgcn_wave_barrier();
     }
 }
@@ -1073,7 +1073,7 @@ __device__ void aa_pieces(const RenderParams& P, Shared& S, WaveLds& L, uint32_t
                                            ((float)(T.x0 + i) + 0.5f) - P.cx, ((float)(T.y0 + j) + 0.5f) - P.cy, rpa,
                                            rpb, rpc, rcls);
             STAT(kStAaFrags, f != 0xFFFFFFFFu ? 1 : 0);
-            atomicMin(&fbo[j * kSideTileW + i], f);
+            if (f != 0xFFFFFFFFu) atomicMin(&fbo[j * P.W + i], f);
         }
     }
 }
@@ -1574,13 +1574,13 @@ __device__ void draw_box_instances(const RenderParams& P, Shared& S, const Tile&
     __builtin_amdgcn_wave_barrier();
 }
 
-// Side buffer of the antialiased mode, tile pixel (i, j) at j * kSideTileW + i:
-// the edge buffer of R14 (the nearest partial-coverage fragment, 0xFFFFFFFF
-// none).  A tile at most kSideTileW columns wide fills its framebuffer rows at
-// a pitch of kSideTileW + 4 words; the side buffer takes the words after them,
-// so this mode needs no LDS beyond the class/depth kernel's.
-constexpr int kSideOff = 64 * (kSideTileW + 4);
-static_assert(kSideOff + 64 * kSideTileW <= kFbCap, "side buffer inside the framebuffer array");
+// Edge buffer of the antialiased mode: the nearest partial-coverage fragment of
+// each pixel (0xFFFFFFFF none), a global minimum kept in the words of the
+// caller's depth image, row pitch W.  The view tile's workgroup fills its words
+// before the static pass, takes the fragments with atomic minima, reads them
+// back in the colour resolve (loads that bypass the CU's L1) and only then
+// writes the depths over them, so the mode needs no LDS beyond the class/depth
+// kernel's and draws 64 x 64 tiles.
 
 // Every mode runs four waves per SIMD (the LDS of eight view tiles per CU).
 // kMode: 0 class and depth, 1 with instance visibility, 2 with antialiased
@@ -1633,13 +1633,6 @@ void render_views_kernel(const RenderParams P_)
     T.w = min(P.tile_w, P.W - T.x0);
     T.h = min(P.tile_h, P.H - T.y0);
     T.pitch = ((T.w + 31) & ~31) + 4;
-    if constexpr (kAA) {
-        // the host keeps tiles within kSideTileW columns; a wider one is not drawn
-        if (T.w > kSideTileW) {
-            if (threadIdx.x == 0) atomicOr(P.dev_err, kDevErrTile);
-            return;
-        }
-    }
     // culling reaches the pixel centres of the tile, and with antialiasing the
     // centres within half a pixel more, where a surface's edge fragments land
     constexpr float tpad = kAA ? 1.0f : 0.5f;
@@ -1663,8 +1656,11 @@ void render_views_kernel(const RenderParams P_)
     const int loff4 = ((lane >> 3) * T.pitch + (lane & 7)) * 4;
     if (P.stats && tid < kNumStats) S.stat[tid] = 0;
     if (tid < 4) S.ctl[tid] = 0;
+    // antialiased mode: the edge buffer (in the depth image's words) starts empty
+    uint32_t* const ebuf = kAA ? (uint32_t*)P.out_depth + v * (int64_t)P.W * P.H + (int64_t)T.y0 * P.W + T.x0 : nullptr;
     if constexpr (kAA) {
-        for (int p = tid; p < 64 * kSideTileW; p += kThreads) S.fb[kSideOff + p] = 0xFFFFFFFFu;
+        for (int row = wid; row < T.h; row += kViewWaves)
+            if (lane < T.w) ebuf[(int64_t)row * P.W + lane] = 0xFFFFFFFFu;
     }
 
     // world-space frustum planes of the tile: four side planes through the
@@ -1708,6 +1704,9 @@ void render_views_kernel(const RenderParams P_)
     const int64_t abase_w = (int64_t)w * P.A;
     const int64_t lbase_w = (int64_t)w * P.L;
     if (tid == 0) { STAT(kStTiles, 1); STAT(kStCellsRect, nrect); }
+    // antialiased mode: every wave's fills of the edge buffer have completed
+    // (vmcnt 0) before any wave passes the barrier and adds fragments
+    if constexpr (kAA) __builtin_amdgcn_s_waitcnt(0);
     __syncthreads();
     TACC(kCycPrologue, t_kernel);
 
@@ -1906,9 +1905,7 @@ void render_views_kernel(const RenderParams P_)
             __builtin_amdgcn_wave_barrier();
             STAT1(kStExact, 1);
             TSTART(t_ex);
-            uint32_t* fbo = nullptr;
-            if constexpr (kAA) fbo = S.fb + kSideOff;
-            exact_pass<kAA>(P, S, L, T, cam, live, entry, abase_w, lbase_w, pxl, pyl, loff4, fbo);
+            exact_pass<kAA>(P, S, L, T, cam, live, entry, abase_w, lbase_w, pxl, pyl, loff4, ebuf);
             TACC(kCycExact, t_ex);
         }
         if (phase == kDone && nq == 0) break;
@@ -2010,6 +2007,41 @@ void render_views_kernel(const RenderParams P_)
     const int64_t view_px = (int64_t)P.W * P.H;
     uint8_t* ocls = P.out_cls + v * view_px;
     float* odep = P.out_depth + v * view_px;
+    auto colour_resolve = [&]() {
+        // R13: shaded colour of each pixel, planar [3][H][W] per view
+        uint8_t* const rgb = P.out_rgb + v * 3 * view_px;
+        for (int p = tid; p < npx; p += kThreads) {
+            const int row = p / T.w, col = p % T.w;
+            const uint32_t key = S.fb[row * T.pitch + col];
+            uint32_t c3[3];
+            shade_rgb(P, key, c3);
+            if constexpr (kAA) {
+                // R14: a partial-coverage fragment not behind the centre's surface and
+                // of another shading id blends over it
+                const uint32_t ko = __hip_atomic_load(&ebuf[(int64_t)row * P.W + col], __ATOMIC_RELAXED,
+                                                      __HIP_MEMORY_SCOPE_AGENT);
+                if (ko != 0xFFFFFFFFu && (ko >> 16) <= (key >> 16) && ((ko >> 8) & 255u) != (key & 255u)) {
+                    uint32_t o3[3];
+                    shade_rgb(P, ((ko >> 16) << 16) | ((ko >> 8) & 255u), o3);
+                    const uint32_t a8 = 255u - (ko & 255u);
+#pragma unroll
+                    for (int c = 0; c < 3; ++c) c3[c] = (o3[c] * a8 + c3[c] * (255u - a8) + 127u) / 255u;
+                }
+            }
+            const int64_t o = (int64_t)(T.y0 + row) * P.W + T.x0 + col;
+            rgb[o] = (uint8_t)c3[0];
+            rgb[view_px + o] = (uint8_t)c3[1];
+            rgb[2 * view_px + o] = (uint8_t)c3[2];
+        }
+    };
+    if constexpr (kAA) {
+        // every wave's fragment minima have completed (vmcnt 0) before any is read,
+        // and every one is read before the depths overwrite the edge buffer
+        __builtin_amdgcn_s_waitcnt(0);
+        __syncthreads();
+        colour_resolve();
+        __syncthreads();
+    }
     if (P.vec_out && (P.W % 16) == 0 && (T.w % 16) == 0) {
         // tile origin in the view's images; the offsets below stay 32-bit
         uint8_t* const cbase = ocls + ((int64_t)T.y0 * P.W + T.x0);
@@ -2061,32 +2093,7 @@ void render_views_kernel(const RenderParams P_)
             odep[o] = (key >> 8) == 0xFFFFFFu ? __uint_as_float(0x7F800000u) : decode_depth(P, key);
         }
     }
-    if (P.out_rgb) {
-        // R13: shaded colour of each pixel, planar [3][H][W] per view
-        uint8_t* const rgb = P.out_rgb + v * 3 * view_px;
-        for (int p = tid; p < npx; p += kThreads) {
-            const int row = p / T.w, col = p % T.w;
-            const uint32_t key = S.fb[row * T.pitch + col];
-            uint32_t c3[3];
-            shade_rgb(P, key, c3);
-            if constexpr (kAA) {
-                // R14: a partial-coverage fragment not behind the centre's surface and
-                // of another shading id blends over it
-                const uint32_t ko = S.fb[kSideOff + row * kSideTileW + col];
-                if (ko != 0xFFFFFFFFu && (ko >> 16) <= (key >> 16) && ((ko >> 8) & 255u) != (key & 255u)) {
-                    uint32_t o3[3];
-                    shade_rgb(P, ((ko >> 16) << 16) | ((ko >> 8) & 255u), o3);
-                    const uint32_t a8 = 255u - (ko & 255u);
-#pragma unroll
-                    for (int c = 0; c < 3; ++c) c3[c] = (o3[c] * a8 + c3[c] * (255u - a8) + 127u) / 255u;
-                }
-            }
-            const int64_t o = (int64_t)(T.y0 + row) * P.W + T.x0 + col;
-            rgb[o] = (uint8_t)c3[0];
-            rgb[view_px + o] = (uint8_t)c3[1];
-            rgb[2 * view_px + o] = (uint8_t)c3[2];
-        }
-    }
+    if constexpr (kMode == 3) colour_resolve();
     if (P.stats) {
         TACC(kCycWriteout, t_out);
         __syncthreads();

@@ -266,12 +266,22 @@ def pictura_render_rgb(ctx, agents, rig, out_cls, out_depth, out_rgb, stream=Non
     _check(ctx, _lib.pictura_render_rgb(ctx, ctypes.byref(a), ctypes.byref(r), oc, od, orgb, _stream(stream)))
 
 
+def _disjoint(name_a: str, a: int, na: int, name_b: str, b: int, nb: int) -> None:
+    """Raise PicturaError(EINVAL) if the byte ranges [a, a + na) and [b, b + nb) meet."""
+    if a < b + nb and b < a + na:
+        raise PicturaError(EINVAL, f"{name_a} overlaps {name_b}")
+
+
 def pictura_render_rgb_aa(ctx, agents, rig, out_cls, out_depth, out_rgb, stream=None):
-    """As pictura_render_rgb, with analytic-coverage antialiasing of out_rgb."""
+    """As pictura_render_rgb, with analytic-coverage antialiasing of out_rgb.
+    The kernel keeps its edge buffer in out_depth's words during the call, so
+    out_depth may not overlap out_cls or out_rgb."""
     r = _rig(rig)
     a = _agents(ctx, agents)
     npx, oc, od = _outputs(ctx, agents, r, out_cls, out_depth)
     orgb = _dev(out_rgb, "out_rgb", "u8", 3 * npx, ctx)
+    _disjoint("out_depth", od, 4 * npx, "out_cls", oc, npx)
+    _disjoint("out_depth", od, 4 * npx, "out_rgb", orgb, 3 * npx)
     _check(ctx, _lib.pictura_render_rgb_aa(ctx, ctypes.byref(a), ctypes.byref(r), oc, od, orgb, _stream(stream)))
 
 

@@ -92,6 +92,17 @@ def test_outputs_dtype_and_size():
             torch.zeros(3 * V * 256 - 1, dtype=torch.uint8))
 
 
+def test_antialiased_depth_may_not_overlap_the_other_outputs():
+    # the antialiased kernel keeps its edge buffer in out_depth's words
+    n = V * 16 * 16
+    big = torch.zeros(4 * n + 4 * n, dtype=torch.uint8)
+    od = big[: 4 * n].view(torch.float32)
+    _raises("out_depth overlaps out_cls", pictura.pictura_render_rgb_aa, None, _agents(), RIG, big[4 * n - 8:][:n], od,
+            torch.zeros(3 * n, dtype=torch.uint8))
+    _raises("out_depth overlaps out_rgb", pictura.pictura_render_rgb_aa, None, _agents(), RIG,
+            torch.zeros(n, dtype=torch.uint8), od, big[8:][: 3 * n])
+
+
 def test_instance_outputs_dtype_and_size():
     oc, od = _out()
     inst = torch.zeros(V * 256, dtype=torch.int32)
