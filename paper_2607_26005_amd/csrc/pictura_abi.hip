@@ -393,7 +393,20 @@ static pictura_status render_setup(pictura_ctx c, const pictura_agents* ag, cons
     // decoded inverse depths lie in [1/far (1 - 2^-20), IZCAP]
     P.fast_decode = (izfar >= 0.000244140625f * 1.0000038f && izcap < 1048576.0f) ? 1 : 0;
     int tw = 64, th = 64;
-    if (c->tile > 0) { tw = c->tile; th = c->tile; }
+    if (c->tile > 0) {
+        tw = c->tile;
+        th = c->tile;
+    } else {
+        // as few 64-wide columns and rows of tiles as the view needs, split
+        // evenly (96 wide: two tiles of 48 rather than 64 and 32); for a view
+        // whose width is a multiple of 16 (the vector write-out's unit) the tile
+        // width is one too, as long as that keeps the count
+        const int nx = (P.W + 63) / 64, ny = (P.H + 63) / 64;
+        const int ex = (P.W + nx - 1) / nx, ey = (P.H + ny - 1) / ny;
+        const int ex16 = (ex + 15) & ~15;
+        tw = (P.W % 16) == 0 && ex16 <= 64 && (P.W + ex16 - 1) / ex16 == nx ? ex16 : ex;
+        th = ey;
+    }
     tw = tw < P.W ? tw : P.W;
     th = th < P.H ? th : P.H;
     P.tile_w = tw; P.tile_h = th;
