@@ -446,12 +446,6 @@ static void raster_tri_f(const Params* P, Frame* F, int32_t X0, int32_t Y0, int3
     }
 }
 
-static void raster_tri(const Params* P, Frame* F, int32_t X0, int32_t Y0, int32_t X1, int32_t Y1,
-                       int32_t X2, int32_t Y2, float pa, float pb, float pc, uint32_t cls)
-{
-    raster_tri_f(P, F, X0, Y0, X1, Y1, X2, Y2, pa, pb, pc, cls, 1);
-}
-
 /* One world-space triangle through R2..R7. */
 static void draw_triangle(const Params* P, const Cam* cam, Frame* F, const float* t, uint32_t cls)
 {
