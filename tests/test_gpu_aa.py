@@ -121,6 +121,22 @@ def test_aa_town_paper_rig_tiles_and_unculled(lib):
     check(lib, wl, views[:16], "aa-town-unculled", cull=0)
 
 
+def test_aa_headline_full_launch_sampled(lib):
+    # the benchmark's antialiased launch: 1024 worlds x 64 agents x 4 cameras,
+    # every view rendered, 64 sampled across the worlds compared with the oracle
+    wl = workload(4)
+    views = np.sort(np.random.default_rng(63).choice(wl.num_views, size=64, replace=False))
+    assert len(np.unique(views // 256)) > 48
+    assert check(lib, wl, views, "aa-headline") > 0
+
+
+def test_aa_highres_full_launch_sampled(lib):
+    # 128 x 128 views in four 64 x 64 tiles, the whole high-res launch
+    wl = workload(5)
+    views = np.sort(np.random.default_rng(64).choice(wl.num_views, size=24, replace=False))
+    assert check(lib, wl, views, "aa-highres") > 0
+
+
 def test_aa_leaves_classes_and_depth_alone(lib):
     wl = workload(2, 1)
     c1, d1, _ = gpu_render(lib, wl.scene, wl.cell_size, wl.agents, wl.rig, antialias=True)

@@ -82,6 +82,14 @@ def test_instances_tiled_and_unculled(lib):
     check(lib, wl, views, "inst-nocull", cull=0)
 
 
+def test_instances_headline_full_launch_sampled(lib):
+    # the benchmark's instance launch: 1024 worlds x 64 agents x 4 cameras
+    wl = workload(4)
+    views = np.sort(np.random.default_rng(44).choice(wl.num_views, size=64, replace=False))
+    assert len(np.unique(views // 256)) > 48
+    check(lib, wl, views, "inst-headline")
+
+
 def test_instances_town_with_lights(lib):
     wl = workload(7, 2)   # paper rig: two tiles per view; lights and parked cars own no instance
     rng = np.random.default_rng(43)
