@@ -43,7 +43,7 @@ HBM_PEAK_GBS = 8000.0   # MI355X HBM3E peak
 # `traffic` is reported as null.
 TRAFFIC = {
     "config": 4,
-    "sources_sha256": "cabf5926ebd65d0d8bd3657d10a10fd5054c0ccecd48505c2b5c8a42461b5079",
+    "sources_sha256": "b8028776e2fb7d9686fba6729440f6d02e37a064df21649e925b931015509bfd",
     "fetch_bytes": 1.1539e9,
     "write_bytes": 5368709120,
 }
