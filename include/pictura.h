@@ -244,8 +244,9 @@ pictura_status pictura_render_rgb_aa(pictura_ctx ctx, const pictura_agents* agen
  *    fraction = 1 - visible / footprint.
  * Device buffers, caller-owned: out_inst V*H*W int32, out_counts
  * V*agents_per_world*2 uint32 (the library clears it on `stream` first).
- * The instance variant of the kernel keeps two extra 64x64 buffers in LDS and
- * runs at half the occupancy of pictura_render_views.  Errors as
+ * After the class/depth pass the kernel draws the visible boxes in ascending
+ * agent order; a pixel is claimed through one bit in the framebuffer's
+ * padding and its owner stored straight into out_inst.  Errors as
  * pictura_render_views, and EINVAL for a null out_inst or out_counts.
  * Asynchronous on `stream`. */
 pictura_status pictura_render_instances(pictura_ctx ctx, const pictura_agents* agents, const pictura_rig* rig,
