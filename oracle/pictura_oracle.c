@@ -79,11 +79,16 @@
  *              min(z * (1/far), 1) on box faces (z the output depth), else 1.
  * R14 antialiasing (optional, colour mode; the paper smooths edges with
  *              analytic coverage at one sample per pixel, Sec. 3.2 and its
- *              appendix on render quality): every snapped fan piece leaves,
- *              on each pixel whose centre is within one pixel of its box, a
- *              fragment with coverage a8 = rint(255 a), a = clamp(sum of
- *              the edges' clamp(0.5 + signed centre distance in px) - 2),
- *              when 0 < a8 < 255 and its R7 key at the centre exists.  The
+ *              appendix on render quality): every surface leaves, on each
+ *              pixel whose centre is within one pixel of its box, a fragment
+ *              with coverage a8 = rint(255 a), a = clamp(sum of the edges'
+ *              clamp(0.5 + signed centre distance in px) - (edges - 1)), when
+ *              0 < a8 < 255 and its R7 key at the centre exists.  A surface
+ *              is a strictly convex snapped 4-gon whose two fan pieces are
+ *              both drawn (a pair of scene triangles (a, b, c), (a, c, d) in
+ *              front of near and not beyond far, or a triangle clipped to
+ *              four vertices; its key from the first piece's plane), else a
+ *              single snapped fan piece.  The
  *              pixel keeps the least o = (key >> 16) << 16 | (key & 255) << 8
  *              | (255 - a8); a kept fragment not behind the centre's key
  *              (16-bit depth prefix) with another shading id blends over the
