@@ -137,6 +137,18 @@ def test_aa_highres_full_launch_sampled(lib):
     assert check(lib, wl, views, "aa-highres") > 0
 
 
+def test_aa_ragged_sizes(lib):
+    # non-square views not a multiple of 16 wide (scalar write-out; even tiles of
+    # 40 x 24, 50 x 35, 17 x 43): the edge buffer's row pitch is the view width
+    wl = workload(2, 1)
+    for (W, H) in ((40, 24), (100, 70), (17, 129)):
+        rig = sg.Rig(width=W, height=H, fx=W / 2.0, fy=W / 2.0, cx=W / 2.0, cy=H / 2.0, near=0.5, far=100.0,
+                     mount=wl.rig.mount)
+        wl2 = sg.Workload(wl.name, 2, 1, wl.scene, wl.agents, rig, wl.cell_size, wl.world_size)
+        views = np.sort(np.random.default_rng(W).choice(wl2.num_views, size=32, replace=False))
+        check(lib, wl2, views, f"aa-ragged {W}x{H}")
+
+
 def test_aa_leaves_classes_and_depth_alone(lib):
     wl = workload(2, 1)
     c1, d1, _ = gpu_render(lib, wl.scene, wl.cell_size, wl.agents, wl.rig, antialias=True)
