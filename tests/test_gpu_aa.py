@@ -149,6 +149,57 @@ def test_aa_ragged_sizes(lib):
         check(lib, wl2, views, f"aa-ragged {W}x{H}")
 
 
+def _random_quads(seed, n=400):
+    """A soup of quads given as pairs (a, b, c), (a, c, d): convex ones, darts
+    (one vertex pulled past the diagonal), slivers a few millimetres wide, and
+    quads that cross the cameras' near plane or reach far to the side."""
+    rng = np.random.default_rng(seed)
+    tris, cls = [], []
+    for q in range(n):
+        kind = q % 5
+        c = np.array([rng.uniform(-40, 40), rng.uniform(-40, 40), rng.uniform(-2, 4)])
+        if kind == 3:   # near the camera centre: crosses the near plane of some views
+            c[:2] = rng.uniform(-1.5, 1.5, 2)
+        u = rng.normal(size=3); u /= np.linalg.norm(u)
+        v = np.cross(u, rng.normal(size=3)); v /= np.linalg.norm(v)
+        ru, rv = rng.uniform(0.2, 8.0), rng.uniform(0.2, 8.0)
+        if kind == 3:
+            ru, rv = rng.uniform(0.3, 1.5), rng.uniform(0.3, 1.5)
+        if kind == 1:
+            rv = rng.uniform(0.002, 0.02)          # sliver
+        if kind == 4:
+            ru = rng.uniform(50.0, 300.0)          # long, reaching far out of the view
+        ang = np.sort(rng.uniform(0, 2 * np.pi, 4))
+        r = np.ones(4)
+        if kind == 2:
+            r[rng.integers(4)] = rng.uniform(0.05, 0.3)   # dart: not convex
+        pts = [c + r[k] * (ru * np.cos(ang[k]) * u + rv * np.sin(ang[k]) * v) for k in range(4)]
+        a, b, cc, d = [tuple(map(float, p)) for p in pts]
+        tris += [[a, b, cc], [a, cc, d]]
+        k = int(rng.choice([0, 1, 2, 5, 7]))
+        cls += [k, k]
+    return tris, cls
+
+
+def test_aa_random_quads_slivers_darts_and_near_clips(lib):
+    # pairs as one surface when convex, per-triangle fragments otherwise,
+    # near-clipped 4-gons, snap-range cases: colour bit-exact off flagged pixels
+    for seed in (71, 72):
+        tris, cls = _random_quads(seed)
+        sc = make_scene(np.asarray(tris, np.float32), cls)
+        rows = [(0.0, 0.0, 0.0, 1.0, 0.0, 4.5, 1.9, 1.5, 3)]
+        rng = np.random.default_rng(seed + 100)
+        for _ in range(5):
+            ang = rng.uniform(0, 2 * np.pi)
+            rows.append((rng.uniform(-20, 20), rng.uniform(-20, 20), 0.0, float(np.cos(ang)), float(np.sin(ang)),
+                         4.5, 1.9, 1.5, 3))
+        ag = make_agents(rows)
+        rig = make_rig(res=64, far=80.0, mounts=((0.0, 0.0, 1.0, 1.0, 0.0), (0.0, 0.0, 1.0, 0.0, 1.0),
+                                                  (0.0, 0.0, 1.0, -1.0, 0.0), (0.0, 0.0, 1.0, 0.0, -1.0)))
+        wl = sg.Workload("random-quads", 0, seed, sc, ag, rig, 16.0, 2000.0)
+        assert check(lib, wl, np.arange(wl.num_views), f"aa-random-quads {seed}") > 0
+
+
 def test_aa_leaves_classes_and_depth_alone(lib):
     wl = workload(2, 1)
     c1, d1, _ = gpu_render(lib, wl.scene, wl.cell_size, wl.agents, wl.rig, antialias=True)
