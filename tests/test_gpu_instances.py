@@ -90,6 +90,24 @@ def test_instances_headline_full_launch_sampled(lib):
     check(lib, wl, views, "inst-headline")
 
 
+def test_instances_among_random_quad_pairs(lib):
+    # boxes among a soup of quad pairs (convex, darts, slivers, near-plane crossings)
+    from tests.test_gpu_aa import _random_quads
+    from tests.scenes import make_agents, make_rig, make_scene
+    tris, cls = _random_quads(91)
+    rng = np.random.default_rng(191)
+    rows = [(0.0, 0.0, 0.0, 1.0, 0.0, 4.5, 1.9, 1.5, 3)]
+    for _ in range(11):
+        ang = rng.uniform(0, 2 * np.pi)
+        rows.append((rng.uniform(-15, 15), rng.uniform(-15, 15), 0.0, float(np.cos(ang)), float(np.sin(ang)),
+                     4.5, 1.9, 1.5, 3))
+    rig = make_rig(res=64, far=80.0, mounts=((0.0, 0.0, 1.0, 1.0, 0.0), (0.0, 0.0, 1.0, 0.0, 1.0),
+                                              (0.0, 0.0, 1.0, -1.0, 0.0), (0.0, 0.0, 1.0, 0.0, -1.0)))
+    wl = sg.Workload("random-quads", 0, 91, make_scene(np.asarray(tris, np.float32), cls), make_agents(rows), rig,
+                     16.0, 2000.0)
+    assert check(lib, wl, np.arange(wl.num_views), "inst-random-quads") > 0
+
+
 def test_instances_town_with_lights(lib):
     wl = workload(7, 2)   # paper rig: two tiles per view; lights and parked cars own no instance
     rng = np.random.default_rng(43)

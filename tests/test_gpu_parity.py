@@ -190,6 +190,25 @@ def test_ragged_sizes_and_tiles(lib):
         check_views(lib, wl2, sample_views(wl2.num_views, 64, W), f"ragged {W}x{H}")
 
 
+def test_random_quad_pairs(lib):
+    # quads given as pairs (a, b, c), (a, c, d): convex, darts, slivers, near-plane
+    # crossings and quads reaching far to the side, seen by four cameras
+    from tests.test_gpu_aa import _random_quads
+    for seed in (81, 82):
+        tris, cls = _random_quads(seed)
+        sc = make_scene(np.asarray(tris, np.float32), cls)
+        rng = np.random.default_rng(seed + 100)
+        rows = [(0.0, 0.0, 0.0, 1.0, 0.0, 4.5, 1.9, 1.5, 3)]
+        for _ in range(5):
+            ang = rng.uniform(0, 2 * np.pi)
+            rows.append((rng.uniform(-20, 20), rng.uniform(-20, 20), 0.0, float(np.cos(ang)), float(np.sin(ang)),
+                         4.5, 1.9, 1.5, 3))
+        rig = make_rig(res=64, far=80.0, mounts=((0.0, 0.0, 1.0, 1.0, 0.0), (0.0, 0.0, 1.0, 0.0, 1.0),
+                                                  (0.0, 0.0, 1.0, -1.0, 0.0), (0.0, 0.0, 1.0, 0.0, -1.0)))
+        wl = sg.Workload("random-quads", 0, seed, sc, make_agents(rows), rig, 16.0, 2000.0)
+        check_views(lib, wl, np.arange(wl.num_views), f"random-quads {seed}")
+
+
 def test_empty_world_and_lone_agent(lib):
     # world 0 has no triangles, world 1 one quad; one agent per world (no boxes)
     q = np.asarray(quad((8.0, -2.0, -2.0), (8.0, 2.0, -2.0), (8.0, 2.0, 2.0), (8.0, -2.0, 2.0)), np.float32)
