@@ -2008,13 +2008,33 @@ void render_views_kernel(const RenderParams P_)
     uint8_t* ocls = P.out_cls + v * view_px;
     float* odep = P.out_depth + v * view_px;
     auto colour_resolve = [&]() {
-        // R13: shaded colour of each pixel, planar [3][H][W] per view
+        // R13: shaded colour of each pixel, planar [3][H][W] per view.  Off box
+        // faces (face bits 0) the colour depends on the class alone: a table of
+        // the 16 such colours, computed by shade_rgb itself, in the wave's list
+        // area (idle after the static pass)
+        uint32_t* const pal0 = S.wv[wid].u.bits;
+        if (lane < 16) {
+            uint32_t t3[3];
+            shade_rgb(P, (uint32_t)lane, t3);
+            pal0[lane] = t3[0] | t3[1] << 8 | t3[2] << 16;
+        }
+        __builtin_amdgcn_wave_barrier();
+        auto shade = [&](uint32_t key, uint32_t* c3) {
+            if (((key >> 4) & 7u) == 0u) {
+                const uint32_t w = pal0[key & 15u];
+                c3[0] = w & 255u;
+                c3[1] = (w >> 8) & 255u;
+                c3[2] = w >> 16;
+            } else {
+                shade_rgb(P, key, c3);
+            }
+        };
         uint8_t* const rgb = P.out_rgb + v * 3 * view_px;
         for (int p = tid; p < npx; p += kThreads) {
             const int row = p / T.w, col = p % T.w;
             const uint32_t key = S.fb[row * T.pitch + col];
             uint32_t c3[3];
-            shade_rgb(P, key, c3);
+            shade(key, c3);
             if constexpr (kAA) {
                 // R14: a partial-coverage fragment not behind the centre's surface and
                 // of another shading id blends over it
@@ -2022,7 +2042,7 @@ void render_views_kernel(const RenderParams P_)
                                                       __HIP_MEMORY_SCOPE_AGENT);
                 if (ko != 0xFFFFFFFFu && (ko >> 16) <= (key >> 16) && ((ko >> 8) & 255u) != (key & 255u)) {
                     uint32_t o3[3];
-                    shade_rgb(P, ((ko >> 16) << 16) | ((ko >> 8) & 255u), o3);
+                    shade(((ko >> 16) << 16) | ((ko >> 8) & 255u), o3);
                     const uint32_t a8 = 255u - (ko & 255u);
 #pragma unroll
                     for (int c = 0; c < 3; ++c) c3[c] = (o3[c] * a8 + c3[c] * (255u - a8) + 127u) / 255u;
