@@ -2029,10 +2029,8 @@ void render_views_kernel(const RenderParams P_)
                 shade_rgb(P, key, c3);
             }
         };
-        uint8_t* const rgb = P.out_rgb + v * 3 * view_px;
-        for (int p = tid; p < npx; p += kThreads) {
-            const int row = p / T.w, col = p % T.w;
-            const uint32_t key = S.fb[row * T.pitch + col];
+        // colour of tile pixel (row, col) with key `key`, packed r | g << 8 | b << 16
+        auto pixel = [&](int row, int col, uint32_t key) -> uint32_t {
             uint32_t c3[3];
             shade(key, c3);
             if constexpr (kAA) {
@@ -2048,10 +2046,37 @@ void render_views_kernel(const RenderParams P_)
                     for (int c = 0; c < 3; ++c) c3[c] = (o3[c] * a8 + c3[c] * (255u - a8) + 127u) / 255u;
                 }
             }
-            const int64_t o = (int64_t)(T.y0 + row) * P.W + T.x0 + col;
-            rgb[o] = (uint8_t)c3[0];
-            rgb[view_px + o] = (uint8_t)c3[1];
-            rgb[2 * view_px + o] = (uint8_t)c3[2];
+            return c3[0] | c3[1] << 8 | c3[2] << 16;
+        };
+        uint8_t* const rgb = P.out_rgb + v * 3 * view_px;
+        if ((reinterpret_cast<uintptr_t>(P.out_rgb) & 3u) == 0 && (P.W % 4) == 0 && (T.w % 4) == 0 && (T.x0 % 4) == 0) {
+            // four pixels of a row per thread, one 32-bit store per channel plane
+            // (u / u4 = (u * ceil(2^16 / u4)) >> 16 exactly for u * u4 < 2^16: u < 1024, u4 <= 16)
+            const int u4 = T.w >> 2, n4 = u4 * T.h;
+            const uint32_t r4 = (65535u + (uint32_t)u4) / (uint32_t)u4;
+            for (int u = tid; u < n4; u += kThreads) {
+                const int row = (int)(((uint32_t)u * r4) >> 16), c4 = u - row * u4;
+                const u32x4 kq = *(const u32x4*)&S.fb[row * T.pitch + 4 * c4];
+                const uint32_t q0 = pixel(row, 4 * c4, kq.x), q1 = pixel(row, 4 * c4 + 1, kq.y);
+                const uint32_t q2 = pixel(row, 4 * c4 + 2, kq.z), q3 = pixel(row, 4 * c4 + 3, kq.w);
+                const int64_t o = (int64_t)(T.y0 + row) * P.W + T.x0 + 4 * c4;
+#pragma unroll
+                for (int c = 0; c < 3; ++c) {
+                    const uint32_t sh = 8u * (uint32_t)c;
+                    const uint32_t w = ((q0 >> sh) & 255u) | ((q1 >> sh) & 255u) << 8 | ((q2 >> sh) & 255u) << 16 |
+                                       ((q3 >> sh) & 255u) << 24;
+                    *(uint32_t*)(rgb + c * view_px + o) = w;
+                }
+            }
+        } else {
+            for (int p = tid; p < npx; p += kThreads) {
+                const int row = p / T.w, col = p % T.w;
+                const uint32_t q = pixel(row, col, S.fb[row * T.pitch + col]);
+                const int64_t o = (int64_t)(T.y0 + row) * P.W + T.x0 + col;
+                rgb[o] = (uint8_t)q;
+                rgb[view_px + o] = (uint8_t)(q >> 8);
+                rgb[2 * view_px + o] = (uint8_t)(q >> 16);
+            }
         }
     };
     if constexpr (kAA) {

@@ -75,3 +75,29 @@ def test_rgb_town_paper_rig_and_tiles(lib):
     views = np.sort(np.random.default_rng(52).choice(wl.num_views, size=64, replace=False))
     check(lib, wl, views, "rgb-town")
     check(lib, wl, views, "rgb-town-tile24", tile=24)
+
+
+@pytest.mark.parametrize("aa", [False, True], ids=["one-sample", "antialiased"])
+def test_rgb_unaligned_output_matches_aligned(lib, aa):
+    """An output colour image that starts at an odd byte address takes the
+    per-pixel byte stores; its bytes equal those of a word-aligned image."""
+    torch = _torch()
+    wl = workload(1)
+    r = lib.Renderer(0)
+    try:
+        r.upload(wl.scene, wl.cell_size)
+        da = lib.DeviceAgents.from_host(wl.agents)
+        c0, d0, rgb0 = r.render_rgb(da, wl.rig, antialias=aa)
+        n = rgb0.numel()
+        buf = torch.full((n + 1,), 7, dtype=torch.uint8, device="cuda")
+        out = buf[1:].view(rgb0.shape)
+        assert out.data_ptr() % 4 == 1
+        c1, d1 = torch.empty_like(c0), torch.empty_like(d0)
+        fn = lib.pictura_render_rgb_aa if aa else lib.pictura_render_rgb
+        fn(r.ctx, da, wl.rig, c1, d1, out)
+        torch.cuda.synchronize()
+        assert int(buf[0]) == 7
+        assert torch.equal(out, rgb0)
+        assert torch.equal(c1, c0) and torch.equal(d1, d0)
+    finally:
+        r.close_checked()
