@@ -43,7 +43,7 @@ HBM_PEAK_GBS = 8000.0   # MI355X HBM3E peak
 # `traffic` is reported as null.
 TRAFFIC = {
     "config": 4,
-    "sources_sha256": "5c8b9a186460826370996f360db5f8d965d372f4502bf879b6ff7b5c417818e3",
+    "sources_sha256": "b365db6709027bbf7010090a3706b14f9039c6331ec9481572806ae8b1599569",
     "fetch_bytes": 1.1539e9,
     "write_bytes": 5368709120,
 }

@@ -7,6 +7,14 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(os.path.dirname(HERE), "include")
 LIB = os.path.join(HERE, "libpictura.so")
 SOURCES = ["pictura_binner.hip", "pictura_render.hip", "pictura_abi.hip"]
+# (source, object name, extra flags): the render source is compiled twice; the
+# second object holds only the production class/depth kernel, scheduled by
+# LLVM's iterative ILP strategy (1.4 % faster on that kernel in A/B runs with
+# identical images; the antialiased kernel spills and slows under it)
+UNITS = [(src, src.replace(".hip", ".o"), []) for src in SOURCES] + [
+    ("pictura_render.hip", "pictura_render_plain.o",
+     ["-DPICTURA_RENDER_PLAIN", "-mllvm", "-amdgpu-sched-strategy=iterative-ilp"]),
+]
 
 # fp32 rules need IEEE arithmetic: no contraction, correctly rounded division,
 # denormals kept.  Packed fp32 instructions are disabled.
@@ -23,9 +31,9 @@ def build(verbose: bool = False) -> str:
     hipcc = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
     objs = []
     procs = []
-    for src in SOURCES:
-        obj = os.path.join(CSRC, src.replace(".hip", ".o"))
-        cmd = [hipcc, *HIPCC_FLAGS, "-I", INCLUDE, "-c", os.path.join(CSRC, src), "-o", obj]
+    for src, oname, extra in UNITS:
+        obj = os.path.join(CSRC, oname)
+        cmd = [hipcc, *HIPCC_FLAGS, *extra, "-I", INCLUDE, "-c", os.path.join(CSRC, src), "-o", obj]
         if verbose:
             print(" ".join(cmd))
         procs.append(subprocess.Popen(cmd))

@@ -2146,6 +2146,15 @@ void render_views_kernel(const RenderParams P_)
     }
 }
 
+#ifdef PICTURA_RENDER_PLAIN
+// This object (the source compiled a second time, with its own scheduler
+// setting) holds only the production class/depth kernel.
+hipError_t launch_render_plain(const RenderParams& p, hipStream_t s)
+{
+    hipLaunchKernelGGL((render_views_kernel<0, false>), dim3((unsigned)p.num_blocks), dim3(kThreads), 0, s, p);
+    return hipGetLastError();
+}
+#else
 hipError_t launch_render(const RenderParams& p, hipStream_t s)
 {
     if (p.num_blocks <= 0) return hipSuccess;
@@ -2160,7 +2169,7 @@ hipError_t launch_render(const RenderParams& p, hipStream_t s)
         if (mode == 1) hipLaunchKernelGGL((render_views_kernel<1, false>), grid, block, 0, s, p);
         else if (mode == 2) hipLaunchKernelGGL((render_views_kernel<2, false>), grid, block, 0, s, p);
         else if (mode == 3) hipLaunchKernelGGL((render_views_kernel<3, false>), grid, block, 0, s, p);
-        else hipLaunchKernelGGL((render_views_kernel<0, false>), grid, block, 0, s, p);
+        else return launch_render_plain(p, s);
     }
     return hipGetLastError();
 }
@@ -2246,5 +2255,7 @@ hipError_t launch_rcp_check_noalloc(uint32_t lo_bits, uint32_t n, unsigned long 
     if (e != hipSuccess) return e;
     return launch_rcp_check(lo_bits, n, counter, s);
 }
+
+#endif  // PICTURA_RENDER_PLAIN
 
 }  // namespace pictura
