@@ -43,7 +43,7 @@ HBM_PEAK_GBS = 8000.0   # MI355X HBM3E peak
 # `traffic` is reported as null.
 TRAFFIC = {
     "config": 4,
-    "sources_sha256": "b365db6709027bbf7010090a3706b14f9039c6331ec9481572806ae8b1599569",
+    "sources_sha256": "c911ef398f1011ae696b13627e8ca7047fae997b22968d0bc4fdac4396910552",
     "fetch_bytes": 1.1539e9,
     "write_bytes": 5368709120,
 }

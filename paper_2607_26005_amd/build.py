@@ -7,13 +7,17 @@ CSRC = os.path.join(HERE, "csrc")
 INCLUDE = os.path.join(os.path.dirname(HERE), "include")
 LIB = os.path.join(HERE, "libpictura.so")
 SOURCES = ["pictura_binner.hip", "pictura_render.hip", "pictura_abi.hip"]
-# (source, object name, extra flags): the render source is compiled twice; the
-# second object holds only the production class/depth kernel, scheduled by
+# (source, object name, extra flags): the render source is compiled three
+# times.  One object holds only the production class/depth kernel, scheduled by
 # LLVM's iterative ILP strategy (1.4 % faster on that kernel in A/B runs with
-# identical images; the antialiased kernel spills and slows under it)
+# identical images), one the production instance and one-sample colour kernels
+# under the AMDGPU register trackers (about 1 % faster each); the antialiased
+# kernel spills and slows under either, so it keeps the default scheduler.
 UNITS = [(src, src.replace(".hip", ".o"), []) for src in SOURCES] + [
     ("pictura_render.hip", "pictura_render_plain.o",
      ["-DPICTURA_RENDER_PLAIN", "-mllvm", "-amdgpu-sched-strategy=iterative-ilp"]),
+    ("pictura_render.hip", "pictura_render_side.o",
+     ["-DPICTURA_RENDER_SIDE", "-mllvm", "-amdgpu-use-amdgpu-trackers=1"]),
 ]
 
 # fp32 rules need IEEE arithmetic: no contraction, correctly rounded division,

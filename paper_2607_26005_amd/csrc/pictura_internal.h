@@ -144,8 +144,11 @@ struct BinWork {
 constexpr uint32_t kPrimFlagPair = 0x80000000u;
 
 hipError_t launch_render(const RenderParams& p, hipStream_t s);
-// the production class/depth kernel alone (its own object, built with its own scheduler setting)
+// the production class/depth kernel alone, and the production instance (1) and
+// one-sample colour (3) kernels: objects of their own, each built with its own
+// scheduler setting
 hipError_t launch_render_plain(const RenderParams& p, hipStream_t s);
+hipError_t launch_render_side(const RenderParams& p, int mode, hipStream_t s);
 hipError_t launch_bin(const BinWork& w, hipStream_t s);
 hipError_t launch_agents_step(const AgentStepParams& p, hipStream_t s);
 hipError_t launch_store_probe(void* dst, uint64_t bytes, hipStream_t s);

@@ -2146,12 +2146,20 @@ void render_views_kernel(const RenderParams P_)
     }
 }
 
-#ifdef PICTURA_RENDER_PLAIN
-// This object (the source compiled a second time, with its own scheduler
-// setting) holds only the production class/depth kernel.
+#if defined(PICTURA_RENDER_PLAIN)
+// This object (the source compiled once more, with its own scheduler setting)
+// holds only the production class/depth kernel.
 hipError_t launch_render_plain(const RenderParams& p, hipStream_t s)
 {
     hipLaunchKernelGGL((render_views_kernel<0, false>), dim3((unsigned)p.num_blocks), dim3(kThreads), 0, s, p);
+    return hipGetLastError();
+}
+#elif defined(PICTURA_RENDER_SIDE)
+// Likewise for the production instance (mode 1) and one-sample colour (mode 3) kernels.
+hipError_t launch_render_side(const RenderParams& p, int mode, hipStream_t s)
+{
+    if (mode == 1) hipLaunchKernelGGL((render_views_kernel<1, false>), dim3((unsigned)p.num_blocks), dim3(kThreads), 0, s, p);
+    else hipLaunchKernelGGL((render_views_kernel<3, false>), dim3((unsigned)p.num_blocks), dim3(kThreads), 0, s, p);
     return hipGetLastError();
 }
 #else
@@ -2166,9 +2174,8 @@ hipError_t launch_render(const RenderParams& p, hipStream_t s)
         else if (mode == 3) hipLaunchKernelGGL((render_views_kernel<3, true>), grid, block, 0, s, p);
         else hipLaunchKernelGGL((render_views_kernel<0, true>), grid, block, 0, s, p);
     } else {
-        if (mode == 1) hipLaunchKernelGGL((render_views_kernel<1, false>), grid, block, 0, s, p);
-        else if (mode == 2) hipLaunchKernelGGL((render_views_kernel<2, false>), grid, block, 0, s, p);
-        else if (mode == 3) hipLaunchKernelGGL((render_views_kernel<3, false>), grid, block, 0, s, p);
+        if (mode == 2) hipLaunchKernelGGL((render_views_kernel<2, false>), grid, block, 0, s, p);
+        else if (mode != 0) return launch_render_side(p, mode, s);
         else return launch_render_plain(p, s);
     }
     return hipGetLastError();
@@ -2256,6 +2263,6 @@ hipError_t launch_rcp_check_noalloc(uint32_t lo_bits, uint32_t n, unsigned long 
     return launch_rcp_check(lo_bits, n, counter, s);
 }
 
-#endif  // PICTURA_RENDER_PLAIN
+#endif  // PICTURA_RENDER_PLAIN, PICTURA_RENDER_SIDE
 
 }  // namespace pictura
