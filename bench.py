@@ -43,7 +43,7 @@ HBM_PEAK_GBS = 8000.0   # MI355X HBM3E peak
 # `traffic` is reported as null.
 TRAFFIC = {
     "config": 4,
-    "sources_sha256": "c911ef398f1011ae696b13627e8ca7047fae997b22968d0bc4fdac4396910552",
+    "sources_sha256": "91e3381bd540296f5a92edbcebe44807d89bac67831a1a78c94be114ea00102a",
     "fetch_bytes": 1.1539e9,
     "write_bytes": 5368709120,
 }

@@ -513,15 +513,29 @@ __device__ __forceinline__ void first_pass_prim(const RenderParams& P, const Til
 // raster
 // ---------------------------------------------------------------------------
 
+// R7 key (Q24 << 8) | cls for 1/z = iz >= 1/far > 0, Q24 = (bits(IZCAP) >> 3) -
+// (bits(min(iz, IZCAP)) >> 3).  Positive floats order like their bit patterns,
+// and IZCAP is a power of two (low bits zero), so min(bits, bits(IZCAP)) >> 3 =
+// min(bits >> 3, qbase): the clamp is a saturating subtract, one instruction.
+// The class/depth kernel keeps the explicit minimum (the same key), with which
+// its schedule ran faster.
+__device__ __forceinline__ uint32_t depth_key(const RenderParams& P, float iz, uint32_t cls)
+{
+#ifdef PICTURA_RENDER_PLAIN
+    const uint32_t bits = min(__float_as_uint(iz), __float_as_uint(P.izcap));
+    return ((P.qbase - (bits >> 3)) << 8) | cls;
+#else
+    return (__builtin_elementwise_sub_sat(P.qbase, __float_as_uint(iz) >> 3) << 8) | cls;
+#endif
+}
+
 // R7: key of a covered pixel, or 0xFFFFFFFF (no effect on the minimum) when
-// the depth test rejects it.  iz >= 1/far > 0 makes the bit patterns of iz
-// and IZCAP order like the values, so min() may run on the bits.
+// the depth test rejects it.
 __device__ __forceinline__ uint32_t pixel_key(const RenderParams& P, float pxf, float pyf, float pa, float pb,
                                               float pc, uint32_t cls)
 {
     const float iz = fmaf(pa, pxf, fmaf(pb, pyf, pc));
-    const uint32_t bits = min(__float_as_uint(iz), __float_as_uint(P.izcap));
-    const uint32_t key = ((P.qbase - (bits >> 3)) << 8) | cls;
+    const uint32_t key = depth_key(P, iz, cls);
     return iz >= P.izfar ? key : 0xFFFFFFFFu;
 }
 
@@ -568,8 +582,7 @@ __device__ __forceinline__ void raster_lane(const RenderParams& P, Shared& S, co
         for (int i = i0; i <= i1; ++i) {
             if constexpr (!Exact) pxf = ((float)i + 0.5f) - P.cx;
             const float iz = fmaf(pa, pxf, inner);
-            const uint32_t bits = min(__float_as_uint(iz), __float_as_uint(P.izcap));
-            const uint32_t key = ((P.qbase - (bits >> 3)) << 8) | kcls;
+            const uint32_t key = depth_key(P, iz, kcls);
             if (((g0 | g1 | g2) >= 0) & (iz >= P.izfar)) atomicMin(&row[i], key);
             g0 += sx0; g1 += sx1; g2 += sx2;
             if constexpr (Exact) pxf += 1.0f;
@@ -628,8 +641,7 @@ __device__ __forceinline__ void raster_packed(const RenderParams& P, Shared& S, 
         const float tpb = __uint_as_float(bperm(t, __float_as_uint(pb)));
         const float tpc = __uint_as_float(bperm(t, __float_as_uint(pc)));
         const float iz = fmaf(tpa, pxf, fmaf(tpb, pyf, tpc));
-        const uint32_t bits = min(__float_as_uint(iz), __float_as_uint(P.izcap));
-        const uint32_t key = ((P.qbase - (bits >> 3)) << 8) | (g >> 24);
+        const uint32_t key = depth_key(P, iz, (g >> 24));
         // p in range keeps the address inside the tile whatever the owner
         // search found; other lanes take word `lane` (distinct banks) and the
         // key 0xFFFFFFFF, which changes nothing, so the LDS minimum needs no
@@ -731,8 +743,7 @@ __device__ __forceinline__ void raster_blocks(const RenderParams& P, Shared& S, 
             const float pxf = pxl + __uint_as_float(gx);
             const float pyf = pyl + __uint_as_float(gy);
             const float iz = fmaf(pa, pxf, fmaf(pb, pyf, pc));
-            const uint32_t bits = min(__float_as_uint(iz), __float_as_uint(P.izcap));
-            const uint32_t key = ((P.qbase - (bits >> 3)) << 8) | cls;
+            const uint32_t key = depth_key(P, iz, cls);
             addr = ga + (uint32_t)loff4;
             return (((e0 | e1 | e2) >= 0) && iz >= P.izfar) ? key : 0xFFFFFFFFu;
         }
@@ -760,8 +771,7 @@ __device__ __forceinline__ void raster_blocks(const RenderParams& P, Shared& S, 
             pyf = ((float)(T.y0 + bY + ly) + 0.5f) - P.cy;
         }
         const float iz = fmaf(pa, pxf, fmaf(pb, pyf, pc));
-        const uint32_t bits = min(__float_as_uint(iz), __float_as_uint(P.izcap));
-        const uint32_t key = ((P.qbase - (bits >> 3)) << 8) | cls;
+        const uint32_t key = depth_key(P, iz, cls);
         addr = (uint32_t)((bY * T.pitch + bX) * 4 + loff4);
         return (cov && iz >= P.izfar) ? key : 0xFFFFFFFFu;
     };
