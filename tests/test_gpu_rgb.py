@@ -101,3 +101,24 @@ def test_rgb_unaligned_output_matches_aligned(lib, aa):
         assert torch.equal(c1, c0) and torch.equal(d1, d0)
     finally:
         r.close_checked()
+
+
+def test_rgb_headline_full_launch_sampled(lib):
+    # the benchmark's one-sample colour launch: 1024 worlds x 64 agents x 4
+    # cameras, every view rendered, 64 sampled across the worlds
+    wl = workload(4)
+    views = np.sort(np.random.default_rng(53).choice(wl.num_views, size=64, replace=False))
+    assert len(np.unique(views // 256)) > 48
+    assert check(lib, wl, views, "rgb-headline") > 0
+
+
+def test_rgb_ragged_sizes(lib):
+    # 40 x 24 and 96 x 54 (two tiles of 48) take the four-pixel colour
+    # stores; 100 x 70 (tiles 50 wide) and 17 x 129 the per-byte ones
+    wl = workload(2, 1)
+    for (W, H) in ((40, 24), (100, 70), (17, 129), (96, 54)):
+        rig = sg.Rig(width=W, height=H, fx=W / 2.0, fy=W / 2.0, cx=W / 2.0, cy=H / 2.0, near=0.5, far=100.0,
+                     mount=wl.rig.mount)
+        wl2 = sg.Workload(wl.name, 2, 1, wl.scene, wl.agents, rig, wl.cell_size, wl.world_size)
+        views = np.sort(np.random.default_rng(W + 1).choice(wl2.num_views, size=32, replace=False))
+        check(lib, wl2, views, f"rgb-ragged {W}x{H}")
