@@ -190,6 +190,29 @@ def test_ragged_sizes_and_tiles(lib):
         check_views(lib, wl2, sample_views(wl2.num_views, 64, W), f"ragged {W}x{H}")
 
 
+def test_largest_view_full_image(lib):
+    # the largest view the ABI accepts, 4096 x 4096 (4,096 tiles of 64 x 64),
+    # on the tiny workload's scene: two whole images against the oracle
+    wl = workload(1)
+    rig = sg.Rig(width=4096, height=4096, fx=2048.0, fy=2048.0, cx=2048.0, cy=2048.0, near=0.5, far=100.0,
+                 mount=wl.rig.mount)
+    wl2 = sg.Workload(wl.name, 1, 0, wl.scene, wl.agents, rig, wl.cell_size, wl.world_size)
+    check_views(lib, wl2, [0, 5], "largest 4096x4096")
+
+
+def test_eight_cameras(lib):
+    # the most cameras a rig may have: eight at 45 degree steps (cos and sin of
+    # the odd steps rounded to fp32), with mount offsets and heights
+    wl = workload(2, 1)
+    c45 = float(np.float32(np.sqrt(0.5)))
+    dirs = ((1.0, 0.0), (c45, c45), (0.0, 1.0), (-c45, c45), (-1.0, 0.0), (-c45, -c45), (0.0, -1.0), (c45, -c45))
+    mounts = tuple((0.4 * cy, -0.3 * sy, 1.2 + 0.1 * k, cy, sy) for k, (cy, sy) in enumerate(dirs))
+    rig = make_rig(res=64, far=100.0, mounts=mounts)
+    wl2 = sg.Workload(wl.name, 2, 1, wl.scene, wl.agents, rig, wl.cell_size, wl.world_size)
+    assert wl2.num_views == 8 * 32
+    check_views(lib, wl2, sample_views(wl2.num_views, 64, 88), "eight cameras")
+
+
 def test_random_quad_pairs(lib):
     # quads given as pairs (a, b, c), (a, c, d): convex, darts, slivers, near-plane
     # crossings and quads reaching far to the side, seen by four cameras
