@@ -206,3 +206,12 @@ def test_aa_leaves_classes_and_depth_alone(lib):
     c0, d0, _ = gpu_render(lib, wl.scene, wl.cell_size, wl.agents, wl.rig, antialias=False)
     assert np.array_equal(c1.cpu().numpy(), c0.cpu().numpy())
     assert np.array_equal(d1.cpu().numpy().view(np.uint32), d0.cpu().numpy().view(np.uint32))
+
+
+def test_aa_largest_view(lib):
+    # the edge buffer of a 4096 x 4096 view (4,096 tiles), two whole images
+    wl = workload(1)
+    rig = sg.Rig(width=4096, height=4096, fx=2048.0, fy=2048.0, cx=2048.0, cy=2048.0, near=0.5, far=100.0,
+                 mount=wl.rig.mount)
+    wl2 = sg.Workload(wl.name, 1, 0, wl.scene, wl.agents, rig, wl.cell_size, wl.world_size)
+    assert check(lib, wl2, [0, 5], "aa-largest") > 0

@@ -140,3 +140,13 @@ def test_instances_faces_behind_near_or_beyond_far(lib):
     ora = O.render(scene, ag, rig, want_instances=True)
     assert ora["counts"][0, 1, 0] > 0 and ora["counts"][0, 2, 0] > 0   # cars 1 and 2 are seen
     assert (ora["counts"][:, 3, 0] == 0).all()                         # car 3 never is
+
+
+def test_instances_largest_view(lib):
+    # owners and counts on the largest view the ABI accepts, 4096 x 4096
+    # (4,096 tiles per view), two whole images against the oracle
+    wl = workload(1)
+    rig = sg.Rig(width=4096, height=4096, fx=2048.0, fy=2048.0, cx=2048.0, cy=2048.0, near=0.5, far=100.0,
+                 mount=wl.rig.mount)
+    wl2 = sg.Workload(wl.name, 1, 0, wl.scene, wl.agents, rig, wl.cell_size, wl.world_size)
+    assert check(lib, wl2, [0, 5], "inst-largest") > 0
