@@ -306,7 +306,7 @@ pictura_status pictura_bins_info(pictura_ctx ctx, int32_t* dims, int64_t* cell_b
 pictura_status pictura_bins_copy(pictura_ctx ctx, uint32_t* cell_start, float* cell_aabb, uint32_t* perm);
 
 #define PICTURA_OPT_CULL   1 /* 1 (default): cell + triangle frustum culling; 0: every triangle of the world */
-#define PICTURA_OPT_TILE   2 /* 0 (default): 64x64 LDS tiles; n in 8..64: force n x n tiles (antialiased colour: at most 32 columns wide) */
+#define PICTURA_OPT_TILE   2 /* 0 (default): tiles of at most 64x64, split evenly over the view; n in 8..64: force n x n tiles (the last row and column ragged) */
 #define PICTURA_OPT_STATS  3 /* 1: count the render kernel's work (cells, triangles, pixels); 0 (default): off */
 /* Set a context option.  Images never depend on any option. */
 pictura_status pictura_set_option(pictura_ctx ctx, int32_t option, int32_t value);

@@ -117,7 +117,7 @@ def test_aa_town_paper_rig_tiles_and_unculled(lib):
     views = np.sort(np.random.default_rng(62).choice(wl.num_views, size=64, replace=False))
     assert check(lib, wl, views, "aa-town") > 0
     check(lib, wl, views, "aa-town-tile24", tile=24)
-    check(lib, wl, views[:32], "aa-town-tile48", tile=48)   # capped at 32 columns: 32 x 48 tiles
+    check(lib, wl, views[:32], "aa-town-tile48", tile=48)   # two 48 x 48 tiles and ragged ones per view
     check(lib, wl, views[:16], "aa-town-unculled", cull=0)
 
 

@@ -78,7 +78,7 @@ def test_instances_tiled_and_unculled(lib):
     rng = np.random.default_rng(42)
     views = np.sort(rng.choice(wl.num_views, size=48, replace=False))
     check(lib, wl, views, "inst-tiles16", tile=16)
-    check(lib, wl, views, "inst-tiles48", tile=48)   # capped at 32 columns: 32 x 48 tiles
+    check(lib, wl, views, "inst-tiles48", tile=48)   # 48 x 48 tiles and ragged 16-wide ones
     check(lib, wl, views, "inst-nocull", cull=0)
 
 
