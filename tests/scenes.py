@@ -34,3 +34,16 @@ def make_rig(res=64, near=0.5, far=100.0, mounts=((0.0, 0.0, 0.0, 1.0, 0.0),), f
 
 def quad(p0, p1, p2, p3):
     return [[p0, p1, p2], [p0, p2, p3]]
+
+
+def walled(scene, height=12.0, inset=80.0, reach=95.0, cls=7):
+    """The one-world scene with four walls of the given height added around
+    its centre (square of half-side `inset`), reaching above any camera."""
+    walls = []
+    for (a, b) in (((inset, -reach), (inset, reach)), ((-inset, reach), (-inset, -reach)),
+                   ((-reach, inset), (reach, inset)), ((reach, -inset), (-reach, -inset))):
+        walls += quad((a[0], a[1], 0.0), (b[0], b[1], 0.0), (b[0], b[1], height), (a[0], a[1], height))
+    verts = np.concatenate([scene.verts, np.asarray(walls, np.float32).reshape(-1, 9)])
+    c = np.concatenate([scene.cls, np.full(len(walls), cls, np.uint8)])
+    return Scene(num_worlds=1, verts=np.ascontiguousarray(verts), cls=c,
+                 tri_offsets=np.asarray([0, len(verts)], np.int64), bounds=scene.bounds)

@@ -149,6 +149,20 @@ def test_aa_ragged_sizes(lib):
         check(lib, wl2, views, f"aa-ragged {W}x{H}")
 
 
+def test_aa_tiles_above_the_horizon(lib):
+    # fragments along the horizon and above it: a flat world and the same world
+    # with walls reaching above the cameras, 128 x 128 views in four tiles and
+    # in forced 16-pixel tiles
+    from tests.scenes import walled
+    wl = workload(1)
+    rig = sg.Rig(width=128, height=128, fx=64.0, fy=64.0, cx=64.0, cy=64.0, near=0.5, far=100.0,
+                 mount=wl.rig.mount)
+    for name, scene in (("flat", wl.scene), ("walled", walled(wl.scene))):
+        wl2 = sg.Workload(wl.name, 1, 0, scene, wl.agents, rig, wl.cell_size, wl.world_size)
+        check(lib, wl2, np.arange(wl2.num_views), f"aa-horizon {name}")
+        check(lib, wl2, np.arange(wl2.num_views), f"aa-horizon {name} tile16", tile=16)
+
+
 def _random_quads(seed, n=400):
     """A soup of quads given as pairs (a, b, c), (a, c, d): convex ones, darts
     (one vertex pulled past the diagonal), slivers a few millimetres wide, and

@@ -15,7 +15,7 @@ import pytest
 from oracle import oracle as O
 from paper_2607_26005_amd import scenegen as sg
 from tests.parity import assert_parity, compare
-from tests.scenes import make_agents, make_rig, make_scene, quad
+from tests.scenes import make_agents, make_rig, make_scene, quad, walled
 
 pytestmark = pytest.mark.gpu
 
@@ -211,6 +211,19 @@ def test_eight_cameras(lib):
     wl2 = sg.Workload(wl.name, 2, 1, wl.scene, wl.agents, rig, wl.cell_size, wl.world_size)
     assert wl2.num_views == 8 * 32
     check_views(lib, wl2, sample_views(wl2.num_views, 64, 88), "eight cameras")
+
+
+def test_tiles_above_the_horizon(lib):
+    # tiles whose pixel centres all lie above the horizon: the tiny workload's
+    # flat world (sky there) and the same world with walls reaching above the
+    # cameras, 128 x 128 views in four tiles and in forced 16-pixel tiles
+    wl = workload(1)
+    rig = sg.Rig(width=128, height=128, fx=64.0, fy=64.0, cx=64.0, cy=64.0, near=0.5, far=100.0,
+                 mount=wl.rig.mount)
+    for name, scene in (("flat", wl.scene), ("walled", walled(wl.scene))):
+        wl2 = sg.Workload(wl.name, 1, 0, scene, wl.agents, rig, wl.cell_size, wl.world_size)
+        check_views(lib, wl2, np.arange(wl2.num_views), f"horizon {name}")
+        check_views(lib, wl2, np.arange(wl2.num_views), f"horizon {name} tile16", tile=16)
 
 
 def test_random_quad_pairs(lib):
