@@ -16,15 +16,17 @@
 //     box) go through a first pass 64 at a time: view transform, the near/far
 //     rule and a conservative test that the snapped triangle can hold a pixel
 //     centre of the tile; survivors are appended to the wave's LDS queue;
-//  3. every 64 survivors go through the exact pass, one lane per triangle:
-//     near clipping, 8-bit subpixel snap, orientation, depth plane.  A
-//     triangle whose bounding box has at most kSmallPx pixels is rasterized
-//     by its own lane.  For the others the lane computes a raster record
-//     (exact edge functions at the tile origin, box, depth plane) that the
-//     wave then reads lane by lane into scalar registers: every lane tests
-//     one 8x8 pixel block of the record's bounding box against its three
-//     edges, and the passing blocks are rasterized one per step, lane l
-//     handling pixel (l & 7, l >> 3) of the block;
+//  3. every 64 survivors go through the exact pass, one lane per primitive (a
+//     triangle, or a pair of triangles sharing a diagonal, set up once and
+//     drawn as two fan pieces): near clipping, 8-bit subpixel snap,
+//     orientation, depth planes.  The bounding-box pixels of all pieces with
+//     at most kSmallPx of them are numbered across the lanes and handed out
+//     64 per step (the packed raster).  For a larger piece the lane computes a
+//     raster record (exact edge functions at the tile origin, box, depth
+//     plane) and hands it to the view's record ring, which both waves drain:
+//     every lane tests one 8x8 pixel block of the record's bounding box
+//     against its three edges, and the passing blocks are rasterized one per
+//     step, lane l handling pixel (l & 7, l >> 3) of the block;
 //  4. visibility is an LDS atomicMin of (24-bit depth | 8-bit class), so the
 //     order in which lanes and waves finish does not matter;
 //  5. the tile is resolved and written with 16-byte non-temporal stores.
