@@ -43,7 +43,7 @@ HBM_PEAK_GBS = 8000.0   # MI355X HBM3E peak
 # `traffic` is reported as null.
 TRAFFIC = {
     "config": 4,
-    "sources_sha256": "7bbfcce068b2df7fd8506d3ba43c126af1deb9270af189b330b160e0b0676597",
+    "sources_sha256": "70784fc6d63c0456b54ca06404b1fb82238dc01b03cc80e1a7b68650005ba66e",
     "fetch_bytes": 1.1539e9,
     "write_bytes": 5368709120,
 }

@@ -2031,34 +2031,34 @@ void render_views_kernel(const RenderParams P_)
             pal0[lane] = t3[0] | t3[1] << 8 | t3[2] << 16;
         }
         __builtin_amdgcn_wave_barrier();
-        auto shade = [&](uint32_t key, uint32_t* c3) {
-            if (((key >> 4) & 7u) == 0u) {
-                const uint32_t w = pal0[key & 15u];
-                c3[0] = w & 255u;
-                c3[1] = (w >> 8) & 255u;
-                c3[2] = w >> 16;
-            } else {
-                shade_rgb(P, key, c3);
-            }
-        };
-        // colour of tile pixel (row, col) with key `key`, packed r | g << 8 | b << 16
-        auto pixel = [&](int row, int col, uint32_t key) -> uint32_t {
+        // colour of a key, packed r | g << 8 | b << 16
+        auto shade = [&](uint32_t key) -> uint32_t {
+            if (((key >> 4) & 7u) == 0u) return pal0[key & 15u];
             uint32_t c3[3];
-            shade(key, c3);
+            shade_rgb(P, key, c3);
+            return c3[0] | c3[1] << 8 | c3[2] << 16;
+        };
+        // colour of tile pixel (row, col) with key `key`, packed
+        auto pixel = [&](int row, int col, uint32_t key) -> uint32_t {
+            uint32_t q = shade(key);
             if constexpr (kAA) {
                 // R14: a partial-coverage fragment not behind the centre's surface and
                 // of another shading id blends over it
                 const uint32_t ko = __hip_atomic_load(&ebuf[(int64_t)row * P.W + col], __ATOMIC_RELAXED,
                                                       __HIP_MEMORY_SCOPE_AGENT);
                 if (ko != 0xFFFFFFFFu && (ko >> 16) <= (key >> 16) && ((ko >> 8) & 255u) != (key & 255u)) {
-                    uint32_t o3[3];
-                    shade(((ko >> 16) << 16) | ((ko >> 8) & 255u), o3);
+                    const uint32_t o = shade(((ko >> 16) << 16) | ((ko >> 8) & 255u));
                     const uint32_t a8 = 255u - (ko & 255u);
+                    uint32_t b = 0;
 #pragma unroll
-                    for (int c = 0; c < 3; ++c) c3[c] = (o3[c] * a8 + c3[c] * (255u - a8) + 127u) / 255u;
+                    for (int c = 0; c < 3; ++c) {
+                        const uint32_t oc = (o >> (8 * c)) & 255u, cc = (q >> (8 * c)) & 255u;
+                        b |= ((oc * a8 + cc * (255u - a8) + 127u) / 255u) << (8 * c);
+                    }
+                    q = b;
                 }
             }
-            return c3[0] | c3[1] << 8 | c3[2] << 16;
+            return q;
         };
         uint8_t* const rgb = P.out_rgb + v * 3 * view_px;
         if ((reinterpret_cast<uintptr_t>(P.out_rgb) & 3u) == 0 && (P.W % 4) == 0 && (T.w % 4) == 0 && (T.x0 % 4) == 0) {
