@@ -43,7 +43,7 @@ HBM_PEAK_GBS = 8000.0   # MI355X HBM3E peak
 # `traffic` is reported as null.
 TRAFFIC = {
     "config": 4,
-    "sources_sha256": "70784fc6d63c0456b54ca06404b1fb82238dc01b03cc80e1a7b68650005ba66e",
+    "sources_sha256": "670fa42ee2425bb88645c67e5598a566d03114d306e4ca58b6f963e3b6f22b11",
     "fetch_bytes": 1.1539e9,
     "write_bytes": 5368709120,
 }

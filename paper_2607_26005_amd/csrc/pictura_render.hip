@@ -1432,33 +1432,46 @@ __device__ __forceinline__ uint32_t div31(uint32_t n, Div31 d) { return d.m ? (_
 // face = sid >> 4 (0: not a box face).  v = base[class] * (face factor * b),
 // b = 1 - 0.6 min(z / far, 1) on box faces (depth-aware brightness, z the
 // decoded depth of R8), 1 elsewhere; byte = rint(255 min(v, 1)).
+__device__ __forceinline__ float decode_depth(const RenderParams& P, uint32_t key)
+{
+    const float d = __uint_as_float(((P.qbase - (key >> 8)) << 3) | 4u);
+    return P.fast_decode ? rcp_rn(d) : 1.0f / d;
+}
+
+constexpr uint8_t kPal[16][3] = {{96, 112, 72},   {72, 72, 78},    {232, 232, 224}, {52, 96, 220},
+                                 {140, 184, 232}, {160, 160, 152}, {224, 72, 64},   {168, 144, 120},
+                                 {255, 32, 24},   {255, 184, 0},   {32, 224, 96},   {128, 128, 128},
+                                 {128, 128, 128}, {128, 128, 128}, {128, 128, 128}, {128, 128, 128}};
+// base = palette / 255 as the correctly rounded fp32 quotient, folded at
+// compile time (the same bits a run-time IEEE division gives)
+struct PalBase {
+    float v[16][3];
+};
+constexpr PalBase make_pal_base()
+{
+    PalBase b{};
+    for (int k = 0; k < 16; ++k)
+        for (int c = 0; c < 3; ++c) b.v[k][c] = (float)kPal[k][c] / 255.0f;
+    return b;
+}
+constexpr PalBase kPalBase = make_pal_base();
+
 __device__ __forceinline__ void shade_rgb(const RenderParams& P, uint32_t key, uint32_t* c3)
 {
-    constexpr uint8_t kPal[16][3] = {{96, 112, 72},   {72, 72, 78},    {232, 232, 224}, {52, 96, 220},
-                                     {140, 184, 232}, {160, 160, 152}, {224, 72, 64},   {168, 144, 120},
-                                     {255, 32, 24},   {255, 184, 0},   {32, 224, 96},   {128, 128, 128},
-                                     {128, 128, 128}, {128, 128, 128}, {128, 128, 128}, {128, 128, 128}};
     constexpr float kFace[8] = {1.0f, 0.45f, 1.0f, 0.55f, 0.85f, 0.7f, 0.7f, 1.0f};
     const uint32_t cls = key & 15u, face = (key >> 4) & 7u;
     float f = kFace[face];
     if (face != 0u && (key >> 8) != 0xFFFFFFu) {
-        const float z = 1.0f / __uint_as_float(((P.qbase - (key >> 8)) << 3) | 4u);
+        const float z = decode_depth(P, key);
         const float t = fminf(z * P.rfar, 1.0f);
         const float b = 1.0f - 0.6f * t;
         f = f * b;
     }
 #pragma unroll
     for (int c = 0; c < 3; ++c) {
-        const float base = (float)kPal[cls][c] / 255.0f;
-        const float val = fminf(base * f, 1.0f);
+        const float val = fminf(kPalBase.v[cls][c] * f, 1.0f);
         c3[c] = (uint32_t)rintf(255.0f * val);
     }
-}
-
-__device__ __forceinline__ float decode_depth(const RenderParams& P, uint32_t key)
-{
-    const float d = __uint_as_float(((P.qbase - (key >> 8)) << 3) | 4u);
-    return P.fast_decode ? rcp_rn(d) : 1.0f / d;
 }
 
 // ---------------------------------------------------------------------------
