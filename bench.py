@@ -43,7 +43,7 @@ HBM_PEAK_GBS = 8000.0   # MI355X HBM3E peak
 # `traffic` is reported as null.
 TRAFFIC = {
     "config": 4,
-    "sources_sha256": "670fa42ee2425bb88645c67e5598a566d03114d306e4ca58b6f963e3b6f22b11",
+    "sources_sha256": "55af84c2fc2e588b5eaee94420fb0b8229d4437569527e9c4bde93475f891af8",
     "fetch_bytes": 1.1539e9,
     "write_bytes": 5368709120,
 }

@@ -70,7 +70,7 @@ enum { kTri = 0, kHalf0 = 1, kHalf1 = 2, kPair = 3 };
 constexpr int kViewWaves = PICTURA_VIEW_WAVES;   // waves per view tile
 constexpr int kThreads = 64 * kViewWaves;
 constexpr int kWavesPerSimd = 4;  // register budget: four waves per SIMD (as many as the LDS admits)
-constexpr int kSmallPx = PICTURA_SMALL_PX;   // bounding boxes of at most this many pixels are rasterized by one lane
+constexpr int kSmallPx = PICTURA_SMALL_PX;   // pieces with at most this many bounding-box pixels take the packed raster
 constexpr int kQueue = 192;       // per-wave queue of first-pass survivors
 // Framebuffer rows are padded to a pitch of 4 mod 32 words, so the 64 lanes
 // of an 8x8 block hit every LDS bank exactly twice.
