@@ -163,6 +163,15 @@ def test_aa_tiles_above_the_horizon(lib):
         check(lib, wl2, np.arange(wl2.num_views), f"aa-horizon {name} tile16", tile=16)
 
 
+def test_aa_off_grid_principal_point_anisotropic(lib):
+    # the antialiased mode with a principal point off the 1/256-pixel grid and fx != fy
+    wl = workload(2, 1)
+    rig = sg.Rig(width=64, height=48, fx=40.0, fy=29.0, cx=31.3, cy=23.7, near=0.5, far=100.0, mount=wl.rig.mount)
+    wl2 = sg.Workload(wl.name, 2, 1, wl.scene, wl.agents, rig, wl.cell_size, wl.world_size)
+    views = np.sort(np.random.default_rng(314).choice(wl2.num_views, size=48, replace=False))
+    assert check(lib, wl2, views, "aa-off-grid") > 0
+
+
 def _random_quads(seed, n=400):
     """A soup of quads given as pairs (a, b, c), (a, c, d): convex ones, darts
     (one vertex pulled past the diagonal), slivers a few millimetres wide, and

@@ -226,6 +226,18 @@ def test_tiles_above_the_horizon(lib):
         check_views(lib, wl2, np.arange(wl2.num_views), f"horizon {name} tile16", tile=16)
 
 
+def test_off_grid_principal_point_anisotropic(lib):
+    # a principal point off the 1/256-pixel grid (31.3, 23.7) and fx != fy:
+    # pixel-centre offsets are no longer exact sums, so the kernel takes its
+    # general block raster and centre arithmetic
+    wl = workload(2, 1)
+    rig = sg.Rig(width=64, height=48, fx=40.0, fy=29.0, cx=31.3, cy=23.7, near=0.5, far=100.0, mount=wl.rig.mount)
+    wl2 = sg.Workload(wl.name, 2, 1, wl.scene, wl.agents, rig, wl.cell_size, wl.world_size)
+    views = sample_views(wl2.num_views, 64, 313)
+    check_views(lib, wl2, views, "off-grid cx/cy")
+    check_views(lib, wl2, views[:24], "off-grid cx/cy tile24", tile=24)
+
+
 def test_random_quad_pairs(lib):
     # quads given as pairs (a, b, c), (a, c, d): convex, darts, slivers, near-plane
     # crossings and quads reaching far to the side, seen by four cameras
