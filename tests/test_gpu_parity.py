@@ -238,6 +238,18 @@ def test_off_grid_principal_point_anisotropic(lib):
     check_views(lib, wl2, views[:24], "off-grid cx/cy tile24", tile=24)
 
 
+def test_extreme_near_and_far(lib):
+    # far = 8 km puts 1/far below 2^-12, so the write-out decodes depths with
+    # IEEE division instead of the fast reciprocal; near = 0.01 m raises the
+    # key's cap to 128 and clips almost nothing; both against the oracle
+    wl = workload(2, 1)
+    for near, far in ((0.5, 8000.0), (0.01, 100.0)):
+        rig = sg.Rig(width=64, height=64, fx=32.0, fy=32.0, cx=32.0, cy=32.0, near=near, far=far,
+                     mount=wl.rig.mount)
+        wl2 = sg.Workload(wl.name, 2, 1, wl.scene, wl.agents, rig, wl.cell_size, wl.world_size)
+        check_views(lib, wl2, sample_views(wl2.num_views, 48, int(far)), f"near {near} far {far}")
+
+
 def test_random_quad_pairs(lib):
     # quads given as pairs (a, b, c), (a, c, d): convex, darts, slivers, near-plane
     # crossings and quads reaching far to the side, seen by four cameras
