@@ -225,6 +225,56 @@ def test_pair_that_is_not_convex_keeps_per_triangle_fragments():
     assert np.array_equal(paired["rgb"][0], apart["rgb"][0])
 
 
+def test_pair_with_a_straight_angle_keeps_per_triangle_fragments():
+    # the triangle (d, b, c) split by a point a on its edge d-b: the 4-gon
+    # (a, b, c, d) turns by zero at a, so it is not strictly convex and no
+    # surface; its halves leave their own fragments, as in the unpaired order
+    d, bb, c = (D, _y(18.0), _z(10.0)), (D, _y(30.0), _z(50.0)), (D, _y(40.0), _z(16.0))
+    a = (D, _y(24.0), _z(30.0))   # the midpoint of d-b
+    paired = _render([[a, bb, c], [a, c, d]], [LANE, LANE])
+    apart = _render([[a, c, d], [a, bb, c]], [LANE, LANE])
+    assert (paired["cls"][0] == LANE).sum() > 100
+    assert np.array_equal(paired["rgb"][0], apart["rgb"][0])
+
+
+def test_surface_fragments_take_the_first_triangles_plane():
+    # a convex square whose first triangle (a, b, c) faces the camera at 16 m
+    # and whose second (a, c, d) tilts back to d at 48 m, in front of a wall at
+    # 30 m.  Its left edge (d-a, the second triangle's) lies at column 19.75:
+    # pixel 19 is a quarter covered and its centre shows the wall.  The
+    # fragment's depth comes from the first triangle's plane (16 m at that
+    # centre), nearer than the wall, so every row of the edge blends; the
+    # second triangle's plane would put the lower rows behind the wall.
+    a = (D, _y(19.75), _z(20.0))
+    b = (D, _y(40.0), _z(20.0))
+    c = (D, _y(40.0), _z(40.0))
+    d = (48.0, 0.75 * (32.0 - 19.75), 0.75 * (32.0 - 40.0))   # projects to (19.75, 40)
+    W = 30.0
+    wall = quad((W, 60.0, -60.0), (W, -60.0, -60.0), (W, -60.0, 60.0), (W, 60.0, 60.0))
+    o = _render([[a, b, c], [a, c, d]] + wall, [LANE, LANE, WALL, WALL])
+    cls = o["cls"][0]
+    # column 19's centres show the wall; in column 20 the square's lower rows
+    # (its second triangle, past 30 m) are behind the wall as well
+    assert (cls[21:40, 19] == WALL).all() and (cls[21:30, 20] == LANE).all() and (cls[36:40, 20] == WALL).all()
+    want = _blend(PAL[LANE], PAL[WALL], 64)   # a quarter: a8 = rint(255 / 4) = 64
+    got = [tuple(int(v) for v in o["rgb"][0][:, j, 19]) for j in range(21, 40)]
+    assert all(g == want for g in got), got
+
+
+def test_pair_wholly_beyond_far_leaves_nothing():
+    # the far-rule pin's square one fp32 step beyond far = 110 (every covered
+    # centre's 1/z rounds to fl(1/far) and would pass the per-pixel test),
+    # given as a pair: neither half is drawn (R4), so the pair is no surface and
+    # leaves no key and no fragment in the antialiased mode either
+    from tests.test_oracle_pins import ego, fronto_quad
+    far = 110.0
+    Dz = float(np.nextafter(np.float32(far), np.float32(np.inf)))
+    r = O.render(make_scene(fronto_quad(Dz, 16.0), [WALL, WALL]), make_agents([ego()]), make_rig(far=far),
+                 view_ids=[0], want_rgb=True, antialias=True)
+    assert (r["cls"][0] == SKY).all()
+    assert (r["rgb"][0] == np.asarray(PAL[SKY], np.uint8)[:, None, None]).all()
+
+
 def _coverage(poly, px, py):
     """R14 coverage of a positively oriented convex polygon (snapped
     subpixel vertices) at pixel centres (px, py) in subpixels, in float64."""
