@@ -225,12 +225,31 @@ def test_pair_that_is_not_convex_keeps_per_triangle_fragments():
     assert np.array_equal(paired["rgb"][0], apart["rgb"][0])
 
 
+def _straight_angle():
+    """The triangle (d, b, c) split by the midpoint a of its edge d-b, as the
+    pair (a, b, c), (a, c, d)."""
+    d, b, c = (D, _y(18.0), _z(10.0)), (D, _y(30.0), _z(50.0)), (D, _y(40.0), _z(16.0))
+    return (D, _y(24.0), _z(30.0)), b, c, d
+
+
+def _folded_before_wall():
+    """A convex square (a, b, c), (a, c, d): the first triangle at 16 m facing
+    the camera, the second tilting back to d at 48 m; a wall at 30 m behind.
+    The left edge (d-a) projects to column 19.75, rows 20 .. 40."""
+    a = (D, _y(19.75), _z(20.0))
+    b = (D, _y(40.0), _z(20.0))
+    c = (D, _y(40.0), _z(40.0))
+    d = (48.0, 0.75 * (32.0 - 19.75), 0.75 * (32.0 - 40.0))   # projects to (19.75, 40)
+    W = 30.0
+    wall = quad((W, 60.0, -60.0), (W, -60.0, -60.0), (W, -60.0, 60.0), (W, 60.0, 60.0))
+    return [[a, b, c], [a, c, d]] + wall, [LANE, LANE, WALL, WALL]
+
+
 def test_pair_with_a_straight_angle_keeps_per_triangle_fragments():
     # the triangle (d, b, c) split by a point a on its edge d-b: the 4-gon
     # (a, b, c, d) turns by zero at a, so it is not strictly convex and no
     # surface; its halves leave their own fragments, as in the unpaired order
-    d, bb, c = (D, _y(18.0), _z(10.0)), (D, _y(30.0), _z(50.0)), (D, _y(40.0), _z(16.0))
-    a = (D, _y(24.0), _z(30.0))   # the midpoint of d-b
+    a, bb, c, d = _straight_angle()
     paired = _render([[a, bb, c], [a, c, d]], [LANE, LANE])
     apart = _render([[a, c, d], [a, bb, c]], [LANE, LANE])
     assert (paired["cls"][0] == LANE).sum() > 100
@@ -245,13 +264,7 @@ def test_surface_fragments_take_the_first_triangles_plane():
     # fragment's depth comes from the first triangle's plane (16 m at that
     # centre), nearer than the wall, so every row of the edge blends; the
     # second triangle's plane would put the lower rows behind the wall.
-    a = (D, _y(19.75), _z(20.0))
-    b = (D, _y(40.0), _z(20.0))
-    c = (D, _y(40.0), _z(40.0))
-    d = (48.0, 0.75 * (32.0 - 19.75), 0.75 * (32.0 - 40.0))   # projects to (19.75, 40)
-    W = 30.0
-    wall = quad((W, 60.0, -60.0), (W, -60.0, -60.0), (W, -60.0, 60.0), (W, 60.0, 60.0))
-    o = _render([[a, b, c], [a, c, d]] + wall, [LANE, LANE, WALL, WALL])
+    o = _render(*_folded_before_wall())
     cls = o["cls"][0]
     # column 19's centres show the wall; in column 20 the square's lower rows
     # (its second triangle, past 30 m) are behind the wall as well

@@ -79,6 +79,7 @@ def test_aa_pin_scenes_bit_exact(lib):
     left = quad((16.0, pins._y(-400.0), pins._z(300.0)), (16.0, pins._y(10.75), pins._z(300.0)),
                 (16.0, pins._y(10.75), pins._z(-200.0)), (16.0, pins._y(-400.0), pins._z(-200.0)))
     da, db, dc, dd = pins._dart()
+    sa, sb, sc, sd = pins._straight_angle()
     scenes = {
         "edge": (pins._wall(10.75), [7, 7]),
         "sliver": (pins._sliver(pins.XL, pins.XR, pins.XB), [2]),
@@ -90,6 +91,8 @@ def test_aa_pin_scenes_bit_exact(lib):
         "split-wide-strip": (pins._strip(20.25, 22.5), [2, 2]),
         "dart": ([[da, db, dc], [da, dc, dd]], [2, 2]),
         "unsnappable-vertex": (pin_scenes._pair_with_unsnappable_vertex()[0], [7, 7]),
+        "straight-angle": ([[sa, sb, sc], [sa, sc, sd]], [2, 2]),
+        "folded-before-wall": pins._folded_before_wall(),
     }
     for name, (tris, cls) in scenes.items():
         sc = make_scene(np.asarray(tris, np.float32), cls)
@@ -99,6 +102,15 @@ def test_aa_pin_scenes_bit_exact(lib):
             print(f"[aa-pin {name} tile={tile}]", flush=True)
             assert np.array_equal(c.cpu().numpy(), ora["cls"]), name
             assert np.array_equal(rgb.cpu().numpy(), ora["rgb"]), (name, tile)
+    # the far-rule square, as a pair, one fp32 step beyond far = 110: nothing
+    far = 110.0
+    sq = pin_scenes.fronto_quad(float(np.nextafter(np.float32(far), np.float32(np.inf))), 16.0)
+    sc = make_scene(np.asarray(sq, np.float32), [7, 7])
+    rig_far = make_rig(far=far)
+    ora = O.render(sc, ag, rig_far, view_ids=[0], want_rgb=True, antialias=True)
+    c, d, rgb = gpu_render(lib, sc, 64.0, ag, rig_far)
+    assert (ora["cls"] == 4).all()
+    assert np.array_equal(c.cpu().numpy(), ora["cls"]) and np.array_equal(rgb.cpu().numpy(), ora["rgb"])
 
 
 def test_aa_tiny_all_views(lib):
