@@ -288,6 +288,31 @@ def test_pair_wholly_beyond_far_leaves_nothing():
     assert (r["rgb"][0] == np.asarray(PAL[SKY], np.uint8)[:, None, None]).all()
 
 
+def _clipped_band():
+    """A triangle 2 mm below the camera with v0 behind it, and the points where
+    the near plane (0.5 m) cuts its edges v0-v1 and v2-v0 (their midpoints)."""
+    z = -0.002
+    return ((-0.5, 0.0, z), (1.5, 1.0, z), (1.5, -1.0, z)), ((0.5, 0.5, z), (0.5, -0.5, z))
+
+
+def test_near_clipped_triangle_is_one_surface():
+    # a triangle 2 mm below the camera with one vertex behind it: the near
+    # plane (0.5 m) cuts its two edges at their midpoints (t = 1/2, exact), so
+    # the clipped 4-gon (c01, v1, v2, c20) is known exactly.  It is a band a
+    # tenth to a quarter of a pixel tall across row 32, crossed lengthwise by
+    # the fan diagonal.  As one surface (R14) it blends exactly like the same
+    # 4-gon given as an unclipped pair (a, b, c), (a, c, d), whose surface the
+    # split-strip pin fixes; per-piece fragments would lose the coverage the
+    # diagonal splits.
+    (v0, v1, v2), (c01, c20) = _clipped_band()
+    clipped = _render([[v0, v1, v2]], [LANE])
+    pair = _render([[c01, v1, v2], [c01, v2, c20]], [LANE, LANE])
+    assert (clipped["cls"][0] == SKY).all()
+    band = clipped["rgb"][0][:, 32, :]
+    assert (band != np.asarray(PAL[SKY], np.uint8)[:, None]).any(0).sum() > 50
+    assert np.array_equal(clipped["rgb"][0], pair["rgb"][0])
+
+
 def _coverage(poly, px, py):
     """R14 coverage of a positively oriented convex polygon (snapped
     subpixel vertices) at pixel centres (px, py) in subpixels, in float64."""

@@ -93,6 +93,7 @@ def test_aa_pin_scenes_bit_exact(lib):
         "unsnappable-vertex": (pin_scenes._pair_with_unsnappable_vertex()[0], [7, 7]),
         "straight-angle": ([[sa, sb, sc], [sa, sc, sd]], [2, 2]),
         "folded-before-wall": pins._folded_before_wall(),
+        "clipped-band": ([list(pins._clipped_band()[0])], [2]),
     }
     for name, (tris, cls) in scenes.items():
         sc = make_scene(np.asarray(tris, np.float32), cls)
