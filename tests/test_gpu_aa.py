@@ -94,6 +94,9 @@ def test_aa_pin_scenes_bit_exact(lib):
         "straight-angle": ([[sa, sb, sc], [sa, sc, sd]], [2, 2]),
         "folded-before-wall": pins._folded_before_wall(),
         "clipped-band": ([list(pins._clipped_band()[0])], [2]),
+        "vertex-inside-snap-range": ([pin_scenes._pair_with_unsnappable_vertex()[0][0],
+                                      pin_scenes._pair_with_unsnappable_vertex()[0][1][:2] + [(0.5625, 13000.0, 0.0)]],
+                                     [7, 7]),
     }
     for name, (tris, cls) in scenes.items():
         sc = make_scene(np.asarray(tris, np.float32), cls)

@@ -192,6 +192,25 @@ def test_vertex_out_of_snap_range_drops_only_its_triangles():
     assert ((r["cls"][0] == 7) != (rc == 7)).sum() <= 40   # only on the triangle's edges
 
 
+def test_vertex_inside_snap_range_is_kept():
+    # the same pair with d at 13 km to the side projects 64 * 13000 / 0.5625 ~
+    # 1.48e6 px from the centre: past 2^20 px but within R5's 2^21 px (2^29
+    # subpixels), so both triangles are drawn, as the float64 ray cast of the
+    # whole pair confirms pixel for pixel
+    pair, first = _pair_with_unsnappable_vertex()
+    d = (0.5625, 13000.0, 0.0)
+    assert 2.0 ** 20 < 64.0 * 13000.0 / 0.5625 < 2.0 ** 21
+    pair = [pair[0], [pair[1][0], pair[1][1], d]]
+    ag = make_agents([ego()])
+    rig = make_rig(res=64, f=64.0)
+    sc = make_scene(np.asarray(pair, np.float32), [7, 7])
+    r = O.render(sc, ag, rig)
+    r1 = O.render(make_scene(np.asarray([first], np.float32), [7]), ag, rig)
+    rc, _, _ = raycast_view(sc, ag, rig, 0)
+    assert (r["cls"][0] == 7).sum() > 2 * (r1["cls"][0] == 7).sum()
+    assert ((r["cls"][0] == 7) != (rc == 7)).sum() == 0
+
+
 def test_depth_error_bound_over_distances():
     # Fronto squares (half-size D/16, 2 px) at 200 seeded distances D in [0.6, 95] m: the decoded depth
     # at the image centre is within 2^-21 (the bucket midpoint) plus a few
