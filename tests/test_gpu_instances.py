@@ -142,6 +142,26 @@ def test_instances_faces_behind_near_or_beyond_far(lib):
     assert (ora["counts"][:, 3, 0] == 0).all()                         # car 3 never is
 
 
+def test_instances_same_class_overlap_and_ties(lib):
+    # Two vehicles overlap in view with the farther one listed first: only the
+    # full depth key, not the class, names the nearer box as the owner.  Two
+    # identical boxes elsewhere tie, and the lower index takes the pixels.
+    from tests.scenes import make_agents, make_rig, make_scene, quad
+    G = 1000.0
+    scene = make_scene(quad((-G, -G, -0.75), (G, -G, -0.75), (G, G, -0.75), (-G, G, -0.75)), [0, 0])
+    ag = make_agents([(0.0, 0.0, 0.0, 1.0, 0.0, 4.5, 1.9, 1.5, 3),
+                      (18.0, -0.6, -0.75, 1.0, 0.0, 4.5, 1.9, 2.5, 3),
+                      (10.0, 0.8, -0.75, 1.0, 0.0, 4.5, 1.9, 1.5, 3),
+                      (12.0, -6.0, -0.75, 0.8, 0.6, 4.5, 1.9, 1.5, 3),
+                      (12.0, -6.0, -0.75, 0.8, 0.6, 4.5, 1.9, 1.5, 3)])
+    rig = make_rig(res=96, mounts=((0.0, 0.0, 0.0, 1.0, 0.0), (0.0, 0.0, 0.0, 0.0, -1.0)))
+    wl = sg.Workload("inst-same-class", 0, 0, scene, ag, rig, 16.0, 2000.0)
+    check(lib, wl, np.arange(wl.num_views), "inst-same-class")
+    c = O.render(scene, ag, rig, view_ids=[0], want_instances=True)["counts"][0]
+    assert c[2, 0] == c[2, 1] > 0 and 0 < c[1, 1] < c[1, 0]
+    assert c[3, 0] == c[4, 0] == c[3, 1] > 0 and c[4, 1] == 0
+
+
 def test_instances_largest_view(lib):
     # owners and counts on the largest view the ABI accepts, 4096 x 4096
     # (4,096 tiles per view), two whole images against the oracle

@@ -61,6 +61,21 @@ def test_nearer_box_wins_and_counts_partition_the_vehicle_pixels():
     assert 0 < c[2, 1] < c[2, 0]         # the farther one is partly hidden
 
 
+def test_nearer_box_owns_the_overlap_whatever_its_index():
+    # the same two boxes with the farther one listed first: both have the vehicle class, so only the
+    # full depth key (not the class alone) tells which one the visible surface belongs to
+    ag = _agents([EGO, (18.0, -0.6, -0.75, 1.0, 0.0, 4.5, 1.9, 2.5), (10.0, 0.8, -0.75, 1.0, 0.0, 4.5, 1.9, 1.5)])
+    o = O.render(_empty(), ag, make_rig(), view_ids=[0], want_instances=True)
+    veh = o["cls"][0] == VEH
+    c = o["counts"][0]
+    assert c[1, 1] + c[2, 1] == veh.sum()
+    assert c[2, 0] == c[2, 1]            # the nearer box, though listed second, keeps all of its pixels
+    assert 0 < c[1, 1] < c[1, 0]
+    alone = O.render(_empty(), _agents([EGO, (10.0, 0.8, -0.75, 1.0, 0.0, 4.5, 1.9, 1.5)]), make_rig(),
+                     view_ids=[0], want_instances=True)
+    assert np.array_equal(o["inst"][0] == 2, alone["inst"][0] == 1)
+
+
 def test_identical_boxes_tie_to_the_lower_index():
     box = (12.0, 0.5, -0.75, 1.0, 0.0, 4.5, 1.9, 1.5)
     o = O.render(_empty(), _agents([EGO, box, box]), make_rig(), view_ids=[0], want_instances=True)
