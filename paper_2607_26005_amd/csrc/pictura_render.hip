@@ -383,10 +383,11 @@ __device__ __forceinline__ void load_prim(const RenderParams& P, uint32_t p, flo
 
 // The world-space polygon of a queue entry: a triangle in tri[0..8], or for a
 // whole pair the 4-gon (a, b, c, d) in tri[0..11] (returns true).
+template <bool kHasLights>
 __device__ __forceinline__ bool load_entry(const RenderParams& P, uint32_t e, int64_t abase_w, int64_t lbase_w,
                                            float* tri, uint32_t& cls)
 {
-    if ((e & kLightFlag) == kLightFlag) {
+    if (kHasLights && (e & kLightFlag) == kLightFlag) {
         load_light(P, lbase_w + ((e & ~kLightFlag) >> 4), (int)(e & 15u), tri, cls);
         return false;
     }
@@ -1090,7 +1091,7 @@ __device__ void aa_pieces(const RenderParams& P, Shared& S, WaveLds& L, uint32_t
     }
 }
 
-template <bool kAA>
+template <bool kAA, bool kHasLights>
 __device__ __forceinline__ void exact_pass(const RenderParams& P, Shared& S, WaveLds& L, const Tile& T, const Cam& cam,
                                            bool live, uint32_t entry, int64_t abase_w, int64_t lbase_w, float pxl,
                                            float pyl, int loff4, uint32_t* fbo)
@@ -1102,7 +1103,7 @@ __device__ __forceinline__ void exact_pass(const RenderParams& P, Shared& S, Wav
     bool snap0 = true, snap1 = true;   // a whole pair's halves: every vertex snapped
     int X0 = 0, Y0 = 0, X1 = 0, Y1 = 0, X2 = 0, Y2 = 0, X3 = 0, Y3 = 0;
     if (live) {
-        quad = load_entry(P, entry, abase_w, lbase_w, tri, cls);
+        quad = load_entry<kHasLights>(P, entry, abase_w, lbase_w, tri, cls);
         float xv[3], yv[3], zv[3];
 #pragma unroll
         for (int k = 0; k < 3; ++k) view_xform(cam, tri[3 * k], tri[3 * k + 1], tri[3 * k + 2], xv[k], yv[k], zv[k]);
@@ -1613,15 +1614,30 @@ __device__ void draw_box_instances(const RenderParams& P, Shared& S, const Tile&
 // culling off are read at run time; otherwise the counter pointer is a
 // constant null and culling constantly on, so every counting site and the
 // unculled paths fold away (and so does the colour code outside modes 2 and 3).
-template <int kMode, bool kDebug>
+// kWhole64: every view is one 64x64 tile with exact pixel-centre offsets,
+// 16-byte aligned outputs and depths the fast reciprocal decodes, and there
+// are no traffic lights (the launcher checks all of it).  The tile's geometry
+// is then known at compile time, and the paths of other tile shapes, of the
+// IEEE decode and of the lights fold away.
+template <int kMode, bool kDebug, bool kWhole64 = false>
 __global__ __launch_bounds__(kThreads, kWavesPerSimd)
 void render_views_kernel(const RenderParams P_)
 {
     constexpr bool kInst = kMode == 1, kAA = kMode == 2;
+    constexpr bool kHasLights = !kWhole64;
     RenderParams P = P_;
     if constexpr (!kDebug) {
         P.stats = nullptr;
         P.cull = 1;
+    }
+    if constexpr (kWhole64) {
+        P.W = 64; P.H = 64;
+        P.tile_w = 64; P.tile_h = 64; P.tiles_x = 1; P.tiles_y = 1;
+        P.div_tiles = Div31{0u, 0u};
+        P.pix_exact = 1;
+        P.vec_out = 1;
+        P.fast_decode = 1;
+        P.L = 0;
     }
     if constexpr (kMode == 0 || kMode == 1) P.out_rgb = nullptr;
     __shared__ Shared S;
@@ -1833,7 +1849,8 @@ void render_views_kernel(const RenderParams P_)
             s0 = 0;
             __builtin_amdgcn_wave_barrier();
         }
-        while (phase == kLights && s0 >= total) {
+        if (!kHasLights && phase == kLights) phase = kDone;
+        while (kHasLights && phase == kLights && s0 >= total) {
             // traffic lights whose visibility cone holds the camera (R10)
             if (achunk * 64 * kViewWaves >= P.L) { phase = kDone; break; }
             const int li = (achunk * 64 + lane) * kViewWaves + wid;
@@ -1908,7 +1925,7 @@ void render_views_kernel(const RenderParams P_)
             const uint32_t vi = (slot * 43691u) >> 19;
             const uint32_t face = slot - 12u * vi;
             const uint32_t ai = (uint32_t)__shfl((int)my_start, (int)min(vi, 63u));
-            const bool boxes = phase == kBoxes;
+            const bool boxes = !kHasLights || phase == kBoxes;
             const uint32_t entry = (boxes ? kBoxFlag : kLightFlag) | (ai << 4) | face;
             if (slot < total) {
                 if (boxes) load_box(P, abase_w + ai, (int)face, tri, cls);
@@ -1930,7 +1947,7 @@ void render_views_kernel(const RenderParams P_)
             __builtin_amdgcn_wave_barrier();
             STAT1(kStExact, 1);
             TSTART(t_ex);
-            exact_pass<kAA>(P, S, L, T, cam, live, entry, abase_w, lbase_w, pxl, pyl, loff4, ebuf);
+            exact_pass<kAA, kHasLights>(P, S, L, T, cam, live, entry, abase_w, lbase_w, pxl, pyl, loff4, ebuf);
             TACC(kCycExact, t_ex);
         }
         if (phase == kDone && nq == 0) break;
@@ -2176,7 +2193,10 @@ void render_views_kernel(const RenderParams P_)
 // holds only the production class/depth kernel.
 hipError_t launch_render_plain(const RenderParams& p, hipStream_t s)
 {
-    hipLaunchKernelGGL((render_views_kernel<0, false>), dim3((unsigned)p.num_blocks), dim3(kThreads), 0, s, p);
+    const bool whole64 = p.W == 64 && p.H == 64 && p.tile_w == 64 && p.tile_h == 64 && p.pix_exact && p.vec_out &&
+                         p.fast_decode && p.L == 0;
+    if (whole64) hipLaunchKernelGGL((render_views_kernel<0, false, true>), dim3((unsigned)p.num_blocks), dim3(kThreads), 0, s, p);
+    else hipLaunchKernelGGL((render_views_kernel<0, false>), dim3((unsigned)p.num_blocks), dim3(kThreads), 0, s, p);
     return hipGetLastError();
 }
 #elif defined(PICTURA_RENDER_SIDE)
