@@ -2188,23 +2188,36 @@ void render_views_kernel(const RenderParams P_)
     }
 }
 
+// The launch meets every assumption of a kWhole64 kernel.
+static bool whole64(const RenderParams& p)
+{
+    return p.W == 64 && p.H == 64 && p.tile_w == 64 && p.tile_h == 64 && p.pix_exact && p.vec_out && p.fast_decode &&
+           p.L == 0;
+}
+
 #if defined(PICTURA_RENDER_PLAIN)
 // This object (the source compiled once more, with its own scheduler setting)
-// holds only the production class/depth kernel.
+// holds only the production class/depth kernels.
 hipError_t launch_render_plain(const RenderParams& p, hipStream_t s)
 {
-    const bool whole64 = p.W == 64 && p.H == 64 && p.tile_w == 64 && p.tile_h == 64 && p.pix_exact && p.vec_out &&
-                         p.fast_decode && p.L == 0;
-    if (whole64) hipLaunchKernelGGL((render_views_kernel<0, false, true>), dim3((unsigned)p.num_blocks), dim3(kThreads), 0, s, p);
-    else hipLaunchKernelGGL((render_views_kernel<0, false>), dim3((unsigned)p.num_blocks), dim3(kThreads), 0, s, p);
+    const dim3 grid((unsigned)p.num_blocks), block(kThreads);
+    if (whole64(p)) hipLaunchKernelGGL((render_views_kernel<0, false, true>), grid, block, 0, s, p);
+    else hipLaunchKernelGGL((render_views_kernel<0, false>), grid, block, 0, s, p);
     return hipGetLastError();
 }
 #elif defined(PICTURA_RENDER_SIDE)
 // Likewise for the production instance (mode 1) and one-sample colour (mode 3) kernels.
 hipError_t launch_render_side(const RenderParams& p, int mode, hipStream_t s)
 {
-    if (mode == 1) hipLaunchKernelGGL((render_views_kernel<1, false>), dim3((unsigned)p.num_blocks), dim3(kThreads), 0, s, p);
-    else hipLaunchKernelGGL((render_views_kernel<3, false>), dim3((unsigned)p.num_blocks), dim3(kThreads), 0, s, p);
+    const dim3 grid((unsigned)p.num_blocks), block(kThreads);
+    const bool w64 = whole64(p);
+    if (mode == 1) {
+        if (w64) hipLaunchKernelGGL((render_views_kernel<1, false, true>), grid, block, 0, s, p);
+        else hipLaunchKernelGGL((render_views_kernel<1, false>), grid, block, 0, s, p);
+    } else {
+        if (w64) hipLaunchKernelGGL((render_views_kernel<3, false, true>), grid, block, 0, s, p);
+        else hipLaunchKernelGGL((render_views_kernel<3, false>), grid, block, 0, s, p);
+    }
     return hipGetLastError();
 }
 #else
@@ -2219,8 +2232,10 @@ hipError_t launch_render(const RenderParams& p, hipStream_t s)
         else if (mode == 3) hipLaunchKernelGGL((render_views_kernel<3, true>), grid, block, 0, s, p);
         else hipLaunchKernelGGL((render_views_kernel<0, true>), grid, block, 0, s, p);
     } else {
-        if (mode == 2) hipLaunchKernelGGL((render_views_kernel<2, false>), grid, block, 0, s, p);
-        else if (mode != 0) return launch_render_side(p, mode, s);
+        if (mode == 2) {
+            if (whole64(p)) hipLaunchKernelGGL((render_views_kernel<2, false, true>), grid, block, 0, s, p);
+            else hipLaunchKernelGGL((render_views_kernel<2, false>), grid, block, 0, s, p);
+        } else if (mode != 0) return launch_render_side(p, mode, s);
         else return launch_render_plain(p, s);
     }
     return hipGetLastError();
