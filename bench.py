@@ -43,8 +43,8 @@ HBM_PEAK_GBS = 8000.0   # MI355X HBM3E peak
 # `traffic` is reported as null.
 TRAFFIC = {
     "config": 4,
-    "sources_sha256": "55af84c2fc2e588b5eaee94420fb0b8229d4437569527e9c4bde93475f891af8",
-    "fetch_bytes": 1.1539e9,
+    "sources_sha256": "6b23c1b05300245804dcd24b5efd44a3360c78a5b7df3c1d9f5f4e214b9670b8",
+    "fetch_bytes": 1.1537e9,
     "write_bytes": 5368709120,
 }
 TRAFFIC_SOURCES = ["paper_2607_26005_amd/csrc/pictura_render.hip",
