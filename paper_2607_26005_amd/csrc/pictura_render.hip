@@ -1614,30 +1614,36 @@ __device__ void draw_box_instances(const RenderParams& P, Shared& S, const Tile&
 // culling off are read at run time; otherwise the counter pointer is a
 // constant null and culling constantly on, so every counting site and the
 // unculled paths fold away (and so does the colour code outside modes 2 and 3).
-// kWhole64: every view is one 64x64 tile with exact pixel-centre offsets,
-// 16-byte aligned outputs and depths the fast reciprocal decodes, and there
-// are no traffic lights (the launcher checks all of it).  The tile's geometry
-// is then known at compile time, and the paths of other tile shapes, of the
-// IEEE decode and of the lights fold away.
-template <int kMode, bool kDebug, bool kWhole64 = false>
+// kShape (the launcher checks every condition): 0 any view; 1 every tile is
+// 64x64 (the view's width and height are multiples of 64), with exact
+// pixel-centre offsets, 16-byte aligned outputs and depths the fast
+// reciprocal decodes, and no traffic lights; 2 as 1, and the view is one
+// tile.  The tile's size (and with 2 its origin) is then known at compile
+// time, and the paths of other tile shapes, of the IEEE decode and of the
+// lights fold away.
+template <int kMode, bool kDebug, int kShape = 0>
 __global__ __launch_bounds__(kThreads, kWavesPerSimd)
 void render_views_kernel(const RenderParams P_)
 {
     constexpr bool kInst = kMode == 1, kAA = kMode == 2;
-    constexpr bool kHasLights = !kWhole64;
+    constexpr bool kTile64 = kShape >= 1;
+    constexpr bool kHasLights = !kTile64;
     RenderParams P = P_;
     if constexpr (!kDebug) {
         P.stats = nullptr;
         P.cull = 1;
     }
-    if constexpr (kWhole64) {
-        P.W = 64; P.H = 64;
-        P.tile_w = 64; P.tile_h = 64; P.tiles_x = 1; P.tiles_y = 1;
-        P.div_tiles = Div31{0u, 0u};
+    if constexpr (kTile64) {
+        P.tile_w = 64; P.tile_h = 64;
         P.pix_exact = 1;
         P.vec_out = 1;
         P.fast_decode = 1;
         P.L = 0;
+    }
+    if constexpr (kShape == 2) {
+        P.W = 64; P.H = 64;
+        P.tiles_x = 1; P.tiles_y = 1;
+        P.div_tiles = Div31{0u, 0u};
     }
     if constexpr (kMode == 0 || kMode == 1) P.out_rgb = nullptr;
     __shared__ Shared S;
@@ -1673,6 +1679,10 @@ void render_views_kernel(const RenderParams P_)
     T.y0 = (tile / P.tiles_x) * P.tile_h;
     T.w = min(P.tile_w, P.W - T.x0);
     T.h = min(P.tile_h, P.H - T.y0);
+    if constexpr (kTile64) {   // the view is a whole number of tiles
+        T.w = 64;
+        T.h = 64;
+    }
     T.pitch = ((T.w + 31) & ~31) + 4;
     // culling reaches the pixel centres of the tile, and with antialiasing the
     // centres within half a pixel more, where a surface's edge fragments land
@@ -2188,11 +2198,13 @@ void render_views_kernel(const RenderParams P_)
     }
 }
 
-// The launch meets every assumption of a kWhole64 kernel.
-static bool whole64(const RenderParams& p)
+// The most specialised kShape whose assumptions the launch meets.
+static int shape_of(const RenderParams& p)
 {
-    return p.W == 64 && p.H == 64 && p.tile_w == 64 && p.tile_h == 64 && p.pix_exact && p.vec_out && p.fast_decode &&
-           p.L == 0;
+    if (!(p.tile_w == 64 && p.tile_h == 64 && p.W % 64 == 0 && p.H % 64 == 0 && p.pix_exact && p.vec_out &&
+          p.fast_decode && p.L == 0))
+        return 0;
+    return p.W == 64 && p.H == 64 ? 2 : 1;
 }
 
 #if defined(PICTURA_RENDER_PLAIN)
@@ -2201,8 +2213,11 @@ static bool whole64(const RenderParams& p)
 hipError_t launch_render_plain(const RenderParams& p, hipStream_t s)
 {
     const dim3 grid((unsigned)p.num_blocks), block(kThreads);
-    if (whole64(p)) hipLaunchKernelGGL((render_views_kernel<0, false, true>), grid, block, 0, s, p);
-    else hipLaunchKernelGGL((render_views_kernel<0, false>), grid, block, 0, s, p);
+    switch (shape_of(p)) {
+    case 2: hipLaunchKernelGGL((render_views_kernel<0, false, 2>), grid, block, 0, s, p); break;
+    case 1: hipLaunchKernelGGL((render_views_kernel<0, false, 1>), grid, block, 0, s, p); break;
+    default: hipLaunchKernelGGL((render_views_kernel<0, false>), grid, block, 0, s, p); break;
+    }
     return hipGetLastError();
 }
 #elif defined(PICTURA_RENDER_SIDE)
@@ -2210,12 +2225,14 @@ hipError_t launch_render_plain(const RenderParams& p, hipStream_t s)
 hipError_t launch_render_side(const RenderParams& p, int mode, hipStream_t s)
 {
     const dim3 grid((unsigned)p.num_blocks), block(kThreads);
-    const bool w64 = whole64(p);
+    const int shape = shape_of(p);
     if (mode == 1) {
-        if (w64) hipLaunchKernelGGL((render_views_kernel<1, false, true>), grid, block, 0, s, p);
+        if (shape == 2) hipLaunchKernelGGL((render_views_kernel<1, false, 2>), grid, block, 0, s, p);
+        else if (shape == 1) hipLaunchKernelGGL((render_views_kernel<1, false, 1>), grid, block, 0, s, p);
         else hipLaunchKernelGGL((render_views_kernel<1, false>), grid, block, 0, s, p);
     } else {
-        if (w64) hipLaunchKernelGGL((render_views_kernel<3, false, true>), grid, block, 0, s, p);
+        if (shape == 2) hipLaunchKernelGGL((render_views_kernel<3, false, 2>), grid, block, 0, s, p);
+        else if (shape == 1) hipLaunchKernelGGL((render_views_kernel<3, false, 1>), grid, block, 0, s, p);
         else hipLaunchKernelGGL((render_views_kernel<3, false>), grid, block, 0, s, p);
     }
     return hipGetLastError();
@@ -2233,7 +2250,9 @@ hipError_t launch_render(const RenderParams& p, hipStream_t s)
         else hipLaunchKernelGGL((render_views_kernel<0, true>), grid, block, 0, s, p);
     } else {
         if (mode == 2) {
-            if (whole64(p)) hipLaunchKernelGGL((render_views_kernel<2, false, true>), grid, block, 0, s, p);
+            const int shape = shape_of(p);
+            if (shape == 2) hipLaunchKernelGGL((render_views_kernel<2, false, 2>), grid, block, 0, s, p);
+            else if (shape == 1) hipLaunchKernelGGL((render_views_kernel<2, false, 1>), grid, block, 0, s, p);
             else hipLaunchKernelGGL((render_views_kernel<2, false>), grid, block, 0, s, p);
         } else if (mode != 0) return launch_render_side(p, mode, s);
         else return launch_render_plain(p, s);
