@@ -30,6 +30,12 @@
  *  - Work is enqueued on `stream` and the calls return without synchronising,
  *    except where a call says it copies to host memory.
  *  - A context is not thread-safe: use one context per host thread.
+ *  - Every render call first copies the agents into a context-owned device
+ *    buffer in the layout its kernels read (48 bytes per agent), so a render
+ *    call on another stream than the previous render call of the context is
+ *    ordered after that call's kernels (an event wait on the device, not a
+ *    host synchronisation).  A call with more agents than any before it grows
+ *    the buffer, which synchronises the device once.
  */
 #ifndef PICTURA_H
 #define PICTURA_H

@@ -56,6 +56,14 @@ struct pictura_ctx_s {
     // traffic lights (caller-owned device arrays; lights.lights_per_world == 0: none)
     pictura_lights lights{};
     uint32_t* dev_err = nullptr;   // device error word (pictura_device_errors), allocated by pictura_create
+    // the agents of the latest render call, packed for the kernels (RenderParams::apk), grown on demand
+    float4* apk = nullptr;
+    size_t apk_cap = 0;   // bytes
+    // render calls share apk: each records apk_event after its kernels, and one
+    // on another stream than the last waits for that event first
+    hipEvent_t apk_event = nullptr;
+    hipStream_t apk_stream = nullptr;
+    bool apk_used = false;
 };
 
 namespace {
@@ -198,6 +206,8 @@ void pictura_destroy(pictura_ctx c)
         (void)hipDeviceSynchronize();
         free_scene(c);
         dfree(c->dev_err);
+        dfree(c->apk);
+        if (c->apk_event) (void)hipEventDestroy(c->apk_event);
     }
     delete c;
 }
@@ -432,6 +442,27 @@ static pictura_status render_setup(pictura_ctx c, const pictura_agents* ag, cons
         P.L = l.lights_per_world;
         P.lcos2 = l.cos_max * l.cos_max;
     }
+    {
+        // the packed agents (written by every render call before its kernels)
+        const size_t need = (size_t)c->num_worlds * (size_t)P.A * 3u * sizeof(float4);
+        hipError_t ae = hipSuccess;
+        if (need > c->apk_cap) {
+            if (c->apk && (ae = hipDeviceSynchronize()) != hipSuccess)   // a render may still read the old one
+                return hip_fail(c, ae, "render_views sync");
+            dfree(c->apk);
+            c->apk_cap = 0;
+            if ((ae = hipMalloc((void**)&c->apk, need)) != hipSuccess) {
+                c->apk = nullptr;
+                return hip_fail(c, ae, "render_views agents alloc");
+            }
+            c->apk_cap = need;
+        }
+        if (!c->apk_event && (ae = hipEventCreateWithFlags(&c->apk_event, hipEventDisableTiming)) != hipSuccess) {
+            c->apk_event = nullptr;
+            return hip_fail(c, ae, "render_views event");
+        }
+        P.apk = c->apk;
+    }
     if (c->stats_on) {
         hipError_t se = hipSuccess;
         if (!c->stats) {
@@ -444,6 +475,21 @@ static pictura_status render_setup(pictura_ctx c, const pictura_agents* ag, cons
     return PICTURA_OK;
 }
 
+// Launch a render set up by render_setup on stream s: pack the agents, then
+// the render kernel.  A call on another stream than the previous render call
+// first waits for that call's kernels, which read the same packed agents.
+static hipError_t render_launch(pictura_ctx c, const RenderParams& P, hipStream_t s)
+{
+    hipError_t e = hipSuccess;
+    if (c->apk_used && c->apk_stream != s && (e = hipStreamWaitEvent(s, c->apk_event, 0)) != hipSuccess) return e;
+    if ((e = launch_pack_agents(P, (int64_t)c->num_worlds * P.A, s)) != hipSuccess) return e;
+    if ((e = launch_render(P, s)) != hipSuccess) return e;
+    if ((e = hipEventRecord(c->apk_event, s)) != hipSuccess) return e;
+    c->apk_stream = s;
+    c->apk_used = true;
+    return hipSuccess;
+}
+
 pictura_status pictura_render_views(pictura_ctx c, const pictura_agents* ag, const pictura_rig* rig,
                                     uint8_t* out_cls, float* out_depth, void* stream)
 {
@@ -454,7 +500,7 @@ pictura_status pictura_render_views(pictura_ctx c, const pictura_agents* ag, con
     bool empty = false;
     const pictura_status st = render_setup(c, ag, rig, out_cls, out_depth, P, &empty);
     if (st != PICTURA_OK || empty) return st;
-    hipError_t e = launch_render(P, (hipStream_t)stream);
+    hipError_t e = render_launch(c, P, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(c, e, "render_views launch");
     return PICTURA_OK;
 }
@@ -474,7 +520,7 @@ static pictura_status render_rgb(pictura_ctx c, const pictura_agents* ag, const 
     P.out_rgb = out_rgb;
     P.rfar = 1.0f / P.farp;
     P.aa = aa ? 1 : 0;
-    hipError_t e = launch_render(P, (hipStream_t)stream);
+    hipError_t e = render_launch(c, P, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(c, e, "render_rgb launch");
     return PICTURA_OK;
 }
@@ -507,7 +553,7 @@ pictura_status pictura_render_instances(pictura_ctx c, const pictura_agents* ag,
     P.out_counts = out_counts;
     hipError_t e = launch_fill_u32(out_counts, (size_t)P.num_views * (size_t)P.A * 2u, 0u, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(c, e, "render_instances clear");
-    e = launch_render(P, (hipStream_t)stream);
+    e = render_launch(c, P, (hipStream_t)stream);
     if (e != hipSuccess) return hip_fail(c, e, "render_instances launch");
     return PICTURA_OK;
 }

@@ -234,6 +234,23 @@ hipError_t launch_agents_step(const AgentStepParams& p, hipStream_t s)
     return hipGetLastError();
 }
 
+// The agents of a render call in the render kernels' layout (RenderParams::apk).
+__global__ void pack_agents_kernel(const RenderParams p, int64_t count)
+{
+    const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+    if (i >= count) return;
+    p.apk[3 * i] = make_float4(p.ax[i], p.ay[i], p.az0[i], p.ah[i]);
+    p.apk[3 * i + 1] = make_float4(p.ac[i], p.as[i], p.al[i], p.aw[i]);
+    p.apk[3 * i + 2] = make_float4(__uint_as_float((uint32_t)p.acls[i]), 0.0f, 0.0f, 0.0f);
+}
+
+hipError_t launch_pack_agents(const RenderParams& p, int64_t count, hipStream_t s)
+{
+    if (count <= 0) return hipSuccess;
+    hipLaunchKernelGGL(pack_agents_kernel, dim3((unsigned)((count + 255) / 256)), dim3(256), 0, s, p, count);
+    return hipGetLastError();
+}
+
 // ---------------------------------------------------------------------------
 // streaming-store reference: zeros written with 16-byte non-temporal stores,
 // the store pattern of the render's write-out, at whatever rate HBM accepts

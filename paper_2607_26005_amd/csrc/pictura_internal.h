@@ -102,6 +102,11 @@ struct RenderParams {
     int32_t L;
     float lcos2;        // cos_max * cos_max (fp32)
     uint32_t* dev_err;  // context-owned device word: bits of kDevErr* OR-ed in by the kernels
+    // the agents as the render kernels read them (pack_agents_kernel, run by
+    // every render call first): agent g = w * A + a is apk[3g] = (x, y, z0,
+    // height), apk[3g + 1] = (cos h, sin h, length, width), apk[3g + 2].x =
+    // the class as bits; one pointer instead of nine keeps scalar registers free
+    float4* apk;
 };
 
 // Device error bits (pictura_device_errors)
@@ -151,6 +156,8 @@ hipError_t launch_render_plain(const RenderParams& p, hipStream_t s);
 hipError_t launch_render_side(const RenderParams& p, int mode, hipStream_t s);
 hipError_t launch_bin(const BinWork& w, hipStream_t s);
 hipError_t launch_agents_step(const AgentStepParams& p, hipStream_t s);
+// Pack the num_worlds * A agents of p's SoA arrays into p.apk.
+hipError_t launch_pack_agents(const RenderParams& p, int64_t count, hipStream_t s);
 hipError_t launch_store_probe(void* dst, uint64_t bytes, hipStream_t s);
 int64_t scan_tmp_needed(int64_t n);
 hipError_t launch_rcp_check(uint32_t lo_bits, uint32_t n, unsigned long long* mismatches, hipStream_t s);

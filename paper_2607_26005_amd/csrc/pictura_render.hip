@@ -307,8 +307,9 @@ __device__ __forceinline__ void near_cross(const RenderParams& P, float ix, floa
 // R9: triangle `face` of agent h's box.
 __device__ __forceinline__ void load_box(const RenderParams& P, int64_t h, int face, float* tri, uint32_t& cls)
 {
-    const float x = P.ax[h], y = P.ay[h], z0 = P.az0[h], c = P.ac[h], s = P.as[h];
-    const float hl = 0.5f * P.al[h], hw = 0.5f * P.aw[h], ztop = z0 + P.ah[h];
+    const float4 r0 = P.apk[3 * h], r1 = P.apk[3 * h + 1];
+    const float x = r0.x, y = r0.y, z0 = r0.z, c = r1.x, s = r1.y;
+    const float hl = 0.5f * r1.z, hw = 0.5f * r1.w, ztop = z0 + r0.w;
     // corner indices (bit 0: +L/2, bit 1: +W/2, bit 2: top) of the 12 triangles
     constexpr uint32_t kBoxTris[12] = {0x310, 0x230, 0x754, 0x674, 0x620, 0x460,
                                        0x731, 0x571, 0x510, 0x450, 0x732, 0x672};
@@ -324,7 +325,7 @@ __device__ __forceinline__ void load_box(const RenderParams& P, int64_t h, int f
         tri[3 * q + 1] = y + oy;
         tri[3 * q + 2] = (n & 4) ? ztop : z0;
     }
-    cls = (uint32_t)P.acls[h];
+    cls = __float_as_uint(P.apk[3 * h + 2].x);
     // R13: in RGB mode the shading id adds the face (1 bottom, 2 top, 3 back, 4 front, 5 right, 6 left)
     if (P.out_rgb) cls = (cls & 15u) | ((uint32_t)(face >> 1) + 1u) << 4;
 }
@@ -1662,14 +1663,15 @@ void render_views_kernel(const RenderParams P_)
     const int64_t v = (int64_t)v32, g = (int64_t)g32;
     Cam cam;
     {
-        const float c = P.ac[g], s = P.as[g];
+        const float4 q0 = P.apk[3 * g], q1 = P.apk[3 * g + 1];
+        const float c = q1.x, s = q1.y;
         const float mx = P_.mount[k][0], my = P_.mount[k][1], mz = P_.mount[k][2];
         const float cm = P_.mount[k][3], sm = P_.mount[k][4];
         const float t1 = mx * c, t2 = my * s, t3 = mx * s, t4 = my * c;
         const float ox = t1 - t2, oy = t3 + t4;
-        cam.x = P.ax[g] + ox;
-        cam.y = P.ay[g] + oy;
-        cam.z = P.az0[g] + mz;
+        cam.x = q0.x + ox;
+        cam.y = q0.y + oy;
+        cam.z = q0.z + mz;
         const float u1 = c * cm, u2 = s * sm, u3 = s * cm, u4 = c * sm;
         cam.cc = u1 - u2;
         cam.sc = u3 + u4;
@@ -1840,9 +1842,9 @@ void render_views_kernel(const RenderParams P_)
                 vis = true;
                 if (cull) {
                     const int64_t h = abase_w + ai;
-                    const float x = P.ax[h], y = P.ay[h], z0 = P.az0[h];
-                    const float R = 0.5f * (P.al[h] + P.aw[h]) * 1.0009765625f + 0.0009765625f;
-                    vis = aabb_visible(P, T, F, cam, x - R, y - R, z0, x + R, y + R, z0 + P.ah[h]);
+                    const float4 r0 = P.apk[3 * h], r1 = P.apk[3 * h + 1];
+                    const float R = 0.5f * (r1.z + r1.w) * 1.0009765625f + 0.0009765625f;
+                    vis = aabb_visible(P, T, F, cam, r0.x - R, r0.y - R, r0.z, r0.x + R, r0.y + R, r0.z + r0.w);
                 }
             }
             const uint64_t m = __ballot(vis);
@@ -2032,9 +2034,9 @@ void render_views_kernel(const RenderParams P_)
                 bool vis = ai < P.A && ai != a;
                 if (vis && cull) {
                     const int64_t h = abase_w + ai;
-                    const float x = P.ax[h], y = P.ay[h], z0 = P.az0[h];
-                    const float R = 0.5f * (P.al[h] + P.aw[h]) * 1.0009765625f + 0.0009765625f;
-                    vis = aabb_visible(P, T, F, cam, x - R, y - R, z0, x + R, y + R, z0 + P.ah[h]);
+                    const float4 r0 = P.apk[3 * h], r1 = P.apk[3 * h + 1];
+                    const float R = 0.5f * (r1.z + r1.w) * 1.0009765625f + 0.0009765625f;
+                    vis = aabb_visible(P, T, F, cam, r0.x - R, r0.y - R, r0.z, r0.x + R, r0.y + R, r0.z + r0.w);
                 }
                 uint64_t m = __ballot(vis);
                 while (m) {
