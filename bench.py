@@ -37,14 +37,14 @@ HBM_PEAK_GBS = 8000.0   # MI355X HBM3E peak
 
 # HBM bytes per launch of render_views_kernel on the headline workload, from
 # rocprofv3 FETCH_SIZE and WRITE_SIZE runs (one counter per run), each scaled
-# by what the counter reads for a plain 1 GiB device copy (FETCH_SIZE x1.99995,
+# by what the counter reads for a plain 1 GiB device copy (FETCH_SIZE x1.99994,
 # WRITE_SIZE x1.0).  The figures hold only for the kernel sources they were
 # measured on (and the workload generator); when the fingerprint differs,
 # `traffic` is reported as null.
 TRAFFIC = {
     "config": 4,
-    "sources_sha256": "6b23c1b05300245804dcd24b5efd44a3360c78a5b7df3c1d9f5f4e214b9670b8",
-    "fetch_bytes": 1.1537e9,
+    "sources_sha256": "ce5b95a6755a85da829bf98af813426b8bb31a40f46ac904d736550496f75a69",
+    "fetch_bytes": 1.1546e9,
     "write_bytes": 5368709120,
 }
 TRAFFIC_SOURCES = ["paper_2607_26005_amd/csrc/pictura_render.hip",
