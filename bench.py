@@ -43,7 +43,7 @@ HBM_PEAK_GBS = 8000.0   # MI355X HBM3E peak
 # `traffic` is reported as null.
 TRAFFIC = {
     "config": 4,
-    "sources_sha256": "ce5b95a6755a85da829bf98af813426b8bb31a40f46ac904d736550496f75a69",
+    "sources_sha256": "5ea88b326a9df7bc350c6b5ef16ea98b3c6baff4c1e50137f15d573cfa7593ec",
     "fetch_bytes": 1.1546e9,
     "write_bytes": 5368709120,
 }

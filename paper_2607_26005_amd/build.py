@@ -8,16 +8,17 @@ INCLUDE = os.path.join(os.path.dirname(HERE), "include")
 LIB = os.path.join(HERE, "libpictura.so")
 SOURCES = ["pictura_binner.hip", "pictura_render.hip", "pictura_abi.hip"]
 # (source, object name, extra flags): the render source is compiled three
-# times.  One object holds only the production class/depth kernel, scheduled by
-# LLVM's iterative ILP strategy (1.4 % faster on that kernel in A/B runs with
-# identical images), one the production instance and one-sample colour kernels
-# under the AMDGPU register trackers (about 1 % faster each); the antialiased
-# kernel spills and slows under either, so it keeps the default scheduler.
+# times.  One object holds only the production class/depth kernels, one the
+# production instance and one-sample colour kernels, both scheduled by LLVM's
+# iterative ILP strategy (1.4 % faster on the class/depth kernel, and 1.6 %
+# and 2.5 % on the tile-shape-specialised instance and colour kernels, than
+# the next best setting, in A/B runs with identical images); the antialiased
+# kernel spills and slows under it, so it keeps the default scheduler.
 UNITS = [(src, src.replace(".hip", ".o"), []) for src in SOURCES] + [
     ("pictura_render.hip", "pictura_render_plain.o",
      ["-DPICTURA_RENDER_PLAIN", "-mllvm", "-amdgpu-sched-strategy=iterative-ilp"]),
     ("pictura_render.hip", "pictura_render_side.o",
-     ["-DPICTURA_RENDER_SIDE", "-mllvm", "-amdgpu-use-amdgpu-trackers=1"]),
+     ["-DPICTURA_RENDER_SIDE", "-mllvm", "-amdgpu-sched-strategy=iterative-ilp"]),
 ]
 
 # fp32 rules need IEEE arithmetic: no contraction, correctly rounded division,
